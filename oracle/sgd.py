@@ -1,0 +1,150 @@
+"""Local minibatch SGD half-step of every worker (oracle, fp64).
+
+Appendix A, update equation (A.2), first line: each node takes a gradient step
+on its private objective f_i from its current model.  Section 5 runs that step
+as SGD over a few examples of the node's own data partition before it
+communicates; Section 6 uses an SVM trained with Bottou's SVM-SGD.
+
+Reading used here (the paper fixes no minibatch rule, no logistic loss and no
+step-size schedule; these come from the workload definitions):
+
+* f_i(w) = mean over the shard of loss(y <x, w>) + (l2 / 2) ||w||^2;
+* logistic loss = softplus(-y m), derivative c = -y sigmoid(-y m);
+  hinge loss = max(0, 1 - y m), subgradient c = -y if y m < 1 else 0
+  (zero at the kink);
+* minibatch k of round r is positions [kB, min((k+1)B, S)) of the round's
+  schedule; all margins use the pre-step model; the gradient is the batch mean
+  (1/B') sum_b c_b x_b + l2 w; the update is w <- w - eta_t g with
+  t = r * ceil(S / B) + k + 1 counted from 1 per worker across rounds, and
+  eta_t = lr0 (constant) or lr0 / sqrt(t);
+* one round = one full pass over the shard.
+
+Pins: closed forms at m = 0, central finite differences of the loss on tiny
+inputs, a hand-computed step, the dense-vs-CSR agreement on the same data.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+LOGISTIC = "logistic"
+HINGE = "hinge"
+
+
+def loss_value(margin_y: np.ndarray, loss: str) -> np.ndarray:
+    """Per-sample loss as a function of y*m (fp64)."""
+    if loss == LOGISTIC:
+        return np.logaddexp(0.0, -margin_y)
+    if loss == HINGE:
+        return np.maximum(0.0, 1.0 - margin_y)
+    raise ValueError(loss)
+
+
+def loss_coef(m: np.ndarray, y: np.ndarray, loss: str) -> np.ndarray:
+    """d loss(y m) / d m for each sample (hinge: zero at and beyond the kink)."""
+    ym = y * m
+    if loss == LOGISTIC:
+        # -y * sigmoid(-y m), written without overflow for either sign of ym.
+        e = np.exp(-np.abs(ym))
+        sig_neg = np.where(ym >= 0, e / (1.0 + e), 1.0 / (1.0 + e))
+        return -y * sig_neg
+    if loss == HINGE:
+        return np.where(ym < 1.0, -y, 0.0)
+    raise ValueError(loss)
+
+
+def step_size(lr_kind: str, lr0: float, t: int) -> float:
+    if lr_kind == "const":
+        return float(lr0)
+    if lr_kind == "inv_sqrt":
+        return float(lr0) / math.sqrt(t)
+    raise ValueError(lr_kind)
+
+
+def n_steps(S: int, B: int) -> int:
+    return -(-S // B)
+
+
+def sgd_pass_dense(w0, X, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd):
+    """One local pass of one worker on dense data; returns the new model (fp64).
+
+    w0 [D], X [S, D], y [S], sched = permutation of [0, S).
+    """
+    w = np.asarray(w0, np.float64).copy()
+    X = np.asarray(X, np.float64)
+    y = np.asarray(y, np.float64)
+    S = X.shape[0]
+    K = n_steps(S, batch)
+    for k in range(K):
+        rows = sched[k * batch:min((k + 1) * batch, S)]
+        xb, yb = X[rows], y[rows]
+        m = xb @ w
+        c = loss_coef(m, yb, loss)
+        g = (c @ xb) / len(rows) + l2 * w
+        w = w - step_size(lr_kind, lr0, rnd * K + k + 1) * g
+    return w
+
+
+def sgd_pass_csr(w0, row_ptr, col, val, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd):
+    """One local pass of one worker on CSR data (local row offsets); fp64.
+
+    The L2 term is applied densely every step, exactly as the update states.
+    """
+    w = np.asarray(w0, np.float64).copy()
+    S = len(row_ptr) - 1
+    K = n_steps(S, batch)
+    for k in range(K):
+        rows = sched[k * batch:min((k + 1) * batch, S)]
+        m = np.empty(len(rows))
+        for b, r in enumerate(rows):
+            lo, hi = row_ptr[r], row_ptr[r + 1]
+            m[b] = np.dot(val[lo:hi].astype(np.float64), w[col[lo:hi]])
+        c = loss_coef(m, y[rows].astype(np.float64), loss)
+        g = l2 * w
+        inv_b = 1.0 / len(rows)
+        for b, r in enumerate(rows):
+            lo, hi = row_ptr[r], row_ptr[r + 1]
+            np.add.at(g, col[lo:hi], c[b] * inv_b * val[lo:hi].astype(np.float64))
+        w = w - step_size(lr_kind, lr0, rnd * K + k + 1) * g
+    return w
+
+
+def objective_dense(w, X, y, loss, l2) -> float:
+    """f_i(w) on a dense shard (fp64)."""
+    m = np.asarray(X, np.float64) @ np.asarray(w, np.float64)
+    return float(np.mean(loss_value(np.asarray(y, np.float64) * m, loss))
+                 + 0.5 * l2 * np.dot(w, w))
+
+
+def margins_csr(w, row_ptr, col, val) -> np.ndarray:
+    """<x_s, w> for every row of a CSR shard (fp64, library sparse product)."""
+    import scipy.sparse as sp
+    S = len(row_ptr) - 1
+    A = sp.csr_matrix((np.asarray(val, np.float64), np.asarray(col, np.int64),
+                       np.asarray(row_ptr, np.int64) - int(row_ptr[0])),
+                      shape=(S, len(w)))
+    return A @ np.asarray(w, np.float64)
+
+
+def objective_csr(w, row_ptr, col, val, y, loss, l2) -> float:
+    """f_i(w) on a CSR shard (fp64)."""
+    m = margins_csr(w, row_ptr, col, val)
+    w = np.asarray(w, np.float64)
+    return float(np.mean(loss_value(np.asarray(y, np.float64) * m, loss))
+                 + 0.5 * l2 * np.dot(w, w))
+
+
+def ambiguous_hinge_rows(w, row_ptr, col, val, y, rows, rel=1e-5):
+    """Rows whose hinge decision y m < 1 could flip under fp32 rounding.
+
+    A row is ambiguous when |y m - 1| <= rel * (1 + sum_j |w_j x_j|).
+    """
+    w = np.asarray(w, np.float64)
+    out = []
+    for r in rows:
+        lo, hi = row_ptr[r], row_ptr[r + 1]
+        prod = val[lo:hi].astype(np.float64) * w[col[lo:hi]]
+        if abs(y[r] * prod.sum() - 1.0) <= rel * (1.0 + np.abs(prod).sum()):
+            out.append(r)
+    return out
