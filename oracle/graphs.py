@@ -77,8 +77,9 @@ def _connected(adj) -> bool:
 
 def random_regular(n: int, d: int, seed: int):
     """Connected simple random d-regular graph as in-neighbour CSR (self included)."""
-    if not (1 <= d < n) or (n * d) % 2:
-        raise ValueError("random_regular needs 1 <= d < n and n*d even")
+    if not (1 <= d < n) or (n * d) % 2 or (d == 1 and n > 2):
+        # a 1-regular graph on more than two nodes is a matching: never connected
+        raise ValueError("random_regular needs 1 <= d < n, n*d even, and d >= 2 unless n == 2")
     rng = SplitMix64(derive_key(seed, TAG_GRAPH, n, d, 0))
     while True:
         stubs = [v for v in range(n) for _ in range(d)]

@@ -86,26 +86,35 @@ def sgd_pass_dense(w0, X, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd):
     return w
 
 
-def sgd_pass_csr(w0, row_ptr, col, val, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd):
+def sgd_pass_csr(w0, row_ptr, col, val, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd,
+                 ambiguous=None):
     """One local pass of one worker on CSR data (local row offsets); fp64.
 
     The L2 term is applied densely every step, exactly as the update states.
+    If `ambiguous` is a list, rows whose hinge decision y m < 1 lies within
+    fp32 rounding of the kink (|y m - 1| <= 1e-5 (1 + sum_j |w_j x_j|)) at
+    the step that uses them are appended to it.
     """
     w = np.asarray(w0, np.float64).copy()
+    row_ptr = np.asarray(row_ptr, np.int64)
     S = len(row_ptr) - 1
     K = n_steps(S, batch)
     for k in range(K):
-        rows = sched[k * batch:min((k + 1) * batch, S)]
-        m = np.empty(len(rows))
-        for b, r in enumerate(rows):
-            lo, hi = row_ptr[r], row_ptr[r + 1]
-            m[b] = np.dot(val[lo:hi].astype(np.float64), w[col[lo:hi]])
-        c = loss_coef(m, y[rows].astype(np.float64), loss)
+        rows = np.asarray(sched[k * batch:min((k + 1) * batch, S)], np.int64)
+        lo, lens = row_ptr[rows], row_ptr[rows + 1] - row_ptr[rows]
+        seg = np.repeat(np.arange(len(rows)), lens)               # pair -> position in batch
+        pos = np.arange(lens.sum()) - np.repeat(np.cumsum(lens) - lens, lens) + np.repeat(lo, lens)
+        cols, vals = col[pos], val[pos].astype(np.float64)
+        prod = vals * w[cols]
+        m = np.bincount(seg, weights=prod, minlength=len(rows))   # margins, pre-step w
+        yb = y[rows].astype(np.float64)
+        if ambiguous is not None and loss == HINGE:
+            absum = np.bincount(seg, weights=np.abs(prod), minlength=len(rows))
+            hit = np.abs(yb * m - 1.0) <= 1e-5 * (1.0 + absum)
+            ambiguous.extend(int(r) for r in rows[hit])
+        c = loss_coef(m, yb, loss)
         g = l2 * w
-        inv_b = 1.0 / len(rows)
-        for b, r in enumerate(rows):
-            lo, hi = row_ptr[r], row_ptr[r + 1]
-            np.add.at(g, col[lo:hi], c[b] * inv_b * val[lo:hi].astype(np.float64))
+        np.add.at(g, cols, c[seg] * vals / len(rows))
         w = w - step_size(lr_kind, lr0, rnd * K + k + 1) * g
     return w
 

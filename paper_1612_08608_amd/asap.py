@@ -1,0 +1,359 @@
+"""Thin ctypes binding of libasap.so (the C ABI declared in include/asap.h).
+
+Functions carry the C names and only marshal arguments: host arrays become
+pointers, torch CUDA tensors become device pointers, the stream defaults to
+torch's current stream.  Every non-OK status raises AsapError with the
+library's message.  All compute runs in the HIP kernels of libasap.so; if the
+library is missing this module raises instead of falling back to anything.
+
+`Session` bundles one context with torch-allocated device memory (workspace
+and the two model buffers): PyTorch provides memory and streams only.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libasap.so")
+
+OK, E_INVALID_ARG, E_GRAPH, E_STATE, E_DEVICE, E_EPOCH = range(6)
+STATUS_NAMES = {0: "ASAP_OK", 1: "ASAP_E_INVALID_ARG", 2: "ASAP_E_GRAPH", 3: "ASAP_E_STATE",
+                4: "ASAP_E_DEVICE", 5: "ASAP_E_EPOCH"}
+LOSS = {"logistic": 0, "hinge": 1}
+LR = {"const": 0, "inv_sqrt": 1}
+ALLOW_NON_DS = 1
+
+# Every symbol include/asap.h declares.
+EXPORTS = (
+    "asap_graph_ring", "asap_graph_complete", "asap_graph_random_regular",
+    "asap_metropolis_weights", "asap_schedule", "asap_create", "asap_workspace_size",
+    "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr",
+    "asap_local_sgd", "asap_stochastic_reduce", "asap_round", "asap_current",
+    "asap_set_round", "asap_schedule_device", "asap_metrics", "asap_check",
+    "asap_debug_set_tag", "asap_last_error", "asap_destroy",
+)
+
+
+class AsapError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class SgdParams(C.Structure):
+    _fields_ = [("loss", C.c_int32), ("lr_kind", C.c_int32), ("lr0", C.c_float),
+                ("l2", C.c_float), ("batch", C.c_int32), ("reserved", C.c_int32),
+                ("seed", C.c_uint64)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libasap.so once; raise loudly if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is missing: build it with `python -m paper_1612_08608_amd.build`")
+    L = C.CDLL(_LIB_PATH)
+    p, i32, i64, u32, u64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_size_t
+    sigs = {
+        "asap_graph_ring": [i32, p, p],
+        "asap_graph_complete": [i32, p, p],
+        "asap_graph_random_regular": [i32, i32, u64, p, p],
+        "asap_metropolis_weights": [i32, p, p, p],
+        "asap_schedule": [i64, u64, i32, i64, p],
+        "asap_create": [i32, i64, p, p, p, u32, C.POINTER(p)],
+        "asap_workspace_size": [p, C.POINTER(sz)],
+        "asap_bind_workspace": [p, p, sz, p],
+        "asap_bind_models": [p, p, p, i64, p],
+        "asap_bind_dense": [p, p, p, i64, i64],
+        "asap_bind_csr": [p, p, p, p, p, i64, p],
+        "asap_local_sgd": [p, C.POINTER(SgdParams), p],
+        "asap_stochastic_reduce": [p, p],
+        "asap_round": [p, C.POINTER(SgdParams), p],
+        "asap_current": [p, C.POINTER(i32), C.POINTER(i64), C.POINTER(i32)],
+        "asap_set_round": [p, i64, i32, p],
+        "asap_schedule_device": [p, u64, i64, p, p],
+        "asap_metrics": [p, i32, C.c_float, p, p],
+        "asap_check": [p, p, C.POINTER(i32)],
+        "asap_debug_set_tag": [p, i32, i32, i64, p],
+    }
+    for name, args in sigs.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = C.c_int
+    L.asap_last_error.argtypes = [p]
+    L.asap_last_error.restype = C.c_char_p
+    L.asap_destroy.argtypes = [p]
+    L.asap_destroy.restype = None
+    _lib = L
+    return L
+
+
+def _check(status: int, ctx=None):
+    if status != OK:
+        msg = lib().asap_last_error(ctx)
+        raise AsapError(status, msg.decode() if msg else "")
+
+
+def _host(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(C.c_void_p)
+
+
+def _dev(t):
+    """Device pointer of a torch CUDA tensor (or a raw integer address)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return C.c_void_p(t)
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return C.c_void_p(stream)
+    return C.c_void_p(stream.cuda_stream)
+
+
+# ---------------------------------------------------------------------------
+# host-only builders
+# ---------------------------------------------------------------------------
+def asap_graph_ring(n: int):
+    ptr = np.zeros(n + 1, np.int32)
+    idx = np.zeros(3 * max(n, 0), np.int32)
+    _check(lib().asap_graph_ring(n, ptr.ctypes.data_as(C.c_void_p), idx.ctypes.data_as(C.c_void_p)))
+    return ptr, idx
+
+
+def asap_graph_complete(n: int):
+    ptr = np.zeros(n + 1, np.int32)
+    idx = np.zeros(max(n, 0) * max(n, 0), np.int32)
+    _check(lib().asap_graph_complete(n, ptr.ctypes.data_as(C.c_void_p), idx.ctypes.data_as(C.c_void_p)))
+    return ptr, idx
+
+
+def asap_graph_random_regular(n: int, d: int, seed: int):
+    ptr = np.zeros(max(n, 0) + 1, np.int32)
+    idx = np.zeros(max(n, 0) * (max(d, 0) + 1), np.int32)
+    _check(lib().asap_graph_random_regular(n, d, seed, ptr.ctypes.data_as(C.c_void_p),
+                                           idx.ctypes.data_as(C.c_void_p)))
+    return ptr, idx
+
+
+def asap_metropolis_weights(ptr, idx):
+    ptr, pp = _host(ptr, np.int32)
+    idx, ip = _host(idx, np.int32)
+    w = np.zeros(idx.size, np.float32)
+    _check(lib().asap_metropolis_weights(ptr.size - 1, pp, ip, w.ctypes.data_as(C.c_void_p)))
+    return w
+
+
+def asap_schedule(samples: int, seed: int, worker: int, round_: int):
+    out = np.zeros(max(samples, 0), np.int32)
+    _check(lib().asap_schedule(samples, seed, worker, round_, out.ctypes.data_as(C.c_void_p)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# context calls (ctx is a ctypes c_void_p)
+# ---------------------------------------------------------------------------
+def asap_create(n: int, dim: int, ptr, idx, w, flags: int = 0):
+    ptr, pp = _host(ptr, np.int32)
+    idx, ip = _host(idx, np.int32)
+    w, wp = _host(w, np.float32)
+    ctx = C.c_void_p()
+    _check(lib().asap_create(n, dim, pp, ip, wp, flags, C.byref(ctx)))
+    return ctx
+
+
+def asap_workspace_size(ctx) -> int:
+    out = C.c_size_t()
+    _check(lib().asap_workspace_size(ctx, C.byref(out)), ctx)
+    return out.value
+
+
+def asap_bind_workspace(ctx, dev, nbytes: int, stream=None):
+    _check(lib().asap_bind_workspace(ctx, _dev(dev), nbytes, _stream(stream)), ctx)
+
+
+def asap_bind_models(ctx, buf0, buf1, ld: int, stream=None):
+    _check(lib().asap_bind_models(ctx, _dev(buf0), _dev(buf1), ld, _stream(stream)), ctx)
+
+
+def asap_bind_dense(ctx, X, y, samples: int, ldx: int):
+    _check(lib().asap_bind_dense(ctx, _dev(X), _dev(y), samples, ldx), ctx)
+
+
+def asap_bind_csr(ctx, row_ptr, col, val, y, samples: int, stream=None):
+    _check(lib().asap_bind_csr(ctx, _dev(row_ptr), _dev(col), _dev(val), _dev(y), samples,
+                               _stream(stream)), ctx)
+
+
+def sgd_params(loss="logistic", lr_kind="const", lr0=0.1, l2=0.0, batch=1, seed=0) -> SgdParams:
+    return SgdParams(LOSS.get(loss, loss), LR.get(lr_kind, lr_kind), lr0, l2, batch, 0, seed)
+
+
+def asap_local_sgd(ctx, params: SgdParams, stream=None):
+    _check(lib().asap_local_sgd(ctx, C.byref(params), _stream(stream)), ctx)
+
+
+def asap_stochastic_reduce(ctx, stream=None):
+    _check(lib().asap_stochastic_reduce(ctx, _stream(stream)), ctx)
+
+
+def asap_round(ctx, params: SgdParams, stream=None):
+    _check(lib().asap_round(ctx, C.byref(params), _stream(stream)), ctx)
+
+
+def asap_current(ctx):
+    b, r, h = C.c_int32(), C.c_int64(), C.c_int32()
+    _check(lib().asap_current(ctx, C.byref(b), C.byref(r), C.byref(h)), ctx)
+    return b.value, r.value, h.value
+
+
+def asap_set_round(ctx, round_: int, buffer: int, stream=None):
+    _check(lib().asap_set_round(ctx, round_, buffer, _stream(stream)), ctx)
+
+
+def asap_schedule_device(ctx, seed: int, round_: int, out, stream=None):
+    _check(lib().asap_schedule_device(ctx, seed, round_, _dev(out), _stream(stream)), ctx)
+
+
+def asap_metrics(ctx, loss="logistic", l2=0.0, stream=None):
+    out = np.zeros(4, np.float64)
+    _check(lib().asap_metrics(ctx, LOSS.get(loss, loss), l2, out.ctypes.data_as(C.c_void_p),
+                              _stream(stream)), ctx)
+    return out
+
+
+def asap_check(ctx, stream=None):
+    """Returns (status, bad_worker) without raising, so callers can inspect E_EPOCH."""
+    bad = C.c_int32(-1)
+    st = lib().asap_check(ctx, _stream(stream), C.byref(bad))
+    return st, bad.value
+
+
+def asap_debug_set_tag(ctx, buffer: int, worker: int, value: int, stream=None):
+    _check(lib().asap_debug_set_tag(ctx, buffer, worker, value, _stream(stream)), ctx)
+
+
+def asap_last_error(ctx=None) -> str:
+    m = lib().asap_last_error(ctx)
+    return m.decode() if m else ""
+
+
+def asap_destroy(ctx):
+    if ctx:
+        lib().asap_destroy(ctx)
+
+
+# ---------------------------------------------------------------------------
+# Session: one context plus its torch-owned device memory
+# ---------------------------------------------------------------------------
+class Session:
+    """A context with torch-allocated workspace and model buffers on `device`.
+
+    Data tensors passed to bind_dense / bind_csr are kept referenced here so
+    that they outlive the context, as the C ABI requires.
+    """
+
+    def __init__(self, n, dim, ptr, idx, w, flags=0, device="cuda:0"):
+        import torch
+        self.torch = torch
+        self.device = torch.device(device)
+        self.n, self.dim = int(n), int(dim)
+        self.ld = (self.dim + 63) // 64 * 64
+        self.ctx = asap_create(self.n, self.dim, ptr, idx, w, flags)
+        self.bufs = [torch.zeros((self.n, self.ld), dtype=torch.float32, device=self.device) for _ in range(2)]
+        self._keep = []
+        self.ws = None
+        asap_bind_models(self.ctx, self.bufs[0], self.bufs[1], self.ld)
+
+    # binds --------------------------------------------------------------
+    def set_models(self, W, stream=None):
+        """Copy W [n, dim] into buffer 0 and restart at round 0."""
+        t = self.torch
+        W = t.as_tensor(W, dtype=t.float32)
+        self.bufs[0].zero_()
+        self.bufs[0][:, :self.dim].copy_(W.to(self.device))
+        asap_bind_models(self.ctx, self.bufs[0], self.bufs[1], self.ld, stream)
+        self.ws = None
+
+    def bind_dense(self, X, y):
+        t = self.torch
+        X = t.as_tensor(X, dtype=t.float32)
+        n, S, D = X.shape
+        ldx = (D + 3) // 4 * 4
+        if ldx != D:
+            X = t.nn.functional.pad(X, (0, ldx - D))
+        X = X.to(self.device).contiguous()
+        y = t.as_tensor(y, dtype=t.float32).to(self.device).contiguous()
+        self._keep += [X, y]
+        asap_bind_dense(self.ctx, X, y, S, ldx)
+        self.ws = None
+
+    def bind_csr(self, row_ptr, col, val, y, samples):
+        t = self.torch
+        rp = t.as_tensor(np.asarray(row_ptr, np.int64)).to(self.device)
+        cl = t.as_tensor(np.asarray(col, np.int32)).to(self.device)
+        vl = t.as_tensor(np.asarray(val, np.float32)).to(self.device)
+        yy = t.as_tensor(np.asarray(y, np.float32)).to(self.device)
+        self._keep += [rp, cl, vl, yy]
+        asap_bind_csr(self.ctx, rp, cl, vl, yy, samples)
+        self.ws = None
+
+    def ready(self, stream=None):
+        """(Re)bind a workspace of the size the current bindings need."""
+        if self.ws is None:
+            nbytes = asap_workspace_size(self.ctx)
+            self.ws = self.torch.empty(max(nbytes, 256), dtype=self.torch.uint8, device=self.device)
+            asap_bind_workspace(self.ctx, self.ws, self.ws.numel(), stream)
+        return self
+
+    # hot path -----------------------------------------------------------
+    def local_sgd(self, params, stream=None):
+        asap_local_sgd(self.ready().ctx, params, stream)
+
+    def stochastic_reduce(self, stream=None):
+        asap_stochastic_reduce(self.ready().ctx, stream)
+
+    def round(self, params, stream=None):
+        asap_round(self.ready().ctx, params, stream)
+
+    # inspection ---------------------------------------------------------
+    def current(self):
+        return asap_current(self.ctx)
+
+    def models(self):
+        """Current models [n, dim] as a device view (no copy)."""
+        b, _, _ = self.current()
+        return self.bufs[b][:, :self.dim]
+
+    def metrics(self, loss="logistic", l2=0.0):
+        return asap_metrics(self.ready().ctx, loss, l2)
+
+    def check(self):
+        return asap_check(self.ctx)
+
+    def close(self):
+        if self.ctx:
+            asap_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

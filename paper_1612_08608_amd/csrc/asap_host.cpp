@@ -1,0 +1,662 @@
+// asap_host.cpp -- the C ABI: graph builders, validation, the round state
+// machine (double buffer + epoch tags) and kernel dispatch.
+//
+// The library owns no device memory.  Device state (graph copy, epoch tags,
+// per-worker L2 scales, error words, the round's sample schedule and metric
+// partials) lives in the caller's workspace at fixed offsets.
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "asap.h"
+#include "asap_common.h"
+#include "asap_launch.h"
+
+using namespace asap;
+
+namespace {
+
+thread_local std::string g_free_error;  // message of the last context-free failure
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+enum DataKind { kNoData = 0, kDense = 1, kCsr = 2 };
+
+}  // namespace
+
+struct asap_ctx {
+  int32_t n = 0;
+  int64_t dim = 0;
+  std::vector<int32_t> ptr, idx;
+  std::vector<float> w;
+  bool complete_uniform = false;
+
+  // caller-owned device memory
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  float* buf[2] = {nullptr, nullptr};
+  int64_t ld = 0;
+
+  int kind = kNoData;
+  const float* X = nullptr;
+  int64_t ldx = 0;
+  const float* y = nullptr;
+  int64_t S = 0;
+  const int64_t* row_ptr = nullptr;
+  const int32_t* col = nullptr;
+  const float* val = nullptr;
+
+  // workspace layout (byte offsets)
+  size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
+         off_vmax = 0, off_scan = 0, off_sched = 0, off_wbar = 0, off_part = 0, off_out = 0,
+         total = 0;
+
+  // round state
+  int32_t cur = 0;
+  int64_t round = 0;
+  bool half_done = false;
+  bool half_scaled = false;  // the half-step left per-worker L2 scales to fold
+  bool tags_ready = false;
+
+  std::string err;
+};
+
+namespace {
+
+asap_status fail(asap_ctx* c, asap_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c)
+    c->err = buf;
+  else
+    g_free_error = buf;
+  return s;
+}
+
+asap_status hip_fail(asap_ctx* c, hipError_t e, const char* what) {
+  return fail(c, ASAP_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+template <class T>
+T* at(asap_ctx* c, size_t off) {
+  return reinterpret_cast<T*>(c->ws + off);
+}
+
+void layout(asap_ctx* c) {
+  const size_t n = size_t(c->n), nnz = c->idx.size();
+  size_t o = 0;
+  c->off_ptr = o;   o = align_up(o + (n + 1) * 4);
+  c->off_idx = o;   o = align_up(o + nnz * 4);
+  c->off_w = o;     o = align_up(o + nnz * 4);
+  c->off_tag = o;   o = align_up(o + 2 * n * 8);
+  c->off_scale = o; o = align_up(o + n * 4);
+  c->off_err = o;   o = align_up(o + kErrWords * 4);
+  c->off_vmax = o;  o = align_up(o + n * 4);
+  c->off_scan = o;  o = align_up(o + 8 * 8);
+  c->off_sched = o; o = align_up(o + n * size_t(c->S) * 4);
+  c->off_wbar = o;  o = align_up(o + size_t(c->dim) * 8);
+  c->off_part = o;  o = align_up(o + (2 * 4096 + 3 * n) * 8);
+  c->off_out = o;   o = align_up(o + 8 * 8);
+  c->total = o;
+}
+
+void unbind_workspace(asap_ctx* c) {
+  c->ws = nullptr;
+  c->ws_bytes = 0;
+  c->tags_ready = false;
+}
+
+// --------------------------------------------------------------------------
+// graph validation
+// --------------------------------------------------------------------------
+asap_status check_graph(asap_ctx* c, int32_t n, const int32_t* ptr, const int32_t* idx,
+                        const float* w, uint32_t flags) {
+  if (ptr[0] != 0) return fail(c, ASAP_E_GRAPH, "nbr_ptr[0] must be 0");
+  for (int32_t i = 0; i < n; ++i)
+    if (ptr[i + 1] < ptr[i]) return fail(c, ASAP_E_GRAPH, "nbr_ptr decreases at row %d", i);
+  const int64_t nnz = ptr[n];
+  if (nnz > int64_t(n) * n) return fail(c, ASAP_E_GRAPH, "more than n*n entries");
+  std::vector<double> colsum(n, 0.0);
+  for (int32_t i = 0; i < n; ++i) {
+    bool self = false;
+    double rs = 0.0;
+    for (int32_t p = ptr[i]; p < ptr[i + 1]; ++p) {
+      const int32_t j = idx[p];
+      if (j < 0 || j >= n) return fail(c, ASAP_E_GRAPH, "row %d: neighbour %d out of range", i, j);
+      if (p > ptr[i] && idx[p - 1] >= j)
+        return fail(c, ASAP_E_GRAPH, "row %d: neighbours not strictly ascending", i);
+      if (j == i) self = true;
+      const float wt = w[p];
+      if (!std::isfinite(wt) || wt < 0.0f)
+        return fail(c, ASAP_E_GRAPH, "row %d: weight %g is negative or not finite", i, double(wt));
+      rs += wt;
+      colsum[j] += wt;
+    }
+    if (!self) return fail(c, ASAP_E_GRAPH, "row %d lacks its self entry", i);
+    const double tol = 1e-6 + double(ptr[i + 1] - ptr[i]) * std::ldexp(1.0, -24);
+    if (!(flags & ASAP_ALLOW_NON_DS) && std::fabs(rs - 1.0) > tol)
+      return fail(c, ASAP_E_GRAPH, "row %d sums to %.9g, not 1 (P must be doubly stochastic)", i, rs);
+  }
+  if (!(flags & ASAP_ALLOW_NON_DS)) {
+    for (int32_t j = 0; j < n; ++j) {
+      // column j collects at most n weights
+      const double tol = 1e-6 + double(n) * std::ldexp(1.0, -24);
+      if (std::fabs(colsum[j] - 1.0) > tol)
+        return fail(c, ASAP_E_GRAPH, "column %d sums to %.9g, not 1 (P must be doubly stochastic)", j,
+                    colsum[j]);
+    }
+  }
+  return ASAP_OK;
+}
+
+bool is_complete_uniform(int32_t n, const int32_t* ptr, const float* w) {
+  if (int64_t(ptr[n]) != int64_t(n) * n) return false;
+  uint32_t w0;
+  std::memcpy(&w0, &w[0], 4);
+  for (int64_t p = 0; p < int64_t(n) * n; ++p) {
+    uint32_t b;
+    std::memcpy(&b, &w[p], 4);
+    if (b != w0) return false;
+  }
+  return true;  // n*n strictly ascending in-range entries = every j in every row
+}
+
+asap_status need_device(asap_ctx* c) {
+  if (!c->buf[0] || !c->buf[1]) return fail(c, ASAP_E_STATE, "models are not bound");
+  if (!c->ws) return fail(c, ASAP_E_STATE, "workspace is not bound");
+  if (!c->tags_ready) return fail(c, ASAP_E_STATE, "workspace is not initialised");
+  return ASAP_OK;
+}
+
+asap_status check_params(asap_ctx* c, const asap_sgd_params* p) {
+  if (!p) return fail(c, ASAP_E_INVALID_ARG, "params is NULL");
+  if (p->loss != ASAP_LOSS_LOGISTIC && p->loss != ASAP_LOSS_HINGE)
+    return fail(c, ASAP_E_INVALID_ARG, "unknown loss %d", p->loss);
+  if (p->lr_kind != ASAP_LR_CONST && p->lr_kind != ASAP_LR_INV_SQRT)
+    return fail(c, ASAP_E_INVALID_ARG, "unknown lr_kind %d", p->lr_kind);
+  if (!(std::isfinite(p->lr0) && p->lr0 > 0.0f)) return fail(c, ASAP_E_INVALID_ARG, "lr0 must be > 0");
+  if (!(std::isfinite(p->l2) && p->l2 >= 0.0f)) return fail(c, ASAP_E_INVALID_ARG, "l2 must be >= 0");
+  if (p->batch < 1) return fail(c, ASAP_E_INVALID_ARG, "batch must be >= 1");
+  if (c->kind == kCsr && p->batch > 512)
+    return fail(c, ASAP_E_INVALID_ARG, "CSR minibatch is limited to 512 rows");
+  if (p->reserved != 0) return fail(c, ASAP_E_INVALID_ARG, "reserved must be 0");
+  return ASAP_OK;
+}
+
+}  // namespace
+
+// ============================================================================
+// host-only builders
+// ============================================================================
+extern "C" asap_status asap_graph_ring(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx) {
+  if (n < 3 || n > (1 << 28)) return fail(nullptr, ASAP_E_INVALID_ARG, "ring needs 3 <= n <= 2^28");
+  if (!nbr_ptr || !nbr_idx) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL output");
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t a = (i + n - 1) % n, b = i, d = (i + 1) % n;
+    int32_t r[3] = {a, b, d};
+    std::sort(r, r + 3);
+    nbr_ptr[i] = 3 * i;
+    for (int k = 0; k < 3; ++k) nbr_idx[3 * i + k] = r[k];
+  }
+  nbr_ptr[n] = 3 * n;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_graph_complete(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx) {
+  if (n < 1 || n > 46340) return fail(nullptr, ASAP_E_INVALID_ARG, "complete needs 1 <= n <= 46340");
+  if (!nbr_ptr || !nbr_idx) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL output");
+  for (int32_t i = 0; i < n; ++i) {
+    nbr_ptr[i] = i * n;
+    for (int32_t j = 0; j < n; ++j) nbr_idx[int64_t(i) * n + j] = j;
+  }
+  nbr_ptr[n] = n * n;
+  return ASAP_OK;
+}
+
+namespace {
+
+struct Stream64 {
+  uint64_t state;
+  uint64_t next() {
+    state += kGamma;
+    return mix64(state);
+  }
+  // Uniform in [0, m): reject the top (2^64 mod m) values.
+  uint64_t below(uint64_t m) {
+    const uint64_t rem = (0 - m) % m;  // 2^64 mod m
+    for (;;) {
+      const uint64_t r = next();
+      if (rem == 0 || r < 0 - rem) return r % m;
+    }
+  }
+};
+
+bool connected(const std::vector<std::vector<int32_t>>& adj) {
+  const size_t n = adj.size();
+  std::vector<char> seen(n, 0);
+  std::vector<int32_t> q;
+  q.reserve(n);
+  q.push_back(0);
+  seen[0] = 1;
+  for (size_t h = 0; h < q.size(); ++h)
+    for (int32_t v : adj[q[h]])
+      if (!seen[v]) {
+        seen[v] = 1;
+        q.push_back(v);
+      }
+  return q.size() == n;
+}
+
+}  // namespace
+
+extern "C" asap_status asap_graph_random_regular(int32_t n, int32_t d, uint64_t seed,
+                                                 int32_t* nbr_ptr, int32_t* nbr_idx) {
+  // a 1-regular graph on more than two nodes is a matching and never connected
+  if (n < 2 || n > (1 << 20) || d < 1 || d >= n || (int64_t(n) * d) % 2 || (d == 1 && n > 2))
+    return fail(nullptr, ASAP_E_INVALID_ARG,
+                "random_regular needs 1 <= d < n <= 2^20, n*d even, d >= 2 unless n == 2");
+  if (!nbr_ptr || !nbr_idx) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL output");
+  Stream64 rng{derive_key(seed, kTagGraph, uint64_t(n), uint64_t(d), 0)};
+  std::vector<std::vector<int32_t>> adj(n);
+  std::vector<int32_t> stubs;
+  for (;;) {
+    stubs.clear();
+    for (int32_t v = 0; v < n; ++v)
+      for (int32_t k = 0; k < d; ++k) stubs.push_back(v);
+    for (auto& a : adj) a.clear();
+    uint64_t stalls = 0;
+    bool ok = true;
+    while (!stubs.empty()) {
+      const uint64_t m = stubs.size();
+      const uint64_t a = rng.below(m), b = rng.below(m);
+      const int32_t u = stubs[a], v = stubs[b];
+      const bool exists = std::find(adj[u].begin(), adj[u].end(), v) != adj[u].end();
+      if (a == b || u == v || exists) {
+        if (++stalls > 100 * m) {
+          ok = false;
+          break;
+        }
+        continue;
+      }
+      stalls = 0;
+      adj[u].push_back(v);
+      adj[v].push_back(u);
+      for (uint64_t k : {std::max(a, b), std::min(a, b)}) {
+        stubs[k] = stubs.back();
+        stubs.pop_back();
+      }
+    }
+    if (ok && connected(adj)) break;
+  }
+  int32_t p = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    std::vector<int32_t> row = adj[i];
+    row.push_back(i);
+    std::sort(row.begin(), row.end());
+    nbr_ptr[i] = p;
+    for (int32_t j : row) nbr_idx[p++] = j;
+  }
+  nbr_ptr[n] = p;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_metropolis_weights(int32_t n, const int32_t* ptr, const int32_t* idx,
+                                               float* w) {
+  if (n < 1 || !ptr || !idx || !w) return fail(nullptr, ASAP_E_INVALID_ARG, "bad arguments");
+  for (int32_t i = 0; i < n; ++i) {
+    double off = 0.0;
+    int32_t self = -1;
+    const int32_t di = ptr[i + 1] - ptr[i] - 1;
+    for (int32_t p = ptr[i]; p < ptr[i + 1]; ++p) {
+      const int32_t j = idx[p];
+      if (j < 0 || j >= n) return fail(nullptr, ASAP_E_GRAPH, "row %d: neighbour out of range", i);
+      if (j == i) {
+        self = p;
+        continue;
+      }
+      const int32_t dj = ptr[j + 1] - ptr[j] - 1;
+      const double pij = 1.0 / (1.0 + double(std::max(di, dj)));
+      off += pij;
+      w[p] = float(pij);
+    }
+    if (self < 0) return fail(nullptr, ASAP_E_GRAPH, "row %d lacks its self entry", i);
+    w[self] = float(1.0 - off);
+  }
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_schedule(int64_t samples, uint64_t seed, int32_t worker, int64_t round,
+                                     int32_t* out) {
+  if (samples < 0 || samples >= (int64_t(1) << 31) || (samples > 0 && !out))
+    return fail(nullptr, ASAP_E_INVALID_ARG, "samples must be in [0, 2^31) with a non-NULL out");
+  const Perm p = perm_make(seed, worker, round, uint32_t(samples));
+  for (int64_t k = 0; k < samples; ++k) out[k] = int32_t(perm_at(p, uint32_t(k)));
+  return ASAP_OK;
+}
+
+// ============================================================================
+// context
+// ============================================================================
+extern "C" asap_status asap_create(int32_t n, int64_t dim, const int32_t* nbr_ptr,
+                                   const int32_t* nbr_idx, const float* nbr_w, uint32_t flags,
+                                   asap_ctx** out) {
+  if (!out) return fail(nullptr, ASAP_E_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (n < 1 || n > (1 << 20)) return fail(nullptr, ASAP_E_INVALID_ARG, "n_workers must be in [1, 2^20]");
+  if (dim < 1 || dim > (int64_t(1) << 34)) return fail(nullptr, ASAP_E_INVALID_ARG, "dim must be in [1, 2^34]");
+  if (!nbr_ptr || !nbr_idx || !nbr_w) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL graph array");
+  if (flags & ~uint32_t(ASAP_ALLOW_NON_DS)) return fail(nullptr, ASAP_E_INVALID_ARG, "unknown flags");
+  asap_status s = check_graph(nullptr, n, nbr_ptr, nbr_idx, nbr_w, flags);
+  if (s != ASAP_OK) return s;
+  asap_ctx* c = new asap_ctx;
+  c->n = n;
+  c->dim = dim;
+  c->ptr.assign(nbr_ptr, nbr_ptr + n + 1);
+  c->idx.assign(nbr_idx, nbr_idx + nbr_ptr[n]);
+  c->w.assign(nbr_w, nbr_w + nbr_ptr[n]);
+  c->complete_uniform = is_complete_uniform(n, nbr_ptr, nbr_w);
+  layout(c);
+  *out = c;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_workspace_size(const asap_ctx* c, size_t* bytes) {
+  if (!c || !bytes) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL argument");
+  *bytes = c->total;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_bind_models(asap_ctx* c, float* b0, float* b1, int64_t ld, void* stream) {
+  (void)stream;
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!b0 || !b1 || b0 == b1) return fail(c, ASAP_E_INVALID_ARG, "need two distinct model buffers");
+  if (ld < c->dim || ld % 64) return fail(c, ASAP_E_INVALID_ARG, "ld must be >= dim and a multiple of 64");
+  if ((uintptr_t(b0) | uintptr_t(b1)) % 256) return fail(c, ASAP_E_INVALID_ARG, "model buffers must be 256-byte aligned");
+  c->buf[0] = b0;
+  c->buf[1] = b1;
+  c->ld = ld;
+  c->cur = 0;
+  c->round = 0;
+  c->half_done = false;
+  c->half_scaled = false;
+  unbind_workspace(c);
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_bind_dense(asap_ctx* c, const float* X, const float* y, int64_t S,
+                                       int64_t ldx) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!X || !y) return fail(c, ASAP_E_INVALID_ARG, "NULL data pointer");
+  if (S < 1 || S >= (int64_t(1) << 31)) return fail(c, ASAP_E_INVALID_ARG, "samples must be in [1, 2^31)");
+  if (ldx < c->dim || ldx % 4 || uintptr_t(X) % 16)
+    return fail(c, ASAP_E_INVALID_ARG, "ldx must be >= dim, a multiple of 4, X 16-byte aligned");
+  if (c->dim > 16384) return fail(c, ASAP_E_INVALID_ARG, "dense path supports dim <= 16384");
+  c->kind = kDense;
+  c->X = X;
+  c->y = y;
+  c->S = S;
+  c->ldx = ldx;
+  c->row_ptr = nullptr;
+  c->col = nullptr;
+  c->val = nullptr;
+  layout(c);
+  unbind_workspace(c);
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_bind_csr(asap_ctx* c, const int64_t* row_ptr, const int32_t* col,
+                                     const float* val, const float* y, int64_t S, void* stream) {
+  (void)stream;
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!row_ptr || !col || !val || !y) return fail(c, ASAP_E_INVALID_ARG, "NULL data pointer");
+  if (S < 1 || S >= (int64_t(1) << 31)) return fail(c, ASAP_E_INVALID_ARG, "samples must be in [1, 2^31)");
+  if (c->dim >= (int64_t(1) << 31)) return fail(c, ASAP_E_INVALID_ARG, "CSR path needs dim < 2^31");
+  c->kind = kCsr;
+  c->row_ptr = row_ptr;
+  c->col = col;
+  c->val = val;
+  c->y = y;
+  c->S = S;
+  c->X = nullptr;
+  c->ldx = 0;
+  layout(c);
+  unbind_workspace(c);
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!dev || uintptr_t(dev) % kAlign) return fail(c, ASAP_E_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (bytes < c->total)
+    return fail(c, ASAP_E_INVALID_ARG, "workspace too small: %zu < %zu bytes", bytes, c->total);
+  if (!c->buf[0]) return fail(c, ASAP_E_STATE, "bind the models before the workspace");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->ws = static_cast<char*>(dev);
+  c->ws_bytes = bytes;
+  c->tags_ready = false;
+  hipError_t e;
+  const size_t n = size_t(c->n), nnz = c->idx.size();
+  if ((e = hipMemcpyAsync(at<int32_t>(c, c->off_ptr), c->ptr.data(), (n + 1) * 4, hipMemcpyHostToDevice, s)) ||
+      (e = hipMemcpyAsync(at<int32_t>(c, c->off_idx), c->idx.data(), nnz * 4, hipMemcpyHostToDevice, s)) ||
+      (e = hipMemcpyAsync(at<float>(c, c->off_w), c->w.data(), nnz * 4, hipMemcpyHostToDevice, s)))
+    return hip_fail(c, e, "graph upload");
+  if ((e = launch_fill_i64(at<int64_t>(c, c->off_tag), 2 * int64_t(n), -1, s)) ||
+      (e = launch_fill_i64(at<int64_t>(c, c->off_tag) + c->cur * n, int64_t(n), tag_start(c->round), s)) ||
+      (e = launch_fill_f32(at<float>(c, c->off_scale), int64_t(n), 1.0f, s)) ||
+      (e = launch_fill_i32(at<int32_t>(c, c->off_err), 1, 0, s)) ||
+      (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)))
+    return hip_fail(c, e, "workspace init");
+  if (c->kind == kCsr) {
+    int64_t* scan = at<int64_t>(c, c->off_scan);
+    if ((e = launch_fill_i64(scan, 8, 0, s)) ||
+        (e = launch_csr_scan(c->row_ptr, c->col, c->val, c->y, c->n, c->S, c->dim,
+                             at<float>(c, c->off_vmax), scan, s)))
+      return hip_fail(c, e, "CSR scan");
+    int64_t h[8];
+    if ((e = hipMemcpyAsync(h, scan, sizeof h, hipMemcpyDeviceToHost, s)) || (e = hipStreamSynchronize(s)))
+      return hip_fail(c, e, "CSR scan readback");
+    if (h[4]) return fail(c, ASAP_E_INVALID_ARG, "row_ptr must start at 0 and not decrease (%lld bad rows)", (long long)h[4]);
+    if (h[1]) return fail(c, ASAP_E_INVALID_ARG, "%lld CSR columns outside [0, dim)", (long long)h[1]);
+    if (h[2]) return fail(c, ASAP_E_INVALID_ARG, "%lld labels outside {-1, +1}", (long long)h[2]);
+    if (h[3]) return fail(c, ASAP_E_INVALID_ARG, "%lld CSR rows with unsorted or repeated columns", (long long)h[3]);
+    if (h[0] > 4096) return fail(c, ASAP_E_INVALID_ARG, "a CSR row holds %lld > 4096 nonzeros", (long long)h[0]);
+  }
+  c->tags_ready = true;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  asap_status st = need_device(c);
+  if (st != ASAP_OK) return st;
+  if (c->kind == kNoData) return fail(c, ASAP_E_STATE, "no data bound");
+  if (c->half_done) return fail(c, ASAP_E_STATE, "the half-step of round %lld already ran", (long long)c->round);
+  if ((st = check_params(c, p)) != ASAP_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SgdArgs a{};
+  a.models = c->buf[c->cur];
+  a.ld = c->ld;
+  a.dim = c->dim;
+  a.n = c->n;
+  a.S = c->S;
+  a.y = c->y;
+  a.X = c->X;
+  a.ldx = c->ldx;
+  a.row_ptr = c->row_ptr;
+  a.col = c->col;
+  a.val = c->val;
+  a.vmax = at<float>(c, c->off_vmax);
+  a.sched = at<int32_t>(c, c->off_sched);
+  a.loss = p->loss;
+  a.lr_kind = p->lr_kind;
+  a.lr0 = p->lr0;
+  a.l2 = p->l2;
+  a.batch = p->batch;
+  a.round = c->round;
+  a.scale = at<float>(c, c->off_scale);
+  a.tag = at<int64_t>(c, c->off_tag) + size_t(c->cur) * c->n;
+  a.tag_value = tag_half(c->round);
+  hipError_t e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->off_sched), s);
+  if (e != hipSuccess) return hip_fail(c, e, "schedule kernel");
+  e = (c->kind == kDense) ? launch_sgd_dense(a, s) : launch_sgd_csr(a, s);
+  if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
+  c->half_done = true;
+  c->half_scaled = (c->kind == kCsr) && p->l2 > 0.0f;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_stochastic_reduce(asap_ctx* c, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  asap_status st = need_device(c);
+  if (st != ASAP_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t n = size_t(c->n);
+  MixArgs a{};
+  a.src = c->buf[c->cur];
+  a.dst = c->buf[c->cur ^ 1];
+  a.ld = c->ld;
+  a.dim = c->dim;
+  a.n = c->n;
+  a.nbr_ptr = at<int32_t>(c, c->off_ptr);
+  a.nbr_idx = at<int32_t>(c, c->off_idx);
+  a.nbr_w = at<float>(c, c->off_w);
+  a.scale = c->half_scaled ? at<float>(c, c->off_scale) : nullptr;
+  a.tag_src = at<int64_t>(c, c->off_tag) + size_t(c->cur) * n;
+  a.tag_dst = at<int64_t>(c, c->off_tag) + size_t(c->cur ^ 1) * n;
+  a.expect = c->half_done ? tag_half(c->round) : tag_start(c->round);
+  a.next = tag_start(c->round + 1);
+  a.err = at<int32_t>(c, c->off_err);
+  hipError_t e = c->complete_uniform ? launch_mean(a, s) : launch_mix(a, s);
+  if (e != hipSuccess) return hip_fail(c, e, "reduce kernel");
+  c->cur ^= 1;
+  c->round += 1;
+  c->half_done = false;
+  c->half_scaled = false;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_round(asap_ctx* c, const asap_sgd_params* p, void* stream) {
+  asap_status s = asap_local_sgd(c, p, stream);
+  if (s != ASAP_OK) return s;
+  return asap_stochastic_reduce(c, stream);
+}
+
+extern "C" asap_status asap_current(const asap_ctx* c, int32_t* buffer, int64_t* round,
+                                    int32_t* half_step_done) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (buffer) *buffer = c->cur;
+  if (round) *round = c->round;
+  if (half_step_done) *half_step_done = c->half_done ? 1 : 0;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_set_round(asap_ctx* c, int64_t round, int32_t buffer, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (round < 0 || (buffer != 0 && buffer != 1)) return fail(c, ASAP_E_INVALID_ARG, "bad round or buffer");
+  asap_status st = need_device(c);
+  if (st != ASAP_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t n = c->n;
+  hipError_t e;
+  if ((e = launch_fill_i64(at<int64_t>(c, c->off_tag), 2 * n, -1, s)) ||
+      (e = launch_fill_i64(at<int64_t>(c, c->off_tag) + buffer * n, n, tag_start(round), s)))
+    return hip_fail(c, e, "tag reset");
+  c->cur = buffer;
+  c->round = round;
+  c->half_done = false;
+  c->half_scaled = false;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_schedule_device(asap_ctx* c, uint64_t seed, int64_t round,
+                                            int32_t* dev_out, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (c->kind == kNoData) return fail(c, ASAP_E_STATE, "no data bound");
+  if (!dev_out || round < 0) return fail(c, ASAP_E_INVALID_ARG, "bad arguments");
+  hipError_t e = launch_schedule(seed, round, c->n, c->S, dev_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "schedule kernel");
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_metrics(asap_ctx* c, int32_t loss, float l2, double* out, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!out) return fail(c, ASAP_E_INVALID_ARG, "out is NULL");
+  if (loss != ASAP_LOSS_LOGISTIC && loss != ASAP_LOSS_HINGE) return fail(c, ASAP_E_INVALID_ARG, "unknown loss");
+  if (!(std::isfinite(l2) && l2 >= 0.0f)) return fail(c, ASAP_E_INVALID_ARG, "l2 must be >= 0");
+  asap_status st = need_device(c);
+  if (st != ASAP_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  MetricArgs a{};
+  a.W = c->buf[c->cur];
+  a.ld = c->ld;
+  a.dim = c->dim;
+  a.n = c->n;
+  a.scale = c->half_scaled ? at<float>(c, c->off_scale) : nullptr;
+  a.S = c->kind == kNoData ? 0 : c->S;
+  a.y = c->y;
+  a.X = c->X;
+  a.ldx = c->ldx;
+  a.row_ptr = c->row_ptr;
+  a.col = c->col;
+  a.val = c->val;
+  a.loss = loss;
+  a.l2 = l2;
+  a.wbar = at<double>(c, c->off_wbar);
+  a.part = at<double>(c, c->off_part);
+  a.out = at<double>(c, c->off_out);
+  hipError_t e = launch_metrics(a, s);
+  if (e != hipSuccess) return hip_fail(c, e, "metrics kernels");
+  if ((e = hipMemcpyAsync(out, a.out, 4 * sizeof(double), hipMemcpyDeviceToHost, s)) ||
+      (e = hipStreamSynchronize(s)))
+    return hip_fail(c, e, "metrics readback");
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_check(asap_ctx* c, void* stream, int32_t* bad_worker) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (bad_worker) *bad_worker = -1;
+  if (!c->ws) return fail(c, ASAP_E_STATE, "workspace is not bound");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t h[2];
+  hipError_t e;
+  if ((e = hipMemcpyAsync(h, at<int32_t>(c, c->off_err), sizeof h, hipMemcpyDeviceToHost, s)) ||
+      (e = hipStreamSynchronize(s)))
+    return hip_fail(c, e, "error readback");
+  if (h[0] != 0) {
+    if (bad_worker) *bad_worker = h[1];
+    if ((e = launch_fill_i32(at<int32_t>(c, c->off_err), 1, 0, s)) ||
+        (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)) ||
+        (e = hipStreamSynchronize(s)))
+      return hip_fail(c, e, "error reset");
+    return fail(c, ASAP_E_EPOCH, "%d reduce rows skipped on a neighbour epoch-tag mismatch (lowest worker %d)",
+                h[0], h[1]);
+  }
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_debug_set_tag(asap_ctx* c, int32_t buffer, int32_t worker, int64_t value,
+                                          void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if ((buffer != 0 && buffer != 1) || worker < 0 || worker >= c->n)
+    return fail(c, ASAP_E_INVALID_ARG, "bad buffer or worker");
+  if (!c->ws) return fail(c, ASAP_E_STATE, "workspace is not bound");
+  hipError_t e = launch_fill_i64(at<int64_t>(c, c->off_tag) + size_t(buffer) * c->n + worker, 1, value,
+                                 static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(c, e, "tag write");
+  return ASAP_OK;
+}
+
+extern "C" const char* asap_last_error(const asap_ctx* c) {
+  return c ? c->err.c_str() : g_free_error.c_str();
+}
+
+extern "C" void asap_destroy(asap_ctx* c) { delete c; }

@@ -1,0 +1,99 @@
+// asap_launch.h -- kernel launchers shared by the host library and the .hip
+// translation units.  Internal; not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace asap {
+
+// Epoch tags: 2r = "models of round r at the start of the round",
+// 2r + 1 = "round r half-step published" (the NOTIFY of Section 4).
+inline int64_t tag_start(int64_t r) { return 2 * r; }
+inline int64_t tag_half(int64_t r) { return 2 * r + 1; }
+
+// Device error words (int32 each).
+enum { kErrEpochCount = 0, kErrEpochWorker = 1, kErrWords = 16 };
+
+struct MixArgs {
+  const float* src;  // [n][ld] models being read (buffer e)
+  float* dst;        // [n][ld] models being written (buffer e^1)
+  int64_t ld, dim;
+  int32_t n;
+  const int32_t* nbr_ptr;
+  const int32_t* nbr_idx;
+  const float* nbr_w;
+  const float* scale;  // per-worker L2 scale of the half-step, or null
+  const int64_t* tag_src;
+  int64_t* tag_dst;
+  int64_t expect;  // tag every in-neighbour must carry in buffer e
+  int64_t next;    // tag written for every reduced row in buffer e^1
+  int32_t* err;
+};
+
+hipError_t launch_mix(const MixArgs& a, hipStream_t s);
+hipError_t launch_mean(const MixArgs& a, hipStream_t s);
+
+struct SgdArgs {
+  float* models;  // current buffer [n][ld]
+  int64_t ld, dim;
+  int32_t n;
+  int64_t S;        // samples per worker
+  const float* y;   // [n*S]
+  // dense shards
+  const float* X;   // [n][S][ldx]
+  int64_t ldx;
+  // CSR shards
+  const int64_t* row_ptr;  // [n*S+1]
+  const int32_t* col;
+  const float* val;
+  const float* vmax;       // [n] max |val| per worker
+  // schedule of this round, [n][S]
+  const int32_t* sched;
+  int32_t loss, lr_kind;
+  float lr0, l2;
+  int32_t batch;
+  int64_t round;
+  float* scale;     // [n] out: final L2 scale (CSR)
+  int64_t* tag;     // [n] tags of the current buffer
+  int64_t tag_value;
+};
+
+hipError_t launch_schedule(uint64_t seed, int64_t round, int32_t n, int64_t S, int32_t* out,
+                           hipStream_t s);
+hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s);
+hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s);
+
+// Bind-time scan of CSR shards: vmax[i] = max |val| of worker i; out[0] =
+// max row length, out[1] = count of columns outside [0, dim), out[2] =
+// count of labels outside {-1, +1}, out[3] = count of rows with unsorted or
+// repeated columns, out[4] = count of rows whose offsets decrease or are
+// negative (plus one if row_ptr[0] != 0).  out must be zeroed before.
+hipError_t launch_csr_scan(const int64_t* row_ptr, const int32_t* col, const float* val,
+                           const float* y, int32_t n, int64_t S, int64_t dim, float* vmax,
+                           int64_t* out, hipStream_t s);
+hipError_t launch_fill_i64(int64_t* p, int64_t count, int64_t value, hipStream_t s);
+hipError_t launch_fill_f32(float* p, int64_t count, float value, hipStream_t s);
+hipError_t launch_fill_i32(int32_t* p, int64_t count, int32_t value, hipStream_t s);
+
+struct MetricArgs {
+  const float* W;  // current buffer [n][ld]
+  int64_t ld, dim;
+  int32_t n;
+  const float* scale;  // or null
+  int64_t S;
+  const float* y;
+  const float* X;
+  int64_t ldx;
+  const int64_t* row_ptr;
+  const int32_t* col;
+  const float* val;
+  int32_t loss;
+  float l2;
+  double* wbar;     // [dim]
+  double* part;     // partial sums: 2 * 4096 column-block + 3 * n worker doubles
+  double* out;      // [4] device
+};
+hipError_t launch_metrics(const MetricArgs& a, hipStream_t s);
+
+}  // namespace asap

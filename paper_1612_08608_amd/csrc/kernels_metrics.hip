@@ -1,0 +1,161 @@
+// kernels_metrics.hip -- per-round metrics, off the hot path.
+//
+// Appendix A states the goal as minimising the sum of the private objectives
+// at a common point and bounds the distance to consensus by sigma_2(P)^t.
+// These kernels report, in fp64 with fixed summation orders:
+//   mean_i f_i(w_i), F(w_bar) = (1/n) sum_i f_i(w_bar), ||W - 1 w_bar^T||_F and
+//   the mean of all model entries (which a doubly-stochastic reduce keeps).
+#include <cmath>
+
+#include "asap_launch.h"
+
+namespace asap {
+namespace {
+
+constexpr int kColBlocksMax = 4096;  // partials 0 .. 2*kColBlocksMax
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return __shfl(v, 0, 64);
+}
+
+// fixed-order tree over the 256 threads of a block
+__device__ double block_sum_d(double v, double* sh) {
+  sh[threadIdx.x] = v;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+    __syncthreads();
+  }
+  const double r = sh[0];
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ double model_at(const MetricArgs& a, int i, int64_t c) {
+  const double s = a.scale ? double(a.scale[i]) : 1.0;
+  return s * double(a.W[int64_t(i) * a.ld + c]);
+}
+
+// column pass: w_bar, consensus partial, mean partial
+__global__ __launch_bounds__(256) void cols_kernel(MetricArgs a) {
+  __shared__ double sh[256];
+  double cons = 0.0, msum = 0.0;
+  for (int64_t c = int64_t(blockIdx.x) * 256 + threadIdx.x; c < a.dim; c += int64_t(gridDim.x) * 256) {
+    double m = 0.0;
+    for (int i = 0; i < a.n; ++i) m += model_at(a, i, c);
+    m /= double(a.n);
+    double d2 = 0.0;
+    for (int i = 0; i < a.n; ++i) {
+      const double d = model_at(a, i, c) - m;
+      d2 += d * d;
+    }
+    a.wbar[c] = m;
+    cons += d2;
+    msum += m;
+  }
+  cons = block_sum_d(cons, sh);
+  msum = block_sum_d(msum, sh);
+  if (threadIdx.x == 0) {
+    a.part[2 * blockIdx.x] = cons;
+    a.part[2 * blockIdx.x + 1] = msum;
+  }
+}
+
+__device__ __forceinline__ double loss_of(double ym, int loss) {
+  if (loss == 1) return fmax(0.0, 1.0 - ym);
+  return fmax(-ym, 0.0) + log1p(exp(-fabs(ym)));  // softplus(-ym)
+}
+
+// one block per worker: loss at own model, loss at w_bar, ||w_i||^2
+__global__ __launch_bounds__(256) void loss_kernel(MetricArgs a, int64_t base) {
+  __shared__ double sh[256];
+  const int i = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double lown = 0.0, lbar = 0.0, nrm = 0.0;
+  for (int64_t r = wave; r < a.S; r += 4) {
+    const int64_t g = int64_t(i) * a.S + r;
+    double mo = 0.0, mb = 0.0;
+    if (a.row_ptr) {
+      const int64_t p0 = a.row_ptr[g], p1 = a.row_ptr[g + 1];
+      for (int64_t p = p0 + lane; p < p1; p += 64) {
+        const double v = a.val[p];
+        mo += v * model_at(a, i, a.col[p]);
+        mb += v * a.wbar[a.col[p]];
+      }
+    } else {
+      const float* x = a.X + g * a.ldx;
+      for (int64_t c = lane; c < a.dim; c += 64) {
+        const double v = x[c];
+        mo += v * model_at(a, i, c);
+        mb += v * a.wbar[c];
+      }
+    }
+    mo = wave_sum_d(mo);
+    mb = wave_sum_d(mb);
+    if (lane == 0) {
+      const double y = a.y[g];
+      lown += loss_of(y * mo, a.loss);
+      lbar += loss_of(y * mb, a.loss);
+    }
+  }
+  for (int64_t c = threadIdx.x; c < a.dim; c += 256) {
+    const double w = model_at(a, i, c);
+    nrm += w * w;
+  }
+  lown = block_sum_d(lown, sh);
+  lbar = block_sum_d(lbar, sh);
+  nrm = block_sum_d(nrm, sh);
+  if (threadIdx.x == 0) {
+    a.part[base + 3 * i] = lown;
+    a.part[base + 3 * i + 1] = lbar;
+    a.part[base + 3 * i + 2] = nrm;
+  }
+}
+
+__global__ __launch_bounds__(256) void finish_kernel(MetricArgs a, int ncb, int64_t base) {
+  __shared__ double sh[256];
+  double cons = 0.0, msum = 0.0, wb2 = 0.0;
+  for (int b = threadIdx.x; b < ncb; b += 256) {
+    cons += a.part[2 * b];
+    msum += a.part[2 * b + 1];
+  }
+  for (int64_t c = threadIdx.x; c < a.dim; c += 256) wb2 += a.wbar[c] * a.wbar[c];
+  cons = block_sum_d(cons, sh);
+  msum = block_sum_d(msum, sh);
+  wb2 = block_sum_d(wb2, sh);
+  double own = 0.0, bar = 0.0;
+  if (a.S > 0) {
+    for (int i = threadIdx.x; i < a.n; i += 256) {
+      own += a.part[base + 3 * i] / double(a.S) + 0.5 * double(a.l2) * a.part[base + 3 * i + 2];
+      bar += a.part[base + 3 * i + 1] / double(a.S);
+    }
+  }
+  own = block_sum_d(own, sh);
+  bar = block_sum_d(bar, sh);
+  if (threadIdx.x == 0) {
+    const double nan = __longlong_as_double(0x7ff8000000000000ll);
+    a.out[0] = a.S > 0 ? own / double(a.n) : nan;
+    a.out[1] = a.S > 0 ? bar / double(a.n) + 0.5 * double(a.l2) * wb2 : nan;
+    a.out[2] = sqrt(cons);
+    a.out[3] = msum / double(a.dim);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_metrics(const MetricArgs& a, hipStream_t s) {
+  const int ncb = int(std::min<int64_t>((a.dim + 255) / 256, kColBlocksMax));
+  const int64_t base = 2 * kColBlocksMax;
+  hipLaunchKernelGGL(cols_kernel, dim3(ncb), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (a.S > 0) {
+    hipLaunchKernelGGL(loss_kernel, dim3(a.n), dim3(256), 0, s, a, base);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(finish_kernel, dim3(1), dim3(256), 0, s, a, ncb, base);
+  return hipGetLastError();
+}
+
+}  // namespace asap

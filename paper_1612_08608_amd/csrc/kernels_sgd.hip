@@ -1,0 +1,444 @@
+// kernels_sgd.hip -- the local half-step of (A.2) (Appendix A): every worker
+// runs one pass of minibatch SGD over its own shard (Section 5), in the order
+// of this round's sample schedule.
+//
+// One workgroup owns one worker for the whole pass, because the steps of a
+// pass form a dependency chain (step k+1's margins read step k's model) and
+// a workgroup barrier is the cheapest way to order them.  The work inside a
+// step is a batched GEMV / SpMV with a rank-B' update: HBM- and
+// latency-bound, no dense contraction, so MFMA is not used.
+//
+// Determinism: every sum has a fixed order.  Margins reduce across lanes with
+// a fixed butterfly and across waves in wave order; the dense gradient sums
+// over the batch in batch order; the sparse gradient accumulates each
+// column's contributions as 64-bit fixed-point integers in an LDS hash
+// table, which is exact and therefore independent of the order in which the
+// lanes' atomics land.
+#include <cmath>
+
+#include "asap_common.h"
+#include "asap_launch.h"
+
+namespace asap {
+namespace {
+
+constexpr int kLogistic = 0;
+constexpr int kHinge = 1;
+
+// d loss(y m) / d m: logistic -y / (1 + e^{y m}); hinge -y if y m < 1 else 0.
+// Margins are accumulated in fp64 (a 4096-term fp32 dot product with a
+// wide dynamic range loses more than the 1e-5 the models are held to), and
+// the coefficient -- including the hinge decision -- is taken in fp64.
+__device__ __forceinline__ double loss_coef(double m, double y, int loss) {
+  const double ym = y * m;
+  if (loss == kHinge) return ym < 1.0 ? -y : 0.0;
+  return -y / (1.0 + exp(ym));
+}
+
+__device__ __forceinline__ double step_size(int lr_kind, float lr0, int64_t t) {
+  return lr_kind == 0 ? double(lr0) : double(lr0) / sqrt(double(t));
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return __shfl(v, 0, 64);  // every lane takes lane 0's association order
+}
+
+// ----------------------------------------------------------------------------
+// schedule
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void schedule_kernel(uint64_t seed, int64_t round, int64_t S,
+                                                       uint32_t blocks_per_worker, int32_t* out) {
+  const int worker = int(blockIdx.x / blocks_per_worker);
+  const Perm p = perm_make(seed, worker, round, uint32_t(S));
+  const int64_t pos = int64_t(blockIdx.x % blocks_per_worker) * 256 + threadIdx.x;
+  if (pos < S) out[int64_t(worker) * S + pos] = int32_t(perm_at(p, uint32_t(pos)));
+}
+
+// ----------------------------------------------------------------------------
+// dense SGD: thread t owns columns t, t+T, ..., t+(CPT-1)T and keeps that
+// slice of w in registers for the whole pass.  Samples of a step are taken
+// SB at a time: each thread loads its columns of the SB rows, the SB margins
+// are reduced over the block, and the rows (still in registers) are folded
+// into the thread's gradient slice.
+// ----------------------------------------------------------------------------
+// samples per block reduction: keep SB * CPT row values within 32 registers
+template <int CPT>
+constexpr int dense_sb() { return CPT >= 16 ? 2 : CPT >= 8 ? 4 : 8; }
+
+template <int CPT>
+__global__ __launch_bounds__(1024) void sgd_dense_kernel(SgdArgs a) {
+  constexpr int SB = dense_sb<CPT>();
+  __shared__ double part[16 * SB];
+  const int i = blockIdx.x;
+  const int T = blockDim.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = T >> 6;
+  float* wrow = a.models + int64_t(i) * a.ld;
+  const float* Xi = a.X + int64_t(i) * a.S * a.ldx;
+  const float* yi = a.y + int64_t(i) * a.S;
+  const int32_t* si = a.sched + int64_t(i) * a.S;
+  float wr[CPT];
+#pragma unroll
+  for (int q = 0; q < CPT; ++q) {
+    const int64_t c = tid + int64_t(q) * T;
+    wr[q] = c < a.dim ? wrow[c] : 0.f;
+  }
+  const int64_t K = (a.S + a.batch - 1) / a.batch;
+  for (int64_t k = 0; k < K; ++k) {
+    const int64_t b0 = k * a.batch;
+    const int Bp = int(min(int64_t(a.batch), a.S - b0));
+    const double eta = step_size(a.lr_kind, a.lr0, a.round * K + k + 1);
+    double gr[CPT];
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) gr[q] = 0.0;
+    for (int sb = 0; sb < Bp; sb += SB) {
+      float xr[SB][CPT];
+      double d[SB];
+#pragma unroll
+      for (int s = 0; s < SB; ++s) {
+        const bool ok = sb + s < Bp;
+        const float* row = Xi + int64_t(ok ? si[b0 + sb + s] : 0) * a.ldx;
+        d[s] = 0.0;
+#pragma unroll
+        for (int q = 0; q < CPT; ++q) {
+          const int64_t c = tid + int64_t(q) * T;
+          xr[s][q] = (ok && c < a.dim) ? row[c] : 0.f;
+          d[s] = fma(double(wr[q]), double(xr[s][q]), d[s]);
+        }
+      }
+      // margins: butterfly within the wave, then waves in order
+#pragma unroll
+      for (int s = 0; s < SB; ++s) d[s] = wave_sum(d[s]);
+      if (lane == 0) {
+#pragma unroll
+        for (int s = 0; s < SB; ++s) part[wave * SB + s] = d[s];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int s = 0; s < SB; ++s) {
+        double m = 0.0;
+        for (int w = 0; w < nw; ++w) m += part[w * SB + s];
+        d[s] = m;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int s = 0; s < SB; ++s) {
+        if (sb + s < Bp) {
+          const double cf = loss_coef(d[s], double(yi[si[b0 + sb + s]]), a.loss);
+#pragma unroll
+          for (int q = 0; q < CPT; ++q) gr[q] = fma(cf, double(xr[s][q]), gr[q]);
+        }
+      }
+    }
+    const double inv = 1.0 / double(Bp);
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+      const double w = wr[q];
+      wr[q] = float(w - eta * fma(gr[q], inv, double(a.l2) * w));
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < CPT; ++q) {
+    const int64_t c = tid + int64_t(q) * T;
+    if (c < a.dim) wrow[c] = wr[q];
+  }
+  if (tid == 0) {
+    a.scale[i] = 1.0f;
+    a.tag[i] = a.tag_value;
+  }
+}
+
+// ----------------------------------------------------------------------------
+// CSR SGD.
+//
+// Per step: the B' rows of the minibatch are gathered (columns, values and
+// the model entries they touch), each row's margin is reduced by one wave,
+// and each (column, c_b x) contribution is added into an LDS hash table
+// keyed by column as a 64-bit fixed-point integer.  After a barrier every
+// occupied slot writes its column once: v <- v - eta / (B' s) * sum.
+//
+// L2 regularisation uses Bottou's scale form w = s v (the SVM-SGD code the
+// paper trains with, Section 6): the dense decay (1 - eta l2) multiplies the
+// scalar s and only the touched columns of v are written.  The final s of
+// each worker is folded into the mixing weights by the reduce.
+//
+// Fast path (B' <= 64, rows <= 128 nonzeros, so at most 8192 distinct
+// columns = table size): 16 waves x 4 rows x 2 entries per lane stay in
+// registers between the gather and the table insert.  Any other step takes
+// the general path: margins first, then the contributions in row chunks of
+// at most 4096 entries, applying the table after each chunk (the update is
+// linear in the contributions, so applying it in parts is the same update).
+// ----------------------------------------------------------------------------
+constexpr int kCapBits = 13;
+constexpr int kCap = 1 << kCapBits;
+constexpr int kEmpty = -1;
+constexpr int kBMax = 512;
+constexpr int kCsrThreads = 1024;
+constexpr int kCsrWaves = kCsrThreads / 64;
+constexpr int kFastRows = 4;  // per wave; kCsrWaves * kFastRows = 64 rows
+constexpr int kFastLen = 128;
+
+struct CsrShared {
+  int keys[kCap];
+  unsigned long long acc[kCap];
+  float vold[kCap];
+  long long rs[kBMax];
+  int rl[kBMax];
+  float ry[kBMax];
+  double coef[kBMax];
+  int maxlen;
+};
+
+__device__ __forceinline__ int hash_slot(int col) {
+  return int((uint32_t(col) * 2654435761u) >> (32 - kCapBits));
+}
+
+// Add q into the slot of `col`, claiming an empty slot if the column is new.
+// The claiming lane records the pre-update model entry.
+__device__ __forceinline__ void table_add(CsrShared& sh, int col, long long q, float vold,
+                                          bool vold_valid, const float* vrow) {
+  int h = hash_slot(col);
+  for (;;) {
+    const int k = __hip_atomic_load(&sh.keys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (k == col) break;
+    if (k == kEmpty) {
+      const int old = atomicCAS(&sh.keys[h], kEmpty, col);
+      if (old == kEmpty) {
+        sh.vold[h] = vold_valid ? vold : vrow[col];
+        break;
+      }
+      if (old == col) break;
+    }
+    h = (h + 1) & (kCap - 1);
+  }
+  atomicAdd(&sh.acc[h], static_cast<unsigned long long>(q));
+}
+
+__device__ __forceinline__ void table_apply(CsrShared& sh, float* vrow, double coefA, double from_fx) {
+  for (int sl = threadIdx.x; sl < kCap; sl += kCsrThreads) {
+    const int col = sh.keys[sl];
+    if (col != kEmpty) {
+      const double G = double(static_cast<long long>(sh.acc[sl])) * from_fx;
+      vrow[col] = float(double(sh.vold[sl]) - coefA * G);
+      sh.keys[sl] = kEmpty;
+      sh.acc[sl] = 0ull;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kCsrThreads) void sgd_csr_kernel(SgdArgs a) {
+  __shared__ CsrShared sh;
+  const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float* vrow = a.models + int64_t(i) * a.ld;
+  const int64_t base = int64_t(i) * a.S;
+  const int32_t* si = a.sched + base;
+  for (int s = tid; s < kCap; s += kCsrThreads) {
+    sh.keys[s] = kEmpty;
+    sh.acc[s] = 0ull;
+  }
+  if (tid == 0) sh.maxlen = 0;
+  // Fixed point: a column collects at most B contributions of size <= vmax
+  // (|c_b| <= 1 for both losses, labels in {-1, +1}), so with
+  // B * vmax < 2^e the sum stays below 2^61 at scale 2^(61 - e).
+  int e2 = 0;
+  frexp(double(a.batch) * double(a.vmax[i]), &e2);
+  const double to_fx = ldexp(1.0, 61 - e2), from_fx = ldexp(1.0, e2 - 61);
+  double s = 1.0;  // w = s * v
+  const int64_t K = (a.S + a.batch - 1) / a.batch;
+  __syncthreads();
+  for (int64_t k = 0; k < K; ++k) {
+    const int64_t b0 = k * a.batch;
+    const int Bp = int(min(int64_t(a.batch), a.S - b0));
+    const double eta = step_size(a.lr_kind, a.lr0, a.round * K + k + 1);
+    for (int b = tid; b < Bp; b += kCsrThreads) {
+      const int64_t g = base + si[b0 + b];
+      const long long r0 = a.row_ptr[g], r1 = a.row_ptr[g + 1];
+      sh.rs[b] = r0;
+      sh.rl[b] = int(r1 - r0);
+      sh.ry[b] = a.y[g];
+      atomicMax(&sh.maxlen, int(r1 - r0));
+    }
+    __syncthreads();
+    const bool fast = Bp <= kCsrWaves * kFastRows && sh.maxlen <= kFastLen;
+    const double s_new = s * (1.0 - eta * double(a.l2));
+    const double coefA = eta / (double(Bp) * s_new);
+    if (fast) {
+      int colr[kFastRows][2];
+      float valr[kFastRows][2], vvr[kFastRows][2];
+#pragma unroll
+      for (int r = 0; r < kFastRows; ++r) {
+        const int b = wave + r * kCsrWaves;
+        const long long st = b < Bp ? sh.rs[b] : 0;
+        const int len = b < Bp ? sh.rl[b] : 0;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int pos = lane + 64 * e;
+          const bool ok = pos < len;
+          colr[r][e] = ok ? a.col[st + pos] : -1;
+          valr[r][e] = ok ? a.val[st + pos] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < kFastRows; ++r)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) vvr[r][e] = colr[r][e] >= 0 ? vrow[colr[r][e]] : 0.f;
+#pragma unroll
+      for (int r = 0; r < kFastRows; ++r) {
+        const int b = wave + r * kCsrWaves;
+        const double dot = wave_sum(fma(double(valr[r][1]), double(vvr[r][1]),
+                                        double(valr[r][0]) * double(vvr[r][0])));
+        if (b < Bp) {
+          const double cf = loss_coef(s * dot, double(sh.ry[b]), a.loss);
+#pragma unroll
+          for (int e = 0; e < 2; ++e)
+            if (colr[r][e] >= 0 && cf != 0.0)  // a zero coefficient leaves the column as it is
+              table_add(sh, colr[r][e], llrint(cf * double(valr[r][e]) * to_fx), vvr[r][e], true, vrow);
+        }
+      }
+      __syncthreads();
+      table_apply(sh, vrow, coefA, from_fx);
+      if (tid == 0) sh.maxlen = 0;
+      __syncthreads();
+    } else {
+      for (int b = wave; b < Bp; b += kCsrWaves) {
+        const long long st = sh.rs[b];
+        const int len = sh.rl[b];
+        double part = 0.0;
+        for (int pos = lane; pos < len; pos += 64)
+          part = fma(double(a.val[st + pos]), double(vrow[a.col[st + pos]]), part);
+        const double dot = wave_sum(part);
+        if (lane == 0) sh.coef[b] = loss_coef(s * dot, double(sh.ry[b]), a.loss);
+      }
+      __syncthreads();
+      if (tid == 0) sh.maxlen = 0;
+      int c0 = 0;
+      while (c0 < Bp) {
+        int c1 = c0, cnt = 0;
+        while (c1 < Bp && cnt + sh.rl[c1] <= kCap / 2) cnt += sh.rl[c1++];
+        if (c1 == c0) ++c1;  // unreachable: rows longer than kCap / 2 are refused at bind
+        for (int b = c0 + wave; b < c1; b += kCsrWaves) {
+          const long long st = sh.rs[b];
+          const int len = sh.rl[b];
+          const double cf = sh.coef[b];
+          if (cf == 0.0) continue;
+          for (int pos = lane; pos < len; pos += 64)
+            table_add(sh, a.col[st + pos], llrint(cf * double(a.val[st + pos]) * to_fx), 0.f, false, vrow);
+        }
+        __syncthreads();
+        table_apply(sh, vrow, coefA, from_fx);
+        __syncthreads();
+        c0 = c1;
+      }
+    }
+    s = s_new;
+    if (s < 1e-6) {  // fold the scale back into v before it underflows
+      const float sf = float(s);
+      for (int64_t c = tid; c < a.dim; c += kCsrThreads) vrow[c] *= sf;
+      s = 1.0;
+      __syncthreads();
+    }
+  }
+  if (tid == 0) {
+    a.scale[i] = float(s);
+    a.tag[i] = a.tag_value;
+  }
+}
+
+// ----------------------------------------------------------------------------
+// bind-time scan of the CSR shards
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void csr_scan_kernel(const int64_t* row_ptr, const int32_t* col,
+                                                       const float* val, const float* y, int64_t S,
+                                                       int64_t dim, float* vmax, int64_t* out) {
+  const int i = blockIdx.x;
+  __shared__ float smax[256];
+  __shared__ int slen[256];
+  float m = 0.f;
+  int maxlen = 0;
+  unsigned long long badcol = 0, bady = 0, badorder = 0, badptr = 0;
+  if (i == 0 && threadIdx.x == 0 && row_ptr[0] != 0) ++badptr;
+  for (int64_t r = threadIdx.x; r < S; r += 256) {
+    const int64_t g = int64_t(i) * S + r;
+    const int64_t p0 = row_ptr[g], p1 = row_ptr[g + 1];
+    if (p1 < p0 || p0 < 0) {  // entries are only read from well-formed rows
+      ++badptr;
+      continue;
+    }
+    maxlen = max(maxlen, int(min<int64_t>(p1 - p0, 1 << 30)));
+    const float yy = y[g];
+    bady += (yy != 1.0f && yy != -1.0f);
+    int prev = -1;
+    for (int64_t p = p0; p < p1; ++p) {
+      const int c = col[p];
+      badcol += (c < 0 || c >= dim);
+      badorder += (c <= prev);
+      prev = c;
+      m = fmaxf(m, fabsf(val[p]));
+    }
+  }
+  smax[threadIdx.x] = m;
+  slen[threadIdx.x] = maxlen;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) {
+      smax[threadIdx.x] = fmaxf(smax[threadIdx.x], smax[threadIdx.x + o]);
+      slen[threadIdx.x] = max(slen[threadIdx.x], slen[threadIdx.x + o]);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    vmax[i] = smax[0];
+    atomicMax(reinterpret_cast<unsigned long long*>(&out[0]), static_cast<unsigned long long>(slen[0]));
+  }
+  if (badcol) atomicAdd(reinterpret_cast<unsigned long long*>(&out[1]), badcol);
+  if (bady) atomicAdd(reinterpret_cast<unsigned long long*>(&out[2]), bady);
+  if (badorder) atomicAdd(reinterpret_cast<unsigned long long*>(&out[3]), badorder);
+  if (badptr) atomicAdd(reinterpret_cast<unsigned long long*>(&out[4]), badptr);
+}
+
+}  // namespace
+
+hipError_t launch_schedule(uint64_t seed, int64_t round, int32_t n, int64_t S, int32_t* out,
+                           hipStream_t s) {
+  if (S <= 0 || n <= 0) return hipSuccess;
+  const uint64_t bx = uint64_t((S + 255) / 256);
+  if (bx * uint64_t(n) >= (1ull << 31)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(schedule_kernel, dim3(uint32_t(bx * uint64_t(n))), dim3(256), 0, s, seed, round, S,
+                     uint32_t(bx), out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s) {
+  int T = int(std::min<int64_t>(1024, (a.dim + 63) / 64 * 64));
+  const int64_t need = (a.dim + T - 1) / T;
+  const dim3 grid{uint32_t(a.n)}, block{uint32_t(T)};
+  if (need <= 1)
+    hipLaunchKernelGGL(sgd_dense_kernel<1>, grid, block, 0, s, a);
+  else if (need <= 2)
+    hipLaunchKernelGGL(sgd_dense_kernel<2>, grid, block, 0, s, a);
+  else if (need <= 4)
+    hipLaunchKernelGGL(sgd_dense_kernel<4>, grid, block, 0, s, a);
+  else if (need <= 8)
+    hipLaunchKernelGGL(sgd_dense_kernel<8>, grid, block, 0, s, a);
+  else if (need <= 16)
+    hipLaunchKernelGGL(sgd_dense_kernel<16>, grid, block, 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s) {
+  if (a.batch > kBMax) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sgd_csr_kernel, dim3(uint32_t(a.n)), dim3(kCsrThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_csr_scan(const int64_t* row_ptr, const int32_t* col, const float* val,
+                           const float* y, int32_t n, int64_t S, int64_t dim, float* vmax,
+                           int64_t* out, hipStream_t s) {
+  hipLaunchKernelGGL(csr_scan_kernel, dim3(uint32_t(n)), dim3(256), 0, s, row_ptr, col, val, y, S, dim,
+                     vmax, out);
+  return hipGetLastError();
+}
+
+}  // namespace asap

@@ -1,0 +1,172 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, its
+host-only builders match the oracle bit for bit, and argument/state errors are
+reported before any device work (no GPU needed)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1612_08608_amd import asap
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built_library():
+    if not os.path.exists(asap._LIB_PATH):
+        from paper_1612_08608_amd import build
+        build.build()
+    return asap.lib()
+
+
+def test_exports_every_declared_symbol():
+    with open(os.path.join(ROOT, "include", "asap.h")) as f:
+        header = f.read()
+    declared = set(re.findall(r"^\s*(?:const\s+char\s*\*|void|asap_status)\s+(asap_\w+)\s*\(", header, re.M))
+    assert declared == set(asap.EXPORTS), declared ^ set(asap.EXPORTS)
+    L = asap.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+@pytest.mark.parametrize("n", [3, 4, 5, 8, 64, 1024])
+def test_ring_bit_identical(n):
+    p, i = asap.asap_graph_ring(n)
+    po, io = oracle.graphs.ring(n)
+    assert np.array_equal(p, po) and np.array_equal(i, io)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 7, 256])
+def test_complete_bit_identical(n):
+    p, i = asap.asap_graph_complete(n)
+    po, io = oracle.graphs.complete(n)
+    assert np.array_equal(p, po) and np.array_equal(i, io)
+    w = asap.asap_metropolis_weights(p, i)
+    assert np.array_equal(w.view(np.uint32), oracle.graphs.metropolis_weights(po, io).view(np.uint32))
+
+
+@pytest.mark.parametrize("n,d,seed", [(64, 4, 0), (256, 8, 0), (32, 6, 0), (1024, 2, 0), (1024, 4, 0),
+                                      (1024, 8, 0), (1024, 16, 0), (10, 9, 3), (64, 4, 12345), (2, 1, 7), (5, 2, 1)])
+def test_random_regular_and_weights_bit_identical(n, d, seed):
+    if (n * d) % 2:
+        pytest.skip("n*d odd")
+    p, i = asap.asap_graph_random_regular(n, d, seed)
+    po, io = oracle.graphs.random_regular(n, d, seed)
+    assert np.array_equal(p, po) and np.array_equal(i, io)
+    w = asap.asap_metropolis_weights(p, i)
+    wo = oracle.graphs.metropolis_weights(po, io)
+    assert np.array_equal(w.view(np.uint32), wo.view(np.uint32))
+
+
+def test_metropolis_irregular_bit_identical():
+    rng = np.random.default_rng(4)
+    n = 40
+    A = rng.random((n, n)) < 0.15
+    A = A | A.T
+    np.fill_diagonal(A, True)
+    ptr = np.concatenate([[0], np.cumsum(A.sum(1))]).astype(np.int32)
+    idx = np.concatenate([np.nonzero(A[r])[0] for r in range(n)]).astype(np.int32)
+    w = asap.asap_metropolis_weights(ptr, idx)
+    assert np.array_equal(w.view(np.uint32), oracle.graphs.metropolis_weights(ptr, idx).view(np.uint32))
+
+
+@pytest.mark.parametrize("S", [0, 1, 2, 3, 17, 1000, 1024, 8192, 20480, 65536, 100003])
+def test_schedule_bit_identical(S):
+    for seed, worker, rnd in ((0, 0, 0), (0, 63, 49), (7, 5, 3), (2**63 + 11, 255, 1 << 40)):
+        assert np.array_equal(asap.asap_schedule(S, seed, worker, rnd), oracle.prng.schedule(S, seed, worker, rnd))
+
+
+def test_builder_argument_errors():
+    for call in (lambda: asap.asap_graph_ring(2), lambda: asap.asap_graph_complete(0),
+                 lambda: asap.asap_graph_random_regular(5, 3, 0), lambda: asap.asap_graph_random_regular(4, 4, 0),
+                 lambda: asap.asap_graph_random_regular(6, 1, 0),
+                 lambda: asap.asap_schedule(-1, 0, 0, 0)):
+        with pytest.raises(asap.AsapError) as e:
+            call()
+        assert e.value.status == asap.E_INVALID_ARG
+    assert "ring" in asap.asap_last_error(None) or asap.asap_last_error(None)
+
+
+def _ring(n=8):
+    p, i = asap.asap_graph_ring(n)
+    return p, i, asap.asap_metropolis_weights(p, i)
+
+
+def test_create_validates_graph():
+    p, i, w = _ring()
+    ctx = asap.asap_create(8, 100, p, i, w)
+    asap.asap_destroy(ctx)
+    bad = [
+        (p, i, w * 1.01),                                    # rows sum to 1.01
+        (p, np.where(i == 0, 1, i), w),                      # row 0 loses self / repeats
+        (p, i, np.where(np.arange(w.size) == 0, -w, w)),     # negative weight
+        (np.concatenate([[1], p[1:]]), i, w),                # ptr[0] != 0
+        (p, np.where(i == 7, 8, i), w),                      # out of range
+    ]
+    for pp, ii, ww in bad:
+        with pytest.raises(asap.AsapError) as e:
+            asap.asap_create(8, 100, pp, ii, ww)
+        assert e.value.status == asap.E_GRAPH
+    # a row-stochastic but not column-stochastic P is refused unless allowed
+    pp = np.array([0, 2, 4, 5], np.int32)
+    ii = np.array([0, 1, 0, 1, 2], np.int32)
+    ww = np.array([0.5, 0.5, 0.5, 0.5, 1.0], np.float32)
+    pp2 = np.array([0, 2, 4, 6], np.int32)
+    ii2 = np.array([0, 1, 0, 1, 0, 2], np.int32)
+    ww2 = np.array([0.5, 0.5, 0.5, 0.5, 0.5, 0.5], np.float32)
+    with pytest.raises(asap.AsapError):
+        asap.asap_create(3, 10, pp2, ii2, ww2)
+    ctx = asap.asap_create(3, 10, pp2, ii2, ww2, asap.ALLOW_NON_DS)
+    asap.asap_destroy(ctx)
+    ctx = asap.asap_create(3, 10, pp, ii, ww)
+    asap.asap_destroy(ctx)
+    for n, dim in ((0, 10), (8, 0)):
+        with pytest.raises(asap.AsapError) as e:
+            asap.asap_create(n, dim, p, i, w)
+        assert e.value.status == asap.E_INVALID_ARG
+
+
+def test_state_errors_before_device_work():
+    p, i, w = _ring()
+    ctx = asap.asap_create(8, 100, p, i, w)
+    try:
+        prm = asap.sgd_params(batch=4)
+        for call in (lambda: asap.asap_local_sgd(ctx, prm, stream=0),
+                     lambda: asap.asap_stochastic_reduce(ctx, stream=0),
+                     lambda: asap.asap_round(ctx, prm, stream=0)):
+            with pytest.raises(asap.AsapError) as e:
+                call()
+            assert e.value.status == asap.E_STATE
+        fake = 1 << 40
+        with pytest.raises(asap.AsapError) as e:      # misaligned buffer
+            asap.asap_bind_models(ctx, fake + 4, fake + 1 << 20, 128, stream=0)
+        assert e.value.status == asap.E_INVALID_ARG
+        with pytest.raises(asap.AsapError) as e:      # ld not a multiple of 64
+            asap.asap_bind_models(ctx, fake, fake + (1 << 20), 100, stream=0)
+        assert e.value.status == asap.E_INVALID_ARG
+        asap.asap_bind_models(ctx, fake, fake + (1 << 20), 128, stream=0)
+        assert asap.asap_current(ctx) == (0, 0, 0)
+        with pytest.raises(asap.AsapError) as e:      # workspace still missing
+            asap.asap_local_sgd(ctx, prm, stream=0)
+        assert e.value.status == asap.E_STATE
+        ws0 = asap.asap_workspace_size(ctx)
+        asap.asap_bind_csr(ctx, fake, fake, fake, fake, 1000, stream=0)
+        assert asap.asap_workspace_size(ctx) >= ws0 + 8 * 1000 * 4   # room for the schedule
+        with pytest.raises(asap.AsapError) as e:
+            asap.asap_bind_workspace(ctx, fake, 16, stream=0)        # too small
+        assert e.value.status == asap.E_INVALID_ARG
+    finally:
+        asap.asap_destroy(ctx)
+
+
+def test_dense_dim_limit():
+    p, i, w = _ring()
+    ctx = asap.asap_create(8, 20000, p, i, w)
+    try:
+        with pytest.raises(asap.AsapError) as e:
+            asap.asap_bind_dense(ctx, 1 << 40, 1 << 41, 10, 20000)
+        assert e.value.status == asap.E_INVALID_ARG
+    finally:
+        asap.asap_destroy(ctx)

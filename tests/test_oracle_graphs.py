@@ -87,7 +87,7 @@ def test_random_regular_deterministic_and_seeded():
 
 
 def test_random_regular_rejects_bad_args():
-    for n, d in ((5, 3), (4, 4), (4, 0)):
+    for n, d in ((5, 3), (4, 4), (4, 0), (6, 1)):
         with pytest.raises(ValueError):
             graphs.random_regular(n, d, 0)
 
