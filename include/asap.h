@@ -162,12 +162,16 @@ asap_status asap_bind_dense(asap_ctx* ctx, const float* X, const float* y,
                             int64_t samples, int64_t ldx);
 
 /* Bind CSR shards with global offsets: worker i owns rows [i*S, (i+1)*S);
- * row_ptr [n*S+1] int64 (row_ptr[0] = 0), col [nnz] int32 in [0, dim),
- * unique within a row, val [nnz] fp32, y [n*S] fp32 in {-1, +1}.  Scans the
- * shards on `stream` and synchronises it once: rows may hold at most 4096
- * nonzeros.  Errors: ASAP_E_INVALID_ARG. */
+ * row_ptr [n*S+1] int64 (row_ptr[0] = 0, non-decreasing, row_ptr[n*S] =
+ * nnz), col [nnz] int32 in [0, dim) strictly ascending within a row, val
+ * [nnz] fp32, y [n*S] fp32 in {-1, +1}; dim < 2^30 and fewer than 2^30
+ * nonzeros per worker.  The next
+ * asap_bind_workspace scans the shards (synchronising its stream) and
+ * rejects violations with ASAP_E_INVALID_ARG; rows may hold at most 4096
+ * nonzeros.  It also ranks the columns by frequency: the most frequent
+ * (up to 8128) are kept in on-chip memory during each SGD pass. */
 asap_status asap_bind_csr(asap_ctx* ctx, const int64_t* row_ptr, const int32_t* col,
-                          const float* val, const float* y, int64_t samples,
+                          const float* val, const float* y, int64_t samples, int64_t nnz,
                           void* stream);
 
 /* Half-step of (A.2) for all workers: worker i runs one pass of minibatch

@@ -71,7 +71,7 @@ def lib():
         "asap_bind_workspace": [p, p, sz, p],
         "asap_bind_models": [p, p, p, i64, p],
         "asap_bind_dense": [p, p, p, i64, i64],
-        "asap_bind_csr": [p, p, p, p, p, i64, p],
+        "asap_bind_csr": [p, p, p, p, p, i64, i64, p],
         "asap_local_sgd": [p, C.POINTER(SgdParams), p],
         "asap_stochastic_reduce": [p, p],
         "asap_round": [p, C.POINTER(SgdParams), p],
@@ -196,8 +196,8 @@ def asap_bind_dense(ctx, X, y, samples: int, ldx: int):
     _check(lib().asap_bind_dense(ctx, _dev(X), _dev(y), samples, ldx), ctx)
 
 
-def asap_bind_csr(ctx, row_ptr, col, val, y, samples: int, stream=None):
-    _check(lib().asap_bind_csr(ctx, _dev(row_ptr), _dev(col), _dev(val), _dev(y), samples,
+def asap_bind_csr(ctx, row_ptr, col, val, y, samples: int, nnz: int, stream=None):
+    _check(lib().asap_bind_csr(ctx, _dev(row_ptr), _dev(col), _dev(val), _dev(y), samples, nnz,
                                _stream(stream)), ctx)
 
 
@@ -311,7 +311,7 @@ class Session:
         vl = t.as_tensor(np.asarray(val, np.float32)).to(self.device)
         yy = t.as_tensor(np.asarray(y, np.float32)).to(self.device)
         self._keep += [rp, cl, vl, yy]
-        asap_bind_csr(self.ctx, rp, cl, vl, yy, samples)
+        asap_bind_csr(self.ctx, rp, cl, vl, yy, samples, int(cl.numel()))
         self.ws = None
 
     def ready(self, stream=None):

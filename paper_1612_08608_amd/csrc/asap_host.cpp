@@ -51,11 +51,17 @@ struct asap_ctx {
   const int64_t* row_ptr = nullptr;
   const int32_t* col = nullptr;
   const float* val = nullptr;
+  int64_t nnz = 0;
+
+  // CSR: columns kept in LDS by the SGD kernel (chosen at workspace bind)
+  std::vector<int32_t> hot_cols;
+  std::vector<int16_t> hot_lut;
+  int32_t max_row = 0;
 
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
-         off_vmax = 0, off_scan = 0, off_sched = 0, off_wbar = 0, off_part = 0, off_out = 0,
-         total = 0;
+         off_vmax = 0, off_scan = 0, off_sched = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
+         off_rowinfo = 0, off_code = 0, off_lut = 0, off_hot = 0, total = 0;
 
   // round state
   int32_t cur = 0;
@@ -102,10 +108,16 @@ void layout(asap_ctx* c) {
   c->off_err = o;   o = align_up(o + kErrWords * 4);
   c->off_vmax = o;  o = align_up(o + n * 4);
   c->off_scan = o;  o = align_up(o + 8 * 8);
+  c->off_rowok = o; o = align_up(o + n * 4);
   c->off_sched = o; o = align_up(o + n * size_t(c->S) * 4);
   c->off_wbar = o;  o = align_up(o + size_t(c->dim) * 8);
   c->off_part = o;  o = align_up(o + (2 * 4096 + 3 * n) * 8);
   c->off_out = o;   o = align_up(o + 8 * 8);
+  const bool csr = c->kind == kCsr;
+  c->off_rowinfo = o; o = align_up(o + (csr ? n * size_t(c->S) * sizeof(RowInfo) : 0));
+  c->off_code = o;    o = align_up(o + (csr ? size_t(c->nnz) * 4 : 0));
+  c->off_lut = o;     o = align_up(o + (csr ? size_t(c->dim) * 2 : 0));
+  c->off_hot = o;     o = align_up(o + (csr ? size_t(kHotMax) * 4 : 0));
   c->total = o;
 }
 
@@ -189,6 +201,41 @@ asap_status check_params(asap_ctx* c, const asap_sgd_params* p) {
   if (c->kind == kCsr && p->batch > 512)
     return fail(c, ASAP_E_INVALID_ARG, "CSR minibatch is limited to 512 rows");
   if (p->reserved != 0) return fail(c, ASAP_E_INVALID_ARG, "reserved must be 0");
+  return ASAP_OK;
+}
+
+// The CSR kernel keeps the model entries of the most frequent columns in LDS
+// for a whole pass.  Frequencies come from every 2^k-th nonzero (a sample
+// large enough to rank the heavy columns); ties break by column index so the
+// choice is deterministic.  Every nonzero then gets its code: -(slot + 2)
+// for a hot column, the column itself otherwise.
+asap_status choose_hot_columns(asap_ctx* c, hipStream_t s) {
+  hipError_t e;
+  const int64_t D = c->dim;
+  int32_t* counts = at<int32_t>(c, c->off_wbar);  // the metric buffer is free at bind time
+  int64_t stride = 1;
+  while (c->nnz / stride > (int64_t(1) << 24)) stride *= 2;
+  std::vector<int32_t> h(size_t(D), 0);
+  if ((e = launch_fill_i32(counts, D, 0, s)) || (e = launch_col_hist(c->col, c->nnz, stride, counts, s)) ||
+      (e = hipMemcpyAsync(h.data(), counts, size_t(D) * 4, hipMemcpyDeviceToHost, s)) ||
+      (e = hipStreamSynchronize(s)))
+    return hip_fail(c, e, "column histogram");
+  std::vector<int32_t> cols;
+  for (int64_t j = 0; j < D; ++j)
+    if (h[j] > 0) cols.push_back(int32_t(j));
+  const size_t H = std::min<size_t>(cols.size(), kHotMax);
+  std::partial_sort(cols.begin(), cols.begin() + H, cols.end(), [&](int32_t x, int32_t y) {
+    return h[x] != h[y] ? h[x] > h[y] : x < y;
+  });
+  c->hot_cols.assign(cols.begin(), cols.begin() + H);
+  c->hot_lut.assign(size_t(D), int16_t(-1));
+  for (size_t k = 0; k < H; ++k) c->hot_lut[c->hot_cols[k]] = int16_t(k);
+  int16_t* lut = at<int16_t>(c, c->off_lut);
+  if ((H && (e = hipMemcpyAsync(at<int32_t>(c, c->off_hot), c->hot_cols.data(), H * 4, hipMemcpyHostToDevice, s))) ||
+      (e = hipMemcpyAsync(lut, c->hot_lut.data(), size_t(D) * 2, hipMemcpyHostToDevice, s)) ||
+      (e = launch_codes(c->col, c->nnz, lut, at<int32_t>(c, c->off_code), s)) ||
+      (e = hipStreamSynchronize(s)))
+    return hip_fail(c, e, "hot column tables");
   return ASAP_OK;
 }
 
@@ -414,13 +461,16 @@ extern "C" asap_status asap_bind_dense(asap_ctx* c, const float* X, const float*
 }
 
 extern "C" asap_status asap_bind_csr(asap_ctx* c, const int64_t* row_ptr, const int32_t* col,
-                                     const float* val, const float* y, int64_t S, void* stream) {
+                                     const float* val, const float* y, int64_t S, int64_t nnz,
+                                     void* stream) {
   (void)stream;
   if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
-  if (!row_ptr || !col || !val || !y) return fail(c, ASAP_E_INVALID_ARG, "NULL data pointer");
+  if (!row_ptr || !y || (nnz > 0 && (!col || !val))) return fail(c, ASAP_E_INVALID_ARG, "NULL data pointer");
+  if (nnz < 0) return fail(c, ASAP_E_INVALID_ARG, "nnz must be >= 0");
   if (S < 1 || S >= (int64_t(1) << 31)) return fail(c, ASAP_E_INVALID_ARG, "samples must be in [1, 2^31)");
-  if (c->dim >= (int64_t(1) << 31)) return fail(c, ASAP_E_INVALID_ARG, "CSR path needs dim < 2^31");
+  if (c->dim >= (int64_t(1) << 30)) return fail(c, ASAP_E_INVALID_ARG, "CSR path needs dim < 2^30");
   c->kind = kCsr;
+  c->nnz = nnz;
   c->row_ptr = row_ptr;
   c->col = col;
   c->val = val;
@@ -469,6 +519,17 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     if (h[2]) return fail(c, ASAP_E_INVALID_ARG, "%lld labels outside {-1, +1}", (long long)h[2]);
     if (h[3]) return fail(c, ASAP_E_INVALID_ARG, "%lld CSR rows with unsorted or repeated columns", (long long)h[3]);
     if (h[0] > 4096) return fail(c, ASAP_E_INVALID_ARG, "a CSR row holds %lld > 4096 nonzeros", (long long)h[0]);
+    if (h[5] >= (int64_t(1) << 30))
+      return fail(c, ASAP_E_INVALID_ARG, "a worker holds %lld >= 2^30 nonzeros", (long long)h[5]);
+    int64_t last = 0;
+    if ((e = hipMemcpyAsync(&last, c->row_ptr + int64_t(c->n) * c->S, 8, hipMemcpyDeviceToHost, s)) ||
+        (e = hipStreamSynchronize(s)))
+      return hip_fail(c, e, "row_ptr readback");
+    if (last != c->nnz)
+      return fail(c, ASAP_E_INVALID_ARG, "row_ptr[n*S] = %lld but nnz = %lld", (long long)last, (long long)c->nnz);
+    c->max_row = int32_t(h[0]);
+    asap_status hs = choose_hot_columns(c, s);
+    if (hs != ASAP_OK) return hs;
   }
   c->tags_ready = true;
   return ASAP_OK;
@@ -505,8 +566,17 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
   a.scale = at<float>(c, c->off_scale);
   a.tag = at<int64_t>(c, c->off_tag) + size_t(c->cur) * c->n;
   a.tag_value = tag_half(c->round);
+  a.rowinfo = at<RowInfo>(c, c->off_rowinfo);
+  a.code = at<int32_t>(c, c->off_code);
+  a.hot_cols = at<int32_t>(c, c->off_hot);
+  a.n_hot = int32_t(c->hot_cols.size());
+  a.max_row = c->max_row;
   hipError_t e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->off_sched), s);
   if (e != hipSuccess) return hip_fail(c, e, "schedule kernel");
+  if (c->kind == kCsr) {
+    e = launch_rowinfo(a.sched, c->row_ptr, c->y, c->n, c->S, at<RowInfo>(c, c->off_rowinfo), s);
+    if (e != hipSuccess) return hip_fail(c, e, "row descriptor kernel");
+  }
   e = (c->kind == kDense) ? launch_sgd_dense(a, s) : launch_sgd_csr(a, s);
   if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
   c->half_done = true;
@@ -535,7 +605,9 @@ extern "C" asap_status asap_stochastic_reduce(asap_ctx* c, void* stream) {
   a.expect = c->half_done ? tag_half(c->round) : tag_start(c->round);
   a.next = tag_start(c->round + 1);
   a.err = at<int32_t>(c, c->off_err);
-  hipError_t e = c->complete_uniform ? launch_mean(a, s) : launch_mix(a, s);
+  a.row_ok = at<int32_t>(c, c->off_rowok);
+  hipError_t e = launch_epoch_check(a, s);
+  if (e == hipSuccess) e = c->complete_uniform ? launch_mean(a, s) : launch_mix(a, s);
   if (e != hipSuccess) return hip_fail(c, e, "reduce kernel");
   c->cur ^= 1;
   c->round += 1;

@@ -29,10 +29,22 @@ struct MixArgs {
   int64_t expect;  // tag every in-neighbour must carry in buffer e
   int64_t next;    // tag written for every reduced row in buffer e^1
   int32_t* err;
+  int32_t* row_ok;  // [n] verdict of the epoch check (1 = every in-neighbour published)
 };
 
+hipError_t launch_epoch_check(const MixArgs& a, hipStream_t s);
 hipError_t launch_mix(const MixArgs& a, hipStream_t s);
 hipError_t launch_mean(const MixArgs& a, hipStream_t s);
+
+// Row descriptor of one minibatch position, in schedule order.
+struct RowInfo {
+  long long start;  // offset of the row's first nonzero
+  int len;          // nonzeros in the row
+  float y;          // label
+};
+
+// Columns whose model entries the CSR kernel keeps in LDS for a whole pass.
+constexpr int kHotMax = 8128;
 
 struct SgdArgs {
   float* models;  // current buffer [n][ld]
@@ -48,6 +60,11 @@ struct SgdArgs {
   const int32_t* col;
   const float* val;
   const float* vmax;       // [n] max |val| per worker
+  const RowInfo* rowinfo;  // [n][S] this round's rows in schedule order
+  const int32_t* code;     // [nnz] -(hot slot + 2) for a hot column, else the column
+  const int32_t* hot_cols; // [n_hot] column of each hot slot
+  int32_t n_hot;
+  int32_t max_row;         // longest row (nonzeros)
   // schedule of this round, [n][S]
   const int32_t* sched;
   int32_t loss, lr_kind;
@@ -63,12 +80,17 @@ hipError_t launch_schedule(uint64_t seed, int64_t round, int32_t n, int64_t S, i
                            hipStream_t s);
 hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s);
 hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s);
+hipError_t launch_rowinfo(const int32_t* sched, const int64_t* row_ptr, const float* y, int32_t n, int64_t S,
+                          RowInfo* out, hipStream_t s);
+hipError_t launch_col_hist(const int32_t* col, int64_t nnz, int64_t stride, int32_t* counts, hipStream_t s);
+hipError_t launch_codes(const int32_t* col, int64_t nnz, const int16_t* lut, int32_t* code, hipStream_t s);
 
 // Bind-time scan of CSR shards: vmax[i] = max |val| of worker i; out[0] =
 // max row length, out[1] = count of columns outside [0, dim), out[2] =
 // count of labels outside {-1, +1}, out[3] = count of rows with unsorted or
 // repeated columns, out[4] = count of rows whose offsets decrease or are
-// negative (plus one if row_ptr[0] != 0).  out must be zeroed before.
+// negative (plus one if row_ptr[0] != 0), out[5] = most nonzeros of one
+// worker.  out must be zeroed before.
 hipError_t launch_csr_scan(const int64_t* row_ptr, const int32_t* col, const float* val,
                            const float* y, int32_t n, int64_t S, int64_t dim, float* vmax,
                            int64_t* out, hipStream_t s);

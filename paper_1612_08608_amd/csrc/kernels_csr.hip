@@ -1,0 +1,598 @@
+// kernels_csr.hip -- local SGD pass on CSR shards (Appendix A, update (A.2),
+// first line; Section 5: each replica trains on its own data partition).
+//
+// One workgroup (1024 threads) runs one worker's whole pass: the steps form
+// a dependency chain through the model, and a workgroup barrier is the
+// cheapest way to order them.  A step is bound by latency, so the kernel is
+// organised around taking global round trips off that chain:
+//
+//  * Hot columns in LDS.  The most frequent columns of the data (chosen once
+//    at bind time) keep their model entries in LDS for the whole pass and are
+//    written back at the end.  A bind-time array gives every nonzero its
+//    "code": -(slot + 2) for a hot column, the column itself for a cold one.
+//  * Software pipeline.  While step k computes, the row descriptors of step
+//    k+3, the nonzeros (code, val) of step k+2 and the cold model entries of
+//    step k+1 are loaded.  Nothing computes on a loaded value before the next
+//    step, so no load is waited for inside the step that issues it.  The cold
+//    entries of step k+1 are read before step k writes its updates; step k+1
+//    patches them from step k's cold table, which keeps the post-update value
+//    of every column it changed.
+//  * Cold tables are bucketed (four keys read with one 128-bit LDS load).
+//  * The barrier between gradient and update orders LDS only, so loads stay
+//    in flight across it; the end-of-step barrier is a full fence.
+//
+// Determinism: a row's margin is summed over a fixed 16-lane tree in fp64;
+// each column's gradient is accumulated as an exact 64-bit fixed-point
+// integer (integer LDS atomics commute).
+//
+// A step whose minibatch has more than 64 rows, a row with more than 16*E
+// nonzeros, or more than 3/4 of the cold table in cold nonzeros takes the
+// general path: margins first, then contributions in row chunks, applied
+// chunk by chunk (the update is linear in the contributions).
+#include <cmath>
+
+#include "asap_launch.h"
+
+namespace asap {
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+constexpr int kRowLanes = 16;                        // lanes per row on the fast path
+constexpr int kFastRows = kWaves * 64 / kRowLanes;   // 64 rows per step
+constexpr int kCold = 2048;                          // cold table slots
+constexpr int kBucket = 4;
+constexpr int kBucketBits = 9;
+constexpr int kBuckets = kCold / kBucket;
+constexpr int kEmpty = -1;
+constexpr int kBMax = 512;
+constexpr int kChunkPairs = kCold / 2;               // general path: nonzeros per chunk
+constexpr int kColdFast = kCold * 3 / 4;             // fast path: cold nonzeros per step
+static_assert(kBuckets == 1 << kBucketBits, "bucket count");
+
+struct ColdTable {
+  int key[kCold];  // bucket b is key[4b .. 4b+3], filled in slot order
+  unsigned long long acc[kCold];
+  float val[kCold];  // pre-update value until applied, then the post-update value
+};
+
+struct Shared {
+  float vhot[kHotMax];
+  unsigned long long acch[kHotMax];
+  ColdTable cold[2];
+  int stats[3][2];  // per step (mod 3): cold nonzeros, rows over the fast length
+};
+static_assert(sizeof(Shared) <= 160 * 1024, "LDS budget of one workgroup");
+static_assert(kBMax <= kCold, "general-path coefficients fit a cold table's accumulators");
+
+// Raw buffer resources over one worker's arrays: 32-bit byte offsets keep a
+// lane's address in one register, and offsets past the end read 0.
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family raw buffer
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), kRsrcWord3);
+}
+__device__ __forceinline__ int ld_i32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ float ld_f32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ void st_f32(__amdgpu_buffer_rsrc_t r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, off, 0, 0);
+}
+
+// Buffer views of one worker: nonzeros [seg, seg + nnz_w) and its model row.
+struct Views {
+  __amdgpu_buffer_rsrc_t code, val, model;
+  long long seg;
+};
+
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// d loss(y m) / d m from an fp64 margin: the hinge decision y m < 1 is taken
+// in fp64; the logistic factor 1 / (1 + e^{y m}) needs only fp32 accuracy.
+__device__ __forceinline__ double loss_coef(double m, double y, int loss) {
+  const double ym = y * m;
+  if (loss == 1) return ym < 1.0 ? -y : 0.0;
+  return -y / double(1.0f + expf(float(ym)));
+}
+
+__device__ __forceinline__ double step_size(int lr_kind, float lr0, int64_t t) {
+  return lr_kind == 0 ? double(lr0) : double(lr0) / sqrt(double(t));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane gets the same bits (each
+// stage adds the same two operands in swapped order).
+__device__ __forceinline__ double row16_sum(double v) {
+#define ASAP_DPP_STAGE(ctrl)                                                                    \
+  {                                                                                             \
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), ctrl, 0xF, 0xF, false);   \
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), ctrl, 0xF, 0xF, false);   \
+    v += __hiloint2double(hi, lo);                                                              \
+  }
+  ASAP_DPP_STAGE(0xB1)   // quad_perm [1,0,3,2]
+  ASAP_DPP_STAGE(0x4E)   // quad_perm [2,3,0,1]
+  ASAP_DPP_STAGE(0x141)  // row_half_mirror
+  ASAP_DPP_STAGE(0x140)  // row_mirror
+#undef ASAP_DPP_STAGE
+  return v;
+}
+
+__device__ __forceinline__ int row16_sum_i(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ int cold_bucket(int col) {
+  return int((uint32_t(col) * 2654435761u) >> (32 - kBucketBits));
+}
+
+typedef int int4v __attribute__((ext_vector_type(4)));
+
+// The four keys of bucket b in one 128-bit LDS read, for a table that no
+// lane is writing.
+__device__ __forceinline__ int4v bucket_keys(const ColdTable& t, int b) {
+  return *reinterpret_cast<const int4v*>(&t.key[b * kBucket]);
+}
+
+// The same keys while other lanes may be claiming slots: each key is read
+// with a relaxed workgroup-scope atomic load, so a retry sees new claims.
+__device__ __forceinline__ int4v bucket_keys_live(ColdTable& t, int b) {
+  int* k = &t.key[b * kBucket];
+  int4v r;
+  r.x = __hip_atomic_load(k + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  r.y = __hip_atomic_load(k + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  r.z = __hip_atomic_load(k + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  r.w = __hip_atomic_load(k + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  return r;
+}
+
+// Slot of `col` in a table nobody is writing, or -1.  Buckets fill in slot
+// order and are probed in order, so a bucket with a free slot ends the search.
+__device__ __forceinline__ int cold_find(const ColdTable& t, int col) {
+  int b = cold_bucket(col);
+  for (int n = 0; n < kBuckets; ++n) {
+    const int4v k = bucket_keys(t, b);
+    if (k.x == col) return b * kBucket;
+    if (k.y == col) return b * kBucket + 1;
+    if (k.z == col) return b * kBucket + 2;
+    if (k.w == col) return b * kBucket + 3;
+    if (k.w == kEmpty) return -1;
+    b = (b + 1) & (kBuckets - 1);
+  }
+  return -1;
+}
+
+// Value of `col` after the step that filled table t, or `fallback`.
+__device__ __forceinline__ float cold_patch(const ColdTable& t, int col, float fallback) {
+  const int sl = cold_find(t, col);
+  return sl < 0 ? fallback : t.val[sl];
+}
+
+// Add q into col's slot, claiming the first free slot of its bucket chain if
+// the column is new; the claiming lane records the pre-update value.
+__device__ __forceinline__ void cold_add(ColdTable& t, int col, long long q, float vold) {
+  int b = cold_bucket(col);
+  int sl = -1;
+  for (int n = 0; n < 4 * kBuckets && sl < 0; ++n) {
+    const int4v k = bucket_keys_live(t, b);
+    const int kk[kBucket] = {k.x, k.y, k.z, k.w};
+    int empty = -1;
+#pragma unroll
+    for (int s = 0; s < kBucket; ++s) {
+      if (sl < 0 && kk[s] == col) sl = b * kBucket + s;
+      if (empty < 0 && kk[s] == kEmpty) empty = s;
+    }
+    if (sl >= 0) break;
+    if (empty < 0) {
+      b = (b + 1) & (kBuckets - 1);
+      continue;
+    }
+    const int old = atomicCAS(&t.key[b * kBucket + empty], kEmpty, col);
+    if (old == kEmpty) {
+      sl = b * kBucket + empty;
+      t.val[sl] = vold;
+    } else if (old == col) {
+      sl = b * kBucket + empty;
+    }  // else another column took the slot: read the bucket again
+  }
+  if (sl >= 0) atomicAdd(&t.acc[sl], static_cast<unsigned long long>(q));
+}
+
+// Apply a cold table: v = vold - coefA * sum for every claimed column, stored
+// to the model and kept in the table; the slot is cleared when `clear`.
+__device__ __forceinline__ void cold_apply(ColdTable& t, const Views& w, double coefA, double from_fx,
+                                           bool clear) {
+  for (int sl = threadIdx.x; sl < kCold; sl += kThreads) {
+    const int col = t.key[sl];
+    if (col != kEmpty) {
+      const float nv =
+          float(double(t.val[sl]) - coefA * double(static_cast<long long>(t.acc[sl])) * from_fx);
+      st_f32(w.model, uint32_t(col) * 4u, nv);
+      t.val[sl] = nv;
+      t.acc[sl] = 0ull;
+      if (clear) t.key[sl] = kEmpty;
+    }
+  }
+}
+
+__device__ __forceinline__ void hot_apply(Shared& sh, int H, double coefA, double from_fx) {
+  for (int h = threadIdx.x; h < H; h += kThreads) {
+    const unsigned long long a = sh.acch[h];
+    if (a != 0ull) {
+      sh.vhot[h] = float(double(sh.vhot[h]) - coefA * double(static_cast<long long>(a)) * from_fx);
+      sh.acch[h] = 0ull;
+    }
+  }
+}
+
+__device__ __forceinline__ bool is_hot(int code) { return code <= -2; }
+__device__ __forceinline__ int hot_slot(int code) { return -code - 2; }
+
+// Raw nonzeros of one lane's share of one fast-path row (entries sub,
+// sub+16, ...): ok bit j says entry j exists, kRowExists that the row does,
+// kRowLong that it has more than 16*E nonzeros.
+constexpr uint32_t kRowExists = 1u << 31;
+constexpr uint32_t kRowLong = 1u << 30;
+
+template <int E>
+struct DataReg {
+  int code[E];
+  float val[E];
+  uint32_t ok;
+  float y;
+};
+
+__device__ __forceinline__ bool row_valid(const SgdArgs& a, int64_t k, int64_t K, int b) {
+  return k < K && b < int(min(int64_t(a.batch), a.S - k * a.batch));
+}
+
+// Row descriptor of step k, fast-path row b, as loaded (row 0 when the row
+// does not exist; nothing is computed on it until the next step).
+__device__ __forceinline__ RowInfo load_row(const SgdArgs& a, const RowInfo* ri, int64_t k, int64_t K, int b) {
+  return ri[row_valid(a, k, K, b) ? k * a.batch + b : 0];
+}
+
+template <int E>
+__device__ __forceinline__ void load_data(const Views& w, const RowInfo& r, bool valid, int sub, DataReg<E>& d) {
+  const int len = valid ? r.len : 0;
+  const uint32_t st = uint32_t(r.start - w.seg);
+  d.ok = (len > 0 ? kRowExists : 0u) | (len > kRowLanes * E ? kRowLong : 0u);
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const int e = sub + kRowLanes * j;
+    const uint32_t p = e < len ? st + uint32_t(e) : 0u;
+    d.code[j] = ld_i32(w.code, p * 4u);
+    d.val[j] = ld_f32(w.val, p * 4u);
+    d.ok |= uint32_t(e < len) << j;
+  }
+  d.y = r.y;
+}
+
+template <int E>
+__device__ __forceinline__ int code_at(const DataReg<E>& d, int j) {
+  return (d.ok >> j) & 1u ? d.code[j] : -1;
+}
+
+template <int E>
+__device__ __forceinline__ void gather_cold(const Views& w, const DataReg<E>& d, float (&vg)[E]) {
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const int c = code_at(d, j);
+    vg[j] = ld_f32(w.model, uint32_t(c >= 0 ? c : 0) * 4u);
+  }
+}
+
+// Count a step's cold nonzeros and rows too long for the fast path (one
+// LDS atomic per row after a 16-lane sum).
+template <int E>
+__device__ __forceinline__ void count_stats(Shared& sh, int slot, const DataReg<E>& d, int sub) {
+  int cold = 0;
+#pragma unroll
+  for (int j = 0; j < E; ++j) cold += code_at(d, j) >= 0;
+  cold = row16_sum_i(cold);
+  if (sub == 0) {
+    if (cold) atomicAdd(&sh.stats[slot][0], cold);
+    if (d.ok & kRowLong) atomicAdd(&sh.stats[slot][1], 1);
+  }
+}
+
+template <int E, bool PIPE>
+__global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
+  __shared__ Shared sh;
+  const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane & (kRowLanes - 1);
+  const int brow = wave * (64 / kRowLanes) + (lane / kRowLanes);  // fast-path row of this lane
+  float* vrow = a.models + int64_t(i) * a.ld;
+  const RowInfo* ri = a.rowinfo + int64_t(i) * a.S;
+  const int H = a.n_hot;
+  const int64_t K = (a.S + a.batch - 1) / a.batch;
+  Views w;
+  w.seg = a.row_ptr[int64_t(i) * a.S];
+  const uint32_t nnz_w = uint32_t(a.row_ptr[int64_t(i + 1) * a.S] - w.seg);
+  w.code = rsrc(a.code + w.seg, nnz_w * 4u);
+  w.val = rsrc(a.val + w.seg, nnz_w * 4u);
+  w.model = rsrc(vrow, uint32_t(a.dim) * 4u);
+
+  for (int h = tid; h < H; h += kThreads) {
+    sh.vhot[h] = vrow[a.hot_cols[h]];
+    sh.acch[h] = 0ull;
+  }
+  for (int q = tid; q < kCold; q += kThreads) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      sh.cold[t].key[q] = kEmpty;
+      sh.cold[t].acc[q] = 0ull;
+    }
+  }
+  if (tid < 6) sh.stats[tid / 2][tid % 2] = 0;
+  // Fixed point: a column collects at most B contributions of size <= vmax
+  // (|c_b| <= 1, labels in {-1, +1}); with B * vmax < 2^e the sum stays
+  // below 2^61 at scale 2^(61 - e).
+  int e2 = 0;
+  frexp(double(a.batch) * double(a.vmax[i]), &e2);
+  const double to_fx = ldexp(1.0, 61 - e2), from_fx = ldexp(1.0, e2 - 61);
+  double s = 1.0;  // w = s * v
+
+  // Pipeline registers; at the top of step k: d0 = nonzeros of step k,
+  // vg0 = its cold model entries, d1 = nonzeros of step k+1, r2 = row of
+  // step k+2.  Each step loads into d2 / vg1 / r3, which the top of the
+  // next step rotates in (after the end-of-step fence, so the moves do not
+  // wait).  stats[k % 3] holds step k's counts.
+  RowInfo r2, r3;
+  DataReg<E> d0, d1, d2;
+  float vg0[E], vg1[E];
+  if (PIPE) {
+    const RowInfo ra = load_row(a, ri, 0, K, brow), rb = load_row(a, ri, 1, K, brow);
+    r2 = load_row(a, ri, 2, K, brow);
+    __syncthreads();
+    load_data<E>(w, ra, row_valid(a, 0, K, brow), sub, d0);
+    load_data<E>(w, rb, row_valid(a, 1, K, brow), sub, d1);
+    __syncthreads();
+    gather_cold<E>(w, d0, vg0);
+    count_stats<E>(sh, 0, d0, sub);
+  }
+  __syncthreads();
+
+  for (int64_t k = 0; k < K; ++k) {
+    if (PIPE && k > 0) {  // rotate what the previous step loaded
+      d0 = d1;
+      d1 = d2;
+      r2 = r3;
+#pragma unroll
+      for (int j = 0; j < E; ++j) vg0[j] = vg1[j];
+    }
+    const int64_t b0 = k * a.batch;
+    const int Bp = int(min(int64_t(a.batch), a.S - b0));
+    const double eta = step_size(a.lr_kind, a.lr0, a.round * K + k + 1);
+    const double s_new = s * (1.0 - eta * double(a.l2));
+    const double coefA = eta / (double(Bp) * s_new);
+    ColdTable& cur = sh.cold[k & 1];
+    ColdTable& prev = sh.cold[(k + 1) & 1];
+    const int st = int(k % 3);
+    const bool fast = PIPE && Bp <= kFastRows && sh.stats[st][1] == 0 && sh.stats[st][0] <= kColdFast;
+
+    if (fast) {
+      // prefetch: row descriptors of k+3, nonzeros of k+2, cold entries of k+1
+      r3 = load_row(a, ri, k + 3, K, brow);
+      load_data<E>(w, r2, row_valid(a, k + 2, K, brow), sub, d2);
+      gather_cold<E>(w, d1, vg1);
+      count_stats<E>(sh, int((k + 1) % 3), d1, sub);
+
+      double part = 0.0;
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const int code = code_at(d0, j);
+        float v = 0.f;
+        if (is_hot(code))
+          v = sh.vhot[hot_slot(code)];
+        else if (code >= 0)
+          v = cold_patch(prev, code, vg0[j]);
+        part = fma(double(d0.val[j]), double(v), part);
+      }
+      const double dot = row16_sum(part);
+      const double cf = (d0.ok & kRowExists) ? loss_coef(s * dot, double(d0.y), a.loss) : 0.0;
+      if (cf != 0.0) {  // a zero coefficient leaves the row's columns as they are
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+          const int code = code_at(d0, j);
+          if (code == -1) continue;
+          const long long q = llrint(cf * double(d0.val[j]) * to_fx);
+          if (is_hot(code))
+            atomicAdd(&sh.acch[hot_slot(code)], static_cast<unsigned long long>(q));
+          else  // the pre-update value is looked up again rather than kept in registers
+            cold_add(cur, code, q, cold_patch(prev, code, vg0[j]));
+        }
+      }
+      lds_barrier();
+      hot_apply(sh, H, coefA, from_fx);
+      cold_apply(cur, w, coefA, from_fx, false);
+      for (int q = tid; q < kCold; q += kThreads) prev.key[q] = kEmpty;
+      if (tid == 0) sh.stats[st][0] = sh.stats[st][1] = 0;
+    } else {
+      // general path: margins (one wave per row), then row chunks.  The
+      // accumulators of the idle previous-step table hold the minibatch's
+      // coefficients (bit patterns of doubles) until the step ends.
+      unsigned long long* coef = prev.acc;
+      for (int b = wave; b < Bp; b += kWaves) {
+        const RowInfo x = ri[b0 + b];
+        double part = 0.0;
+        for (int e = lane; e < x.len; e += 64) {
+          const long long p = x.start + e;
+          const int code = a.code[p];
+          float v;
+          if (is_hot(code))
+            v = sh.vhot[hot_slot(code)];
+          else
+            v = vrow[code];
+          part = fma(double(a.val[p]), double(v), part);
+        }
+        const double dot = wave_sum(part);
+        if (lane == 0) coef[b] = __builtin_bit_cast(unsigned long long, loss_coef(s * dot, double(x.y), a.loss));
+      }
+      __syncthreads();
+      if (tid == 0) sh.stats[st][0] = sh.stats[st][1] = 0;
+      int c0 = 0;
+      while (c0 < Bp) {
+        int c1 = c0, cnt = 0;
+        while (c1 < Bp) {
+          const int len = ri[b0 + c1].len;
+          if (c1 > c0 && cnt + len > kChunkPairs) break;
+          cnt += len;
+          ++c1;
+        }
+        for (int b = c0 + wave; b < c1; b += kWaves) {
+          const double cf = __builtin_bit_cast(double, coef[b]);
+          if (cf == 0.0) continue;
+          const RowInfo x = ri[b0 + b];
+          for (int e = lane; e < x.len; e += 64) {
+            const long long p = x.start + e;
+            const int code = a.code[p];
+            const long long q = llrint(cf * double(a.val[p]) * to_fx);
+            if (is_hot(code))
+              atomicAdd(&sh.acch[hot_slot(code)], static_cast<unsigned long long>(q));
+            else
+              cold_add(cur, code, q, vrow[code]);
+          }
+        }
+        __syncthreads();
+        hot_apply(sh, H, coefA, from_fx);
+        cold_apply(cur, w, coefA, from_fx, true);
+        __syncthreads();
+        c0 = c1;
+      }
+      for (int q = tid; q < kCold; q += kThreads) {
+        prev.key[q] = kEmpty;
+        prev.acc[q] = 0ull;
+      }
+      if (PIPE) {  // re-prime the pipeline for step k+1 (this step's stores are visible)
+        const RowInfo ra = load_row(a, ri, k + 1, K, brow), rb = load_row(a, ri, k + 2, K, brow);
+        r3 = load_row(a, ri, k + 3, K, brow);
+        __syncthreads();
+        load_data<E>(w, ra, row_valid(a, k + 1, K, brow), sub, d1);
+        load_data<E>(w, rb, row_valid(a, k + 2, K, brow), sub, d2);
+        __syncthreads();
+        gather_cold<E>(w, d1, vg1);
+        count_stats<E>(sh, int((k + 1) % 3), d1, sub);
+      }
+    }
+
+    s = s_new;
+    if (s < 1e-6) {  // fold the scale back into v before it underflows
+      const float sf = float(s);
+      __syncthreads();
+      for (int h = tid; h < H; h += kThreads) sh.vhot[h] *= sf;
+      for (int64_t c = tid; c < a.dim; c += kThreads) vrow[c] *= sf;
+      for (int q = tid; q < kCold; q += kThreads) cur.key[q] = kEmpty;  // nothing left to patch
+      s = 1.0;
+      __syncthreads();
+      if (PIPE) gather_cold<E>(w, d1, vg1);  // the next step's cold entries, rescaled
+    }
+    __syncthreads();  // full fence: cold stores and LDS updates visible, loads landed
+  }
+
+  for (int h = tid; h < H; h += kThreads) vrow[a.hot_cols[h]] = sh.vhot[h];
+  if (tid == 0) {
+    a.scale[i] = float(s);
+    a.tag[i] = a.tag_value;
+  }
+}
+
+// ----------------------------------------------------------------------------
+// per-round row descriptors in schedule order
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rowinfo_kernel(const int32_t* sched, const int64_t* row_ptr,
+                                                      const float* y, int64_t S, int64_t total,
+                                                      RowInfo* out) {
+  const int64_t q = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (q >= total) return;
+  const int64_t worker = q / S;
+  const int64_t g = worker * S + sched[q];
+  const int64_t p0 = row_ptr[g], p1 = row_ptr[g + 1];
+  RowInfo r;
+  r.start = p0;
+  r.len = int(p1 - p0);
+  r.y = y[g];
+  out[q] = r;
+}
+
+// ----------------------------------------------------------------------------
+// bind time: column frequencies (sampled) and per-nonzero codes
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void col_hist_kernel(const int32_t* col, int64_t nnz, int64_t stride,
+                                                       int32_t* counts) {
+  for (int64_t k = int64_t(blockIdx.x) * 256 + threadIdx.x; k * stride < nnz;
+       k += int64_t(gridDim.x) * 256)
+    atomicAdd(&counts[col[k * stride]], 1);
+}
+
+__global__ __launch_bounds__(256) void code_kernel(const int32_t* col, int64_t nnz, const int16_t* lut,
+                                                   int32_t* code) {
+  for (int64_t p = int64_t(blockIdx.x) * 256 + threadIdx.x; p < nnz; p += int64_t(gridDim.x) * 256) {
+    const int c = col[p];
+    const int h = lut[c];
+    code[p] = h >= 0 ? -h - 2 : c;
+  }
+}
+
+template <int E>
+hipError_t launch_e(const SgdArgs& a, hipStream_t s, bool pipe) {
+  if (pipe)
+    hipLaunchKernelGGL((sgd_csr_kernel<E, true>), dim3(uint32_t(a.n)), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((sgd_csr_kernel<E, false>), dim3(uint32_t(a.n)), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_rowinfo(const int32_t* sched, const int64_t* row_ptr, const float* y, int32_t n, int64_t S,
+                          RowInfo* out, hipStream_t s) {
+  const int64_t total = int64_t(n) * S;
+  if (total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rowinfo_kernel, dim3(uint32_t((total + 255) / 256)), dim3(256), 0, s, sched, row_ptr, y, S,
+                     total, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s) {
+  if (a.batch > kBMax || a.n_hot > kHotMax) return hipErrorInvalidValue;
+  const bool pipe = a.batch <= kFastRows;
+  // entries per lane: enough for the longest row, up to 8 (longer rows take the general path)
+  if (a.max_row <= kRowLanes * 2) return launch_e<2>(a, s, pipe);
+  if (a.max_row <= kRowLanes * 3) return launch_e<3>(a, s, pipe);
+  if (a.max_row <= kRowLanes * 4) return launch_e<4>(a, s, pipe);
+  if (a.max_row <= kRowLanes * 6) return launch_e<6>(a, s, pipe);
+  return launch_e<8>(a, s, pipe);
+}
+
+hipError_t launch_col_hist(const int32_t* col, int64_t nnz, int64_t stride, int32_t* counts, hipStream_t s) {
+  if (nnz <= 0) return hipSuccess;
+  const int64_t samples = (nnz + stride - 1) / stride;
+  const int64_t blocks = std::min<int64_t>((samples + 255) / 256, 8192);
+  hipLaunchKernelGGL(col_hist_kernel, dim3(uint32_t(blocks)), dim3(256), 0, s, col, nnz, stride, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_codes(const int32_t* col, int64_t nnz, const int16_t* lut, int32_t* code, hipStream_t s) {
+  if (nnz <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((nnz + 255) / 256, 65536);
+  hipLaunchKernelGGL(code_kernel, dim3(uint32_t(blocks)), dim3(256), 0, s, col, nnz, lut, code);
+  return hipGetLastError();
+}
+
+}  // namespace asap

@@ -10,11 +10,11 @@
 // handed to a single XCD so that the deg+1 re-reads of a neighbour's segment
 // hit that XCD's L2 instead of HBM.
 //
-// NOTIFY-ACK (Section 4) on one device: before a tile reads buffer e it
-// checks that every in-neighbour of its rows carries the tag "published in
-// this round"; a row with a stale neighbour is not reduced and the mismatch
-// is counted in the device error words.  Rows it reduces get the next
-// round's tag in buffer e^1.
+// NOTIFY-ACK (Section 4) on one device: a prologue kernel (the WAIT) checks,
+// one thread per worker, that every in-neighbour carries the tag "published
+// in this round" in buffer e and records the verdict in row_ok; a row with a
+// stale neighbour is not reduced and the mismatch is counted in the device
+// error words.  Rows that are reduced get the next round's tag in buffer e^1.
 #include "asap_launch.h"
 
 namespace asap {
@@ -49,30 +49,28 @@ __device__ __forceinline__ void store_tail(float* d, const float4& v, int64_t c,
   }
 }
 
+__global__ __launch_bounds__(256) void epoch_check_kernel(MixArgs a) {
+  const int r = int(blockIdx.x) * 256 + int(threadIdx.x);
+  if (r >= a.n) return;
+  int ok = 1;
+  const int p0 = a.nbr_ptr[r], p1 = a.nbr_ptr[r + 1];
+  for (int p = p0; p < p1; ++p) ok &= (a.tag_src[a.nbr_idx[p]] == a.expect);
+  a.row_ok[r] = ok;
+  if (!ok) {
+    atomicAdd(&a.err[kErrEpochCount], 1);
+    atomicMin(&a.err[kErrEpochWorker], r);
+  }
+}
+
 __global__ __launch_bounds__(kMixThreads) void mix_kernel(MixArgs a, uint32_t nseg, uint32_t nrg) {
   const uint32_t tile = xcd_tile(blockIdx.x, nseg * nrg);
   const uint32_t seg = tile / nrg, rg = tile % nrg;
   const int row0 = int(rg) * kTileRows;
   const int row1 = min(row0 + kTileRows, a.n);
-  __shared__ int bad[kTileRows];
-  if (threadIdx.x < kTileRows) bad[threadIdx.x] = 0;
-  __syncthreads();
-  for (int r = row0; r < row1; ++r) {
-    const int p0 = a.nbr_ptr[r], p1 = a.nbr_ptr[r + 1];
-    for (int p = p0 + int(threadIdx.x); p < p1; p += kMixThreads)
-      if (a.tag_src[a.nbr_idx[p]] != a.expect) bad[r - row0] = 1;
-  }
-  __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t c = int64_t(seg) * kSegFloats + lane * 4;
   for (int r = row0 + wave; r < row1; r += kMixThreads / 64) {
-    if (bad[r - row0]) {
-      if (seg == 0 && lane == 0) {
-        atomicAdd(&a.err[kErrEpochCount], 1);
-        atomicMin(&a.err[kErrEpochWorker], r);
-      }
-      continue;
-    }
+    if (!a.row_ok[r]) continue;
     if (c < a.dim) {
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
       const int p0 = a.nbr_ptr[r], p1 = a.nbr_ptr[r + 1];
@@ -93,19 +91,14 @@ __global__ __launch_bounds__(kMixThreads) void mix_kernel(MixArgs a, uint32_t ns
 // row is the same weighted column sum, so compute it once per column and
 // broadcast it: n reads and n writes per column instead of n^2 reads.  The
 // sum runs over j ascending with the same fused multiply-adds as mix_kernel,
-// so both kernels produce identical bits on this graph.
+// so both kernels produce identical bits on this graph.  On the complete
+// graph one stale worker makes every row stale.
 __global__ __launch_bounds__(64) void mean_kernel(MixArgs a, uint32_t nseg) {
   const uint32_t seg = xcd_tile(blockIdx.x, nseg);
   const int lane = threadIdx.x;
   int stale = 0;
-  for (int j = lane; j < a.n; j += 64) stale |= (a.tag_src[j] != a.expect);
-  if (__ballot(stale) != 0ull) {
-    if (seg == 0 && lane == 0) {
-      atomicAdd(&a.err[kErrEpochCount], a.n);
-      atomicMin(&a.err[kErrEpochWorker], 0);
-    }
-    return;
-  }
+  for (int j = lane; j < a.n; j += 64) stale |= !a.row_ok[j];
+  if (__ballot(stale) != 0ull) return;
   const int64_t c = int64_t(seg) * kSegFloats + lane * 4;
   if (c < a.dim) {
     const float w0 = a.nbr_w[0];
@@ -140,6 +133,11 @@ hipError_t fill(T* p, int64_t count, T value, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_epoch_check(const MixArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(epoch_check_kernel, dim3(uint32_t((a.n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_mix(const MixArgs& a, hipStream_t s) {
   const uint32_t nseg = uint32_t((a.dim + kSegFloats - 1) / kSegFloats);

@@ -1,19 +1,16 @@
-// kernels_sgd.hip -- the local half-step of (A.2) (Appendix A): every worker
-// runs one pass of minibatch SGD over its own shard (Section 5), in the order
-// of this round's sample schedule.
+// kernels_sgd.hip -- the sample schedule, the local half-step of (A.2)
+// (Appendix A) on dense shards, and the bind-time scan of CSR shards.
 //
-// One workgroup owns one worker for the whole pass, because the steps of a
-// pass form a dependency chain (step k+1's margins read step k's model) and
-// a workgroup barrier is the cheapest way to order them.  The work inside a
-// step is a batched GEMV / SpMV with a rank-B' update: HBM- and
-// latency-bound, no dense contraction, so MFMA is not used.
+// Every worker runs one pass of minibatch SGD over its own shard (Section 5)
+// in the order of this round's sample schedule.  One workgroup owns one
+// worker for the whole pass, because the steps of a pass form a dependency
+// chain (step k+1's margins read step k's model) and a workgroup barrier is
+// the cheapest way to order them.  The work inside a step is a batched GEMV
+// with a rank-B' update: HBM- and latency-bound, no dense contraction, so
+// MFMA is not used.
 //
-// Determinism: every sum has a fixed order.  Margins reduce across lanes with
-// a fixed butterfly and across waves in wave order; the dense gradient sums
-// over the batch in batch order; the sparse gradient accumulates each
-// column's contributions as 64-bit fixed-point integers in an LDS hash
-// table, which is exact and therefore independent of the order in which the
-// lanes' atomics land.
+// Determinism: margins reduce across lanes with a fixed butterfly and across
+// waves in wave order; the gradient sums over the batch in batch order.
 #include <cmath>
 
 #include "asap_common.h"
@@ -149,202 +146,6 @@ __global__ __launch_bounds__(1024) void sgd_dense_kernel(SgdArgs a) {
 }
 
 // ----------------------------------------------------------------------------
-// CSR SGD.
-//
-// Per step: the B' rows of the minibatch are gathered (columns, values and
-// the model entries they touch), each row's margin is reduced by one wave,
-// and each (column, c_b x) contribution is added into an LDS hash table
-// keyed by column as a 64-bit fixed-point integer.  After a barrier every
-// occupied slot writes its column once: v <- v - eta / (B' s) * sum.
-//
-// L2 regularisation uses Bottou's scale form w = s v (the SVM-SGD code the
-// paper trains with, Section 6): the dense decay (1 - eta l2) multiplies the
-// scalar s and only the touched columns of v are written.  The final s of
-// each worker is folded into the mixing weights by the reduce.
-//
-// Fast path (B' <= 64, rows <= 128 nonzeros, so at most 8192 distinct
-// columns = table size): 16 waves x 4 rows x 2 entries per lane stay in
-// registers between the gather and the table insert.  Any other step takes
-// the general path: margins first, then the contributions in row chunks of
-// at most 4096 entries, applying the table after each chunk (the update is
-// linear in the contributions, so applying it in parts is the same update).
-// ----------------------------------------------------------------------------
-constexpr int kCapBits = 13;
-constexpr int kCap = 1 << kCapBits;
-constexpr int kEmpty = -1;
-constexpr int kBMax = 512;
-constexpr int kCsrThreads = 1024;
-constexpr int kCsrWaves = kCsrThreads / 64;
-constexpr int kFastRows = 4;  // per wave; kCsrWaves * kFastRows = 64 rows
-constexpr int kFastLen = 128;
-
-struct CsrShared {
-  int keys[kCap];
-  unsigned long long acc[kCap];
-  float vold[kCap];
-  long long rs[kBMax];
-  int rl[kBMax];
-  float ry[kBMax];
-  double coef[kBMax];
-  int maxlen;
-};
-
-__device__ __forceinline__ int hash_slot(int col) {
-  return int((uint32_t(col) * 2654435761u) >> (32 - kCapBits));
-}
-
-// Add q into the slot of `col`, claiming an empty slot if the column is new.
-// The claiming lane records the pre-update model entry.
-__device__ __forceinline__ void table_add(CsrShared& sh, int col, long long q, float vold,
-                                          bool vold_valid, const float* vrow) {
-  int h = hash_slot(col);
-  for (;;) {
-    const int k = __hip_atomic_load(&sh.keys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (k == col) break;
-    if (k == kEmpty) {
-      const int old = atomicCAS(&sh.keys[h], kEmpty, col);
-      if (old == kEmpty) {
-        sh.vold[h] = vold_valid ? vold : vrow[col];
-        break;
-      }
-      if (old == col) break;
-    }
-    h = (h + 1) & (kCap - 1);
-  }
-  atomicAdd(&sh.acc[h], static_cast<unsigned long long>(q));
-}
-
-__device__ __forceinline__ void table_apply(CsrShared& sh, float* vrow, double coefA, double from_fx) {
-  for (int sl = threadIdx.x; sl < kCap; sl += kCsrThreads) {
-    const int col = sh.keys[sl];
-    if (col != kEmpty) {
-      const double G = double(static_cast<long long>(sh.acc[sl])) * from_fx;
-      vrow[col] = float(double(sh.vold[sl]) - coefA * G);
-      sh.keys[sl] = kEmpty;
-      sh.acc[sl] = 0ull;
-    }
-  }
-}
-
-__global__ __launch_bounds__(kCsrThreads) void sgd_csr_kernel(SgdArgs a) {
-  __shared__ CsrShared sh;
-  const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  float* vrow = a.models + int64_t(i) * a.ld;
-  const int64_t base = int64_t(i) * a.S;
-  const int32_t* si = a.sched + base;
-  for (int s = tid; s < kCap; s += kCsrThreads) {
-    sh.keys[s] = kEmpty;
-    sh.acc[s] = 0ull;
-  }
-  if (tid == 0) sh.maxlen = 0;
-  // Fixed point: a column collects at most B contributions of size <= vmax
-  // (|c_b| <= 1 for both losses, labels in {-1, +1}), so with
-  // B * vmax < 2^e the sum stays below 2^61 at scale 2^(61 - e).
-  int e2 = 0;
-  frexp(double(a.batch) * double(a.vmax[i]), &e2);
-  const double to_fx = ldexp(1.0, 61 - e2), from_fx = ldexp(1.0, e2 - 61);
-  double s = 1.0;  // w = s * v
-  const int64_t K = (a.S + a.batch - 1) / a.batch;
-  __syncthreads();
-  for (int64_t k = 0; k < K; ++k) {
-    const int64_t b0 = k * a.batch;
-    const int Bp = int(min(int64_t(a.batch), a.S - b0));
-    const double eta = step_size(a.lr_kind, a.lr0, a.round * K + k + 1);
-    for (int b = tid; b < Bp; b += kCsrThreads) {
-      const int64_t g = base + si[b0 + b];
-      const long long r0 = a.row_ptr[g], r1 = a.row_ptr[g + 1];
-      sh.rs[b] = r0;
-      sh.rl[b] = int(r1 - r0);
-      sh.ry[b] = a.y[g];
-      atomicMax(&sh.maxlen, int(r1 - r0));
-    }
-    __syncthreads();
-    const bool fast = Bp <= kCsrWaves * kFastRows && sh.maxlen <= kFastLen;
-    const double s_new = s * (1.0 - eta * double(a.l2));
-    const double coefA = eta / (double(Bp) * s_new);
-    if (fast) {
-      int colr[kFastRows][2];
-      float valr[kFastRows][2], vvr[kFastRows][2];
-#pragma unroll
-      for (int r = 0; r < kFastRows; ++r) {
-        const int b = wave + r * kCsrWaves;
-        const long long st = b < Bp ? sh.rs[b] : 0;
-        const int len = b < Bp ? sh.rl[b] : 0;
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int pos = lane + 64 * e;
-          const bool ok = pos < len;
-          colr[r][e] = ok ? a.col[st + pos] : -1;
-          valr[r][e] = ok ? a.val[st + pos] : 0.f;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < kFastRows; ++r)
-#pragma unroll
-        for (int e = 0; e < 2; ++e) vvr[r][e] = colr[r][e] >= 0 ? vrow[colr[r][e]] : 0.f;
-#pragma unroll
-      for (int r = 0; r < kFastRows; ++r) {
-        const int b = wave + r * kCsrWaves;
-        const double dot = wave_sum(fma(double(valr[r][1]), double(vvr[r][1]),
-                                        double(valr[r][0]) * double(vvr[r][0])));
-        if (b < Bp) {
-          const double cf = loss_coef(s * dot, double(sh.ry[b]), a.loss);
-#pragma unroll
-          for (int e = 0; e < 2; ++e)
-            if (colr[r][e] >= 0 && cf != 0.0)  // a zero coefficient leaves the column as it is
-              table_add(sh, colr[r][e], llrint(cf * double(valr[r][e]) * to_fx), vvr[r][e], true, vrow);
-        }
-      }
-      __syncthreads();
-      table_apply(sh, vrow, coefA, from_fx);
-      if (tid == 0) sh.maxlen = 0;
-      __syncthreads();
-    } else {
-      for (int b = wave; b < Bp; b += kCsrWaves) {
-        const long long st = sh.rs[b];
-        const int len = sh.rl[b];
-        double part = 0.0;
-        for (int pos = lane; pos < len; pos += 64)
-          part = fma(double(a.val[st + pos]), double(vrow[a.col[st + pos]]), part);
-        const double dot = wave_sum(part);
-        if (lane == 0) sh.coef[b] = loss_coef(s * dot, double(sh.ry[b]), a.loss);
-      }
-      __syncthreads();
-      if (tid == 0) sh.maxlen = 0;
-      int c0 = 0;
-      while (c0 < Bp) {
-        int c1 = c0, cnt = 0;
-        while (c1 < Bp && cnt + sh.rl[c1] <= kCap / 2) cnt += sh.rl[c1++];
-        if (c1 == c0) ++c1;  // unreachable: rows longer than kCap / 2 are refused at bind
-        for (int b = c0 + wave; b < c1; b += kCsrWaves) {
-          const long long st = sh.rs[b];
-          const int len = sh.rl[b];
-          const double cf = sh.coef[b];
-          if (cf == 0.0) continue;
-          for (int pos = lane; pos < len; pos += 64)
-            table_add(sh, a.col[st + pos], llrint(cf * double(a.val[st + pos]) * to_fx), 0.f, false, vrow);
-        }
-        __syncthreads();
-        table_apply(sh, vrow, coefA, from_fx);
-        __syncthreads();
-        c0 = c1;
-      }
-    }
-    s = s_new;
-    if (s < 1e-6) {  // fold the scale back into v before it underflows
-      const float sf = float(s);
-      for (int64_t c = tid; c < a.dim; c += kCsrThreads) vrow[c] *= sf;
-      s = 1.0;
-      __syncthreads();
-    }
-  }
-  if (tid == 0) {
-    a.scale[i] = float(s);
-    a.tag[i] = a.tag_value;
-  }
-}
-
-// ----------------------------------------------------------------------------
 // bind-time scan of the CSR shards
 // ----------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void csr_scan_kernel(const int64_t* row_ptr, const int32_t* col,
@@ -389,6 +190,8 @@ __global__ __launch_bounds__(256) void csr_scan_kernel(const int64_t* row_ptr, c
   if (threadIdx.x == 0) {
     vmax[i] = smax[0];
     atomicMax(reinterpret_cast<unsigned long long*>(&out[0]), static_cast<unsigned long long>(slen[0]));
+    const long long seg = row_ptr[int64_t(i + 1) * S] - row_ptr[int64_t(i) * S];
+    atomicMax(reinterpret_cast<unsigned long long*>(&out[5]), static_cast<unsigned long long>(seg < 0 ? 0 : seg));
   }
   if (badcol) atomicAdd(reinterpret_cast<unsigned long long*>(&out[1]), badcol);
   if (bady) atomicAdd(reinterpret_cast<unsigned long long*>(&out[2]), bady);
@@ -424,12 +227,6 @@ hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(sgd_dense_kernel<16>, grid, block, 0, s, a);
   else
     return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
-hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s) {
-  if (a.batch > kBMax) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(sgd_csr_kernel, dim3(uint32_t(a.n)), dim3(kCsrThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -152,7 +152,7 @@ def test_state_errors_before_device_work():
             asap.asap_local_sgd(ctx, prm, stream=0)
         assert e.value.status == asap.E_STATE
         ws0 = asap.asap_workspace_size(ctx)
-        asap.asap_bind_csr(ctx, fake, fake, fake, fake, 1000, stream=0)
+        asap.asap_bind_csr(ctx, fake, fake, fake, fake, 1000, 5000, stream=0)
         assert asap.asap_workspace_size(ctx) >= ws0 + 8 * 1000 * 4   # room for the schedule
         with pytest.raises(asap.AsapError) as e:
             asap.asap_bind_workspace(ctx, fake, 16, stream=0)        # too small
