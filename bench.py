@@ -51,10 +51,15 @@ def copy_probe(gib: int):
     a = torch.ones(n, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
     torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
     for _ in range(3):
         b.copy_(a)
+    t1.record()
     torch.cuda.synchronize()
-    print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 3}))
+    ms = t0.elapsed_time(t1) / 3
+    print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 3,
+                      "ms_per_copy": ms, "GB/s": 8 * n / ms / 1e6}))
 
 
 def graph_for(wl, d=None):
@@ -178,8 +183,8 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="GIB")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build runs every logical worker on a single MI355X "
-              "and has no multi-GPU path (--gpus 1 only)", file=sys.stderr)
+        print("bench.py measures one GPU: every logical worker runs on a single MI355X "
+              "and there is no multi-GPU path (--gpus 1 only)", file=sys.stderr)
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)

@@ -151,7 +151,10 @@ asap_status asap_bind_workspace(asap_ctx* ctx, void* dev, size_t bytes, void* st
  * 256-byte aligned, ld >= dim and a multiple of 64.  Buffer 0 holds the
  * round-0 models; the round counter is reset to 0 and every epoch tag of
  * buffer 0 is set to "round 0 published".  Entries in [dim, ld) are never
- * read by SGD and never written. */
+ * read by SGD and never written.  A row stride that is a multiple of 4 KiB
+ * puts every row start in the same DRAM channel and bank and slows the
+ * reduce, which reads all rows at one column range at a time; pad such an ld
+ * (the Python binding adds 128 floats). */
 asap_status asap_bind_models(asap_ctx* ctx, float* buf0, float* buf1, int64_t ld,
                              void* stream);
 

@@ -259,6 +259,15 @@ def asap_destroy(ctx):
         lib().asap_destroy(ctx)
 
 
+def model_ld(dim: int) -> int:
+    """Row stride (floats) for the model buffers: dim rounded up to 64, plus
+    128 when that is a multiple of 1024.  Rows a multiple of 4 KiB apart all
+    start in the same DRAM channel and bank, which costs the reduce, whose
+    loads touch every row at the same column, up to a third of its rate."""
+    ld = (int(dim) + 63) // 64 * 64
+    return ld + 128 if ld % 1024 == 0 else ld
+
+
 # ---------------------------------------------------------------------------
 # Session: one context plus its torch-owned device memory
 # ---------------------------------------------------------------------------
@@ -274,7 +283,7 @@ class Session:
         self.torch = torch
         self.device = torch.device(device)
         self.n, self.dim = int(n), int(dim)
-        self.ld = (self.dim + 63) // 64 * 64
+        self.ld = model_ld(self.dim)
         self.ctx = asap_create(self.n, self.dim, ptr, idx, w, flags)
         self.bufs = [torch.zeros((self.n, self.ld), dtype=torch.float32, device=self.device) for _ in range(2)]
         self._keep = []

@@ -36,6 +36,8 @@ struct asap_ctx {
   std::vector<int32_t> ptr, idx;
   std::vector<float> w;
   bool complete_uniform = false;
+  int32_t max_deg = 0;  // longest row of the graph (entries, self included)
+  int32_t n_cu = 256;   // compute units of the device the workspace is on
 
   // caller-owned device memory
   char* ws = nullptr;
@@ -411,6 +413,7 @@ extern "C" asap_status asap_create(int32_t n, int64_t dim, const int32_t* nbr_pt
   c->idx.assign(nbr_idx, nbr_idx + nbr_ptr[n]);
   c->w.assign(nbr_w, nbr_w + nbr_ptr[n]);
   c->complete_uniform = is_complete_uniform(n, nbr_ptr, nbr_w);
+  for (int32_t i = 0; i < n; ++i) c->max_deg = std::max(c->max_deg, nbr_ptr[i + 1] - nbr_ptr[i]);
   layout(c);
   *out = c;
   return ASAP_OK;
@@ -490,6 +493,12 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     return fail(c, ASAP_E_INVALID_ARG, "workspace too small: %zu < %zu bytes", bytes, c->total);
   if (!c->buf[0]) return fail(c, ASAP_E_STATE, "bind the models before the workspace");
   hipStream_t s = static_cast<hipStream_t>(stream);
+  {
+    int dev_id = 0, cus = 0;
+    if (hipGetDevice(&dev_id) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev_id) == hipSuccess && cus > 0)
+      c->n_cu = cus;
+  }
   c->ws = static_cast<char*>(dev);
   c->ws_bytes = bytes;
   c->tags_ready = false;
@@ -607,7 +616,14 @@ extern "C" asap_status asap_stochastic_reduce(asap_ctx* c, void* stream) {
   a.err = at<int32_t>(c, c->off_err);
   a.row_ok = at<int32_t>(c, c->off_rowok);
   hipError_t e = launch_epoch_check(a, s);
-  if (e == hipSuccess) e = c->complete_uniform ? launch_mean(a, s) : launch_mix(a, s);
+  if (e == hipSuccess) {
+    if (c->complete_uniform) {
+      e = launch_mean(a, s);
+    } else {
+      e = launch_mix_slab(a, c->max_deg, c->n_cu, s);
+      if (e == hipErrorNotSupported) e = launch_mix(a, s);
+    }
+  }
   if (e != hipSuccess) return hip_fail(c, e, "reduce kernel");
   c->cur ^= 1;
   c->round += 1;

@@ -34,6 +34,7 @@ struct MixArgs {
 
 hipError_t launch_epoch_check(const MixArgs& a, hipStream_t s);
 hipError_t launch_mix(const MixArgs& a, hipStream_t s);
+hipError_t launch_mix_slab(const MixArgs& a, int max_deg, int n_cu, hipStream_t s);
 hipError_t launch_mean(const MixArgs& a, hipStream_t s);
 
 // Row descriptor of one minibatch position, in schedule order.

@@ -4,11 +4,22 @@
 // The reduce is a low fan-in streaming product: every output element is
 // deg+1 fused multiply-adds over rows that are each read by deg+1 outputs.
 // It is bound by HBM bandwidth (arithmetic intensity < 1 flop/byte), so MFMA
-// has no role here.  What matters is that every model byte crosses HBM
-// once: a tile is one 1 KiB segment of 16 consecutive output rows, one wave
-// per row segment with 16-byte loads, and the tiles of one column range are
-// handed to a single XCD so that the deg+1 re-reads of a neighbour's segment
-// hit that XCD's L2 instead of HBM.
+// has no role here.  What matters is that every model byte crosses HBM once.
+//
+// slab kernel (n a power of two in [8, 1024], rows of at most 17 entries): one
+// 1024-thread workgroup per CU owns a contiguous range of column chunks; a
+// chunk holds all n rows of 16384/n columns (64 KiB) and is staged in LDS,
+// so each neighbour re-read is an LDS read.  Thread t keeps the neighbour
+// list of row t mod n in registers and computes 4 float4 of it per chunk;
+// the next chunk's loads are in flight while the current one is computed.
+// LDS slots of a row are XOR-swizzled by the row's low bits so that lanes
+// reading random rows spread over the banks.  Results are transposed across
+// groups of 4 lanes (DPP) so that each store writes 64 contiguous bytes of a
+// row rather than 16 bytes in each of 64 rows.
+//
+// tile kernel (any n): a tile is one 1 KiB segment of 16 consecutive output
+// rows, one wave per row segment with 16-byte loads; the tiles of one column
+// range go to one XCD so that re-reads of a neighbour's segment hit its L2.
 //
 // NOTIFY-ACK (Section 4) on one device: a prologue kernel (the WAIT) checks,
 // one thread per worker, that every in-neighbour carries the tag "published
@@ -117,6 +128,199 @@ __global__ __launch_bounds__(64) void mean_kernel(MixArgs a, uint32_t nseg) {
     for (int j = lane; j < a.n; j += 64) a.tag_dst[j] = a.next;
 }
 
+// Barrier that orders LDS only: global loads stay in flight across it, and
+// global stores need not have landed.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+constexpr int kSlabThreads = 1024;
+
+// x of lane i ^ S (S = 1, 2, 4) by DPP moves: quad_perm [1,0,3,2] and
+// [2,3,0,1] are the xor-1 and xor-2 exchanges; xor 4 is the mirror inside
+// each 8-lane half-row (i -> i ^ 7) followed by quad_perm [3,2,1,0]
+// (i -> i ^ 3).
+template <int S>
+__device__ __forceinline__ float xor_lane(float x) {
+  int v = __builtin_bit_cast(int, x);
+  if constexpr (S == 1) {
+    v = __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  } else if constexpr (S == 2) {
+    v = __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  } else {
+    static_assert(S == 4, "xor_lane: S in {1, 2, 4}");
+    v = __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+    v = __builtin_amdgcn_update_dpp(0, v, 0x1B, 0xF, 0xF, false);
+  }
+  return __builtin_bit_cast(float, v);
+}
+
+template <int S>
+__device__ __forceinline__ float4 xor_lane4(const float4& x) {
+  return make_float4(xor_lane<S>(x.x), xor_lane<S>(x.y), xor_lane<S>(x.z), xor_lane<S>(x.w));
+}
+
+// v[k] of lane i <- v[i] of lane k, within aligned groups of PF lanes
+// (PF = 4 or 8): butterfly exchanges with the lanes i ^ s, s = PF/2 .. 1.
+__device__ __forceinline__ float4 sel4(bool c, const float4& a, const float4& b) {
+  return make_float4(c ? a.x : b.x, c ? a.y : b.y, c ? a.z : b.z, c ? a.w : b.w);
+}
+
+template <int S, int PF>
+__device__ __forceinline__ void transpose_stage(float4 (&v)[PF], int lane_in) {
+  const bool hi = lane_in & S;
+#pragma unroll
+  for (int k = 0; k < PF; ++k) {
+    if (k & S) continue;
+    // a lane keeps the slot whose bit S matches its own and sends the other
+    // (value selects only: a select of the slot to write would put v in
+    // scratch memory)
+    const float4 lo_v = v[k], hi_v = v[k | S];
+    const float4 recv = xor_lane4<S>(sel4(hi, lo_v, hi_v));
+    v[k] = sel4(hi, recv, lo_v);
+    v[k | S] = sel4(hi, hi_v, recv);
+  }
+}
+
+template <int PF>
+__device__ __forceinline__ void transpose_lanes(float4 (&v)[PF], int lane_in) {
+  static_assert(PF == 4 || PF == 8, "transpose_lanes: PF in {4, 8}");
+  if constexpr (PF == 8) transpose_stage<4>(v, lane_in);
+  transpose_stage<2>(v, lane_in);
+  transpose_stage<1>(v, lane_in);
+}
+
+// 1 to 3 leading components of v (a row's ragged last float4)
+__device__ __forceinline__ void store_partial(float* d, float4 v, int k) {
+  d[0] = v.x;
+  if (k > 1) d[1] = v.y;
+  if (k > 2) d[2] = v.z;
+}
+
+// LDS reads in flight per thread
+template <int DEG> constexpr int slab_group() { return DEG <= 5 ? DEG : 4; }
+
+// PF float4 per thread per chunk: a chunk is PF*16 KiB of LDS and PF
+// registers' worth of loads in flight per thread.
+template <int DEG, int PF>
+__global__ __launch_bounds__(kSlabThreads) void mix_slab_kernel(MixArgs a, int nchunks) {
+  constexpr int kVec = PF * kSlabThreads;    // float4 slots per chunk
+  __shared__ float4 slab[kVec];
+  const int n = a.n;
+  const int Q = kVec / n;                    // float4 per row per chunk
+  const int C = 4 * Q;                       // columns per chunk
+  const int X = min(Q, 8) - 1;               // swizzle mask
+  const int tid = threadIdx.x;
+  const int row = tid % n, grp = tid / n;    // compute: row, float4 [grp*PF, grp*PF+PF)
+  constexpr int G = slab_group<DEG>();
+  // jq = j*Q | (j & X): the slot of float4 q of row j is jq ^ q, because
+  // X < Q and Q is a power of two (see the staging writes below).
+  // jq < n*Q <= 8192, so two of them share a register.
+  uint32_t jq2[(DEG + 1) / 2] = {};
+  float nw[DEG];
+  const int p0 = a.nbr_ptr[row], deg = a.nbr_ptr[row + 1] - p0;
+#pragma unroll
+  for (int u = 0; u < DEG; ++u) {
+    const bool has = u < deg;  // padding: own row, weight 0
+    const int j = has ? a.nbr_idx[p0 + u] : row;
+    float wt = has ? a.nbr_w[p0 + u] : 0.f;
+    if (a.scale && has) wt *= a.scale[j];
+    jq2[u / 2] |= uint32_t(j * Q | (j & X)) << (16 * (u & 1));
+    nw[u] = wt;
+  }
+  const bool ok = a.row_ok[row] != 0;
+  const int per = (nchunks + int(gridDim.x) - 1) / int(gridDim.x);
+  const int ch0 = int(blockIdx.x) * per, ch1 = min(nchunks, ch0 + per);
+
+  // Staging: thread t always moves float4 slot q0 = t mod Q of rows
+  // r0 + m*rstep.  The per-thread part of the address is a 32-bit byte
+  // offset below 2^31 (the launcher checks it); the rest is wave-uniform.
+  const int q0 = tid % Q, r0 = tid / Q, rstep = kSlabThreads / Q;
+  const uint32_t voff = (uint32_t(r0) * uint32_t(a.ld) + 4u * uint32_t(q0)) * 4u;
+  float4 nxt[PF];
+  auto load = [&](int ch) {
+    const int64_t off = int64_t(ch) * C;
+    const bool in = off + 4 * q0 < a.dim;
+    // an empty asm makes voff opaque per chunk, so the compiler does not
+    // hoist PF 64-bit row addresses out of the chunk loop
+    uint32_t vo = voff;
+    asm volatile("" : "+v"(vo));
+#pragma unroll
+    for (int m = 0; m < PF; ++m) {
+      const char* base = reinterpret_cast<const char*>(a.src + off + int64_t(m * rstep) * a.ld);
+      nxt[m] = in ? *reinterpret_cast<const float4*>(base + vo) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  // Output float4 q of this thread's row from the staged chunk.  Padding
+  // entries read the own row with weight 0, which adds an exact zero, so the
+  // reads of a group issue back to back with no branches.
+  auto slab_row = [&](int q) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    // Empty asm statements pin the register plan: the packed slots stay
+    // packed and the weights stay in registers (not reloaded from memory),
+    // and the reads of one group are not hoisted above the previous group.
+#pragma unroll
+    for (int k = 0; k < (DEG + 1) / 2; ++k) asm volatile("" : "+v"(jq2[k]));
+#pragma unroll
+    for (int k = 0; k < DEG; ++k) asm volatile("" : "+v"(nw[k]));
+#pragma unroll
+    for (int p0 = 0; p0 < DEG; p0 += G) {
+      if (p0 > 0) asm volatile("" ::: "memory");
+      float4 x[G];
+#pragma unroll
+      for (int p = p0; p < p0 + G && p < DEG; ++p)
+        x[p - p0] = slab[((jq2[p / 2] >> (16 * (p & 1))) & 0xffffu) ^ q];
+#pragma unroll
+      for (int p = p0; p < p0 + G && p < DEG; ++p) fma4(acc, nw[p], x[p - p0]);
+    }
+    // all four components here, or the compiler splits 16-byte LDS reads
+    asm volatile("" : "+v"(acc.x), "+v"(acc.y), "+v"(acc.z), "+v"(acc.w));
+    return acc;
+  };
+  // Stores: lane = row is the natural compute layout, but then every store
+  // instruction would scatter 16 bytes to each of 64 rows.  The PF outputs
+  // of PF consecutive lanes are transposed across those lanes instead, so
+  // that store k of lane i writes float4 slot grp*PF + i of row
+  // (row & ~(PF-1)) + k: PF lanes fill PF*16 contiguous bytes of one row.
+  const int lane_in = row & (PF - 1), row_base = row & ~(PF - 1);
+  const uint64_t okmask = __ballot(ok);
+  const int lane = int(threadIdx.x) & 63;
+  if (ch0 < ch1) load(ch0);
+  for (int ch = ch0; ch < ch1; ++ch) {
+    lds_barrier();  // the previous chunk is no longer read
+#pragma unroll
+    for (int m = 0; m < PF; ++m) {
+      const int r = r0 + m * rstep;
+      slab[(r * Q | (r & X)) ^ q0] = nxt[m];
+    }
+    lds_barrier();
+    if (ch + 1 < ch1) load(ch + 1);
+    float4 res[PF];
+#pragma unroll
+    for (int u = 0; u < PF; ++u) res[u] = slab_row(grp * PF + u);
+    transpose_lanes<PF>(res, lane_in);
+    const int64_t c = int64_t(ch) * C + 4 * (grp * PF + lane_in);
+    if (c < a.dim) {
+      const bool full = c + 4 <= a.dim;
+      const int k_tail = int(min<int64_t>(a.dim - c, 4));
+#pragma unroll
+      for (int k = 0; k < PF; ++k) {
+        if ((okmask >> (lane - lane_in + k)) & 1) {
+          float* d = a.dst + int64_t(row_base + k) * a.ld + c;
+          if (full) {
+            *reinterpret_cast<float4*>(d) = res[k];
+          } else {
+            store_partial(d, res[k], k_tail);
+          }
+        }
+      }
+    }
+  }
+  if (blockIdx.x == 0 && grp == 0 && ok) a.tag_dst[row] = a.next;
+}
+
 template <class T>
 __global__ void fill_kernel(T* p, int64_t count, T value) {
   for (int64_t k = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; k < count;
@@ -137,6 +341,32 @@ hipError_t fill(T* p, int64_t count, T value, hipStream_t s) {
 hipError_t launch_epoch_check(const MixArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(epoch_check_kernel, dim3(uint32_t((a.n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+// Slab kernel when n is a power of two in [8, 1024] and every row has at most
+// 17 entries (returns hipErrorNotSupported otherwise).
+template <int DEG, int PF>
+hipError_t launch_slab(const MixArgs& a, int n_cu, hipStream_t s) {
+  const int n = a.n;
+  const int C = 4 * PF * kSlabThreads / n;
+  // per-thread staging offset: rows below 1024/(C/4), float4 slots below C/4
+  if ((int64_t(kSlabThreads / (C / 4) - 1) * a.ld + C) * 4 >= (int64_t(1) << 31))
+    return hipErrorNotSupported;
+  const int64_t nchunks64 = (a.dim + C - 1) / C;
+  if (nchunks64 >= (int64_t(1) << 31)) return hipErrorNotSupported;
+  const int nchunks = int(nchunks64);
+  const int grid = std::max(1, std::min(nchunks, n_cu));
+  hipLaunchKernelGGL((mix_slab_kernel<DEG, PF>), dim3(grid), dim3(kSlabThreads), 0, s, a, nchunks);
+  return hipGetLastError();
+}
+
+hipError_t launch_mix_slab(const MixArgs& a, int max_deg, int n_cu, hipStream_t s) {
+  const int n = a.n;
+  if (n < 8 || n > kSlabThreads || (n & (n - 1)) || max_deg > 17) return hipErrorNotSupported;
+  if (max_deg <= 3) return launch_slab<3, 4>(a, n_cu, s);
+  if (max_deg <= 5) return launch_slab<5, 4>(a, n_cu, s);
+  if (max_deg <= 9) return launch_slab<9, 4>(a, n_cu, s);
+  return launch_slab<17, 4>(a, n_cu, s);
 }
 
 hipError_t launch_mix(const MixArgs& a, hipStream_t s) {

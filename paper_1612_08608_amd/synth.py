@@ -245,8 +245,3 @@ def initial_models(wl: Workload, rows=None, cols=None) -> np.ndarray:
     with ThreadPoolExecutor(_pool_size()) as ex:
         list(ex.map(fill, enumerate(rows)))
     return out
-
-
-def padded_ld(dim: int) -> int:
-    """Model row stride in floats: dim rounded up to a multiple of 64 (256 B)."""
-    return (dim + 63) // 64 * 64

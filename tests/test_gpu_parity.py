@@ -328,6 +328,62 @@ def test_reduce_matches_oracle_ragged_dim(torch, d):
     sess.close()
 
 
+def irregular_graph(kind, n):
+    """A graph with unequal degrees, built here; weights from both builders."""
+    if kind == "path":      # the chain of Figure 2: end points have degree 1
+        adj = [{j for j in (i - 1, i + 1) if 0 <= j < n} for i in range(n)]
+    elif kind == "star":    # parameter-server shape: the hub has degree n-1
+        adj = [set(range(1, n))] + [{0} for _ in range(1, n)]
+    else:                   # ring plus chords from every third node
+        adj = [{(i - 1) % n, (i + 1) % n} for i in range(n)]
+        for i in range(0, n, 3):
+            j = (i + n // 2 + 1) % n
+            adj[i].add(j)
+            adj[j].add(i)
+    ptr = np.zeros(n + 1, np.int32)
+    idx = []
+    for i in range(n):
+        row = sorted(adj[i] | {i})
+        idx.extend(row)
+        ptr[i + 1] = ptr[i] + len(row)
+    idx = np.asarray(idx, np.int32)
+    w = oracle.graphs.metropolis_weights(ptr, idx)
+    assert np.array_equal(asap.asap_metropolis_weights(ptr, idx).view(np.uint32), w.view(np.uint32))
+    return ptr, idx, w
+
+
+# (workers, graph, degree, dim): powers of two up to 1024 with rows of at most
+# 17 entries take the LDS-slab kernel (chunks of 2^15 or 2^14 floats split
+# over the rows), the rest the tile kernel; dims cover one partial float4,
+# exact chunk multiples, ragged tails and fewer chunks than compute units.
+REDUCE_SHAPES = [
+    (8, "ring", 2, 1), (8, "ring", 2, 4097), (8, "ring", 2, 3 * 4096),
+    (16, "random", 6, 64), (32, "ring", 2, 33), (64, "random", 4, 3 * 512),
+    (64, "random", 4, 515), (256, "random", 8, 130), (1024, "random", 16, 130),
+    (1024, "random", 2, 67), (16, "path", 0, 1003), (128, "chords", 0, 999),
+    (100, "random", 4, 777), (64, "random", 20, 1001), (64, "star", 0, 300),
+    (3, "ring", 2, 5),
+]
+
+
+@pytest.mark.parametrize("n,kind,d,dim", REDUCE_SHAPES)
+def test_reduce_kernel_shapes(torch, n, kind, d, dim):
+    if kind in ("path", "star", "chords"):
+        p, i, w = irregular_graph(kind, n)
+    else:
+        p, i, w = graph(kind, n, d)
+    W = synth.initial_models(synth.MIX_STRESS_1024W.with_(n_workers=n, dim=dim))
+    sess = asap.Session(n, dim, p, i, w)
+    sess.set_models(W)
+    ref = W.astype(np.float64)
+    for r in range(2):
+        sess.stochastic_reduce()
+        ref = oracle.mix.stochastic_reduce(ref, p, i, w)
+        assert_models_close(sess.models().cpu().numpy(), ref, what=f"{kind} n={n} dim={dim} reduce {r}")
+    assert sess.check()[0] == asap.OK
+    sess.close()
+
+
 def test_complete_graph_reduce_is_column_mean(torch):
     n, dim = 256, 3000
     p, i, w = graph("complete", n)

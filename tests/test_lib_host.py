@@ -170,3 +170,11 @@ def test_dense_dim_limit():
         assert e.value.status == asap.E_INVALID_ARG
     finally:
         asap.asap_destroy(ctx)
+
+
+def test_model_row_stride_avoids_4k_multiples():
+    assert [asap.model_ld(d) for d in (1, 64, 65, 1000, 1001, 4096, 1 << 20)] == \
+        [64, 64, 128, 1152, 1152, 4224, (1 << 20) + 128]
+    for d in range(1, 5000, 37):
+        ld = asap.model_ld(d)
+        assert ld >= d and ld % 64 == 0 and ld % 1024 != 0 and ld - d < 64 + 128

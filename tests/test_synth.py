@@ -51,5 +51,3 @@ def test_initial_models_rows_and_column_samples():
     assert abs(W.mean()) < 0.1 and abs(W.std() - 1) < 0.1
 
 
-def test_padded_ld():
-    assert [synth.padded_ld(d) for d in (1, 64, 65, 4096, 1 << 20)] == [64, 64, 128, 4096, 1 << 20]
