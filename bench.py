@@ -280,7 +280,7 @@ def main():
         out["reduce"] = reduce_info
         if wl.features == "csr":
             alg, reads, writes = csr_algorithmic_bytes(wl, rp, col)
-            kernel, src = "sgd_csr_kernel", os.path.join(csrc, "kernels_sgd.hip")
+            kernel, src = "sgd_csr_kernel", os.path.join(csrc, "kernels_csr.hip")
         else:
             S, B = wl.samples, wl.batch
             steps_per_pass = -(-S // B)
