@@ -151,7 +151,7 @@ asap_status asap_bind_workspace(asap_ctx* ctx, void* dev, size_t bytes, void* st
  * 256-byte aligned, ld >= dim and a multiple of 64.  Buffer 0 holds the
  * round-0 models; the round counter is reset to 0 and every epoch tag of
  * buffer 0 is set to "round 0 published".  Entries in [dim, ld) are never
- * read by SGD and never written.  A row stride that is a multiple of 4 KiB
+ * written and their values do not affect any result.  A row stride that is a multiple of 4 KiB
  * puts every row start in the same DRAM channel and bank and slows the
  * reduce, which reads all rows at one column range at a time; pad such an ld
  * (the Python binding adds 128 floats). */
@@ -160,7 +160,10 @@ asap_status asap_bind_models(asap_ctx* ctx, float* buf0, float* buf1, int64_t ld
 
 /* Bind dense shards: X [n][samples][ldx] fp32 (ldx >= dim, multiple of 4,
  * 16-byte aligned), y [n][samples] fp32 in {-1, +1}; worker i owns
- * X[i], y[i].  dim <= 16384 on this path.  samples >= 1. */
+ * X[i], y[i].  dim <= 16384 on this path.  samples >= 1.  Entries of X past
+ * dim are never used.  For dim > 1024 a pass may use several workgroups per
+ * worker that meet once per minibatch step (a cooperative launch); the
+ * workspace holds their partial gradients. */
 asap_status asap_bind_dense(asap_ctx* ctx, const float* X, const float* y,
                             int64_t samples, int64_t ldx);
 
@@ -225,7 +228,10 @@ asap_status asap_metrics(asap_ctx* ctx, int32_t loss, float l2, double* out, voi
 /* Synchronise `stream` and read the device error words.  Returns
  * ASAP_E_EPOCH (and clears the words) if any reduce since the last check
  * found a mismatched tag; *bad_worker (may be NULL) gets the lowest such
- * worker. */
+ * worker.  Returns ASAP_E_DEVICE (and clears the word) if a dense SGD pass
+ * with several workgroups per worker found a member missing at a step's
+ * rendezvous for too long; that pass stopped early and its models are not
+ * valid. */
 asap_status asap_check(asap_ctx* ctx, void* stream, int32_t* bad_worker);
 
 /* Failure-injection hook for tests: overwrite the epoch tag of `worker` in

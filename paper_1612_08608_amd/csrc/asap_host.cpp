@@ -28,6 +28,12 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 enum DataKind { kNoData = 0, kDense = 1, kCsr = 2 };
 
+// dense workspace: up to 8 workgroups per worker, sized for a 256-CU device
+// (the launch takes fewer when fewer are co-resident)
+constexpr int kDenseMaxMembers = 8;
+constexpr int kDenseCus = 256;
+constexpr uint32_t kDenseSpinLimit = 1u << 20;
+
 }  // namespace
 
 struct asap_ctx {
@@ -63,7 +69,9 @@ struct asap_ctx {
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_sched = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
-         off_rowinfo = 0, off_code = 0, off_lut = 0, off_hot = 0, total = 0;
+         off_rowinfo = 0, off_code = 0, off_lut = 0, off_hot = 0, off_dpart = 0, off_dcount = 0,
+         total = 0;
+  int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
   // round state
   int32_t cur = 0;
@@ -120,6 +128,11 @@ void layout(asap_ctx* c) {
   c->off_code = o;    o = align_up(o + (csr ? size_t(c->nnz) * 4 : 0));
   c->off_lut = o;     o = align_up(o + (csr ? size_t(c->dim) * 2 : 0));
   c->off_hot = o;     o = align_up(o + (csr ? size_t(kHotMax) * 4 : 0));
+  const int cpq = c->kind == kDense ? dense_wide_cpq(c->dim) : 0;
+  c->dense_k = cpq ? std::max(1, std::min(kDenseMaxMembers, kDenseCus / std::max(1, c->n))) : 1;
+  const size_t ldp = size_t(cpq) * 2048;
+  c->off_dpart = o;   o = align_up(o + (c->dense_k > 1 ? n * c->dense_k * 2 * ldp * 8 : 0));
+  c->off_dcount = o;  o = align_up(o + (cpq ? n * 4 : 0));
   c->total = o;
 }
 
@@ -512,7 +525,8 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
       (e = launch_fill_i64(at<int64_t>(c, c->off_tag) + c->cur * n, int64_t(n), tag_start(c->round), s)) ||
       (e = launch_fill_f32(at<float>(c, c->off_scale), int64_t(n), 1.0f, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err), 1, 0, s)) ||
-      (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)))
+      (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)) ||
+      (e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)))
     return hip_fail(c, e, "workspace init");
   if (c->kind == kCsr) {
     int64_t* scan = at<int64_t>(c, c->off_scan);
@@ -586,7 +600,19 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
     e = launch_rowinfo(a.sched, c->row_ptr, c->y, c->n, c->S, at<RowInfo>(c, c->off_rowinfo), s);
     if (e != hipSuccess) return hip_fail(c, e, "row descriptor kernel");
   }
-  e = (c->kind == kDense) ? launch_sgd_dense(a, s) : launch_sgd_csr(a, s);
+  if (c->kind == kDense && dense_wide_cpq(c->dim)) {
+    DenseSync ds{};
+    ds.part = at<double>(c, c->off_dpart);
+    ds.count = at<uint32_t>(c, c->off_dcount);
+    ds.ldp = int64_t(dense_wide_cpq(c->dim)) * 2048;
+    ds.K = std::max(1, std::min(c->dense_k, dense_wide_max_members(a, c->n_cu) / c->n));
+    ds.spin_limit = kDenseSpinLimit;
+    ds.err = at<int32_t>(c, c->off_err) + kErrRendezvous;
+    e = launch_fill_i32(reinterpret_cast<int32_t*>(ds.count), c->n, 0, s);
+    if (e == hipSuccess) e = launch_sgd_dense_wide(a, ds, s);
+  } else {
+    e = (c->kind == kDense) ? launch_sgd_dense(a, s) : launch_sgd_csr(a, s);
+  }
   if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
   c->half_done = true;
   c->half_scaled = (c->kind == kCsr) && p->l2 > 0.0f;
@@ -714,11 +740,18 @@ extern "C" asap_status asap_check(asap_ctx* c, void* stream, int32_t* bad_worker
   if (bad_worker) *bad_worker = -1;
   if (!c->ws) return fail(c, ASAP_E_STATE, "workspace is not bound");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  int32_t h[2];
+  int32_t h[3];
   hipError_t e;
   if ((e = hipMemcpyAsync(h, at<int32_t>(c, c->off_err), sizeof h, hipMemcpyDeviceToHost, s)) ||
       (e = hipStreamSynchronize(s)))
     return hip_fail(c, e, "error readback");
+  if (h[kErrRendezvous] != 0) {
+    if ((e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)) ||
+        (e = hipStreamSynchronize(s)))
+      return hip_fail(c, e, "error reset");
+    return fail(c, ASAP_E_DEVICE, "dense SGD: %d workgroup rendezvous timed out; the pass was cut short",
+                h[kErrRendezvous]);
+  }
   if (h[0] != 0) {
     if (bad_worker) *bad_worker = h[1];
     if ((e = launch_fill_i32(at<int32_t>(c, c->off_err), 1, 0, s)) ||

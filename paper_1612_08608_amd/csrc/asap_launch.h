@@ -13,7 +13,7 @@ inline int64_t tag_start(int64_t r) { return 2 * r; }
 inline int64_t tag_half(int64_t r) { return 2 * r + 1; }
 
 // Device error words (int32 each).
-enum { kErrEpochCount = 0, kErrEpochWorker = 1, kErrWords = 16 };
+enum { kErrEpochCount = 0, kErrEpochWorker = 1, kErrRendezvous = 2, kErrWords = 16 };
 
 struct MixArgs {
   const float* src;  // [n][ld] models being read (buffer e)
@@ -80,6 +80,22 @@ struct SgdArgs {
 hipError_t launch_schedule(uint64_t seed, int64_t round, int32_t n, int64_t S, int32_t* out,
                            hipStream_t s);
 hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s);
+
+// Dense SGD for dim in (1024, 8192]: K workgroups per worker exchange
+// partial gradients once per step through `part` ([n][K][2][ldp] doubles)
+// and the arrival counters `count` ([n], zero at launch).  A rendezvous that
+// waits longer than spin_limit polls adds 1 to *err and ends the pass.
+struct DenseSync {
+  double* part;
+  uint32_t* count;
+  int64_t ldp;
+  int32_t K;
+  uint32_t spin_limit;
+  int32_t* err;
+};
+int dense_wide_cpq(int64_t dim);                               // 0: not handled
+int dense_wide_max_members(const SgdArgs& a, int n_cu);        // co-resident workgroups
+hipError_t launch_sgd_dense_wide(const SgdArgs& a, const DenseSync& ds, hipStream_t s);
 hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s);
 hipError_t launch_rowinfo(const int32_t* sched, const int64_t* row_ptr, const float* y, int32_t n, int64_t S,
                           RowInfo* out, hipStream_t s);

@@ -21,6 +21,11 @@
 // rows, one wave per row segment with 16-byte loads; the tiles of one column
 // range go to one XCD so that re-reads of a neighbour's segment hit its L2.
 //
+// Precision: the slab kernel accumulates its at most 17 terms with fp32
+// fused multiply-adds (error below 17 ulp of sum_j |P_ij w_j|); the tile and
+// mean kernels take rows of any length (a hub, the complete graph) and
+// accumulate in fp64, rounding once.
+//
 // NOTIFY-ACK (Section 4) on one device: a prologue kernel (the WAIT) checks,
 // one thread per worker, that every in-neighbour carries the tag "published
 // in this round" in buffer e and records the verdict in row_ok; a row with a
@@ -49,6 +54,19 @@ __device__ __forceinline__ void fma4(float4& acc, float w, const float4& x) {
   acc.z = fmaf(w, x.z, acc.z);
   acc.w = fmaf(w, x.w, acc.w);
 }
+
+// fp64 accumulator of one float4 slot: rows of any length (the tile and mean
+// kernels) sum without fp32 error growth; the result is rounded once
+struct Acc4 {
+  double x = 0.0, y = 0.0, z = 0.0, w = 0.0;
+  __device__ void fma(double wt, const float4& v) {
+    x = ::fma(wt, double(v.x), x);
+    y = ::fma(wt, double(v.y), y);
+    z = ::fma(wt, double(v.z), z);
+    w = ::fma(wt, double(v.w), w);
+  }
+  __device__ float4 round() const { return make_float4(float(x), float(y), float(z), float(w)); }
+};
 
 __device__ __forceinline__ void store_tail(float* d, const float4& v, int64_t c, int64_t dim) {
   if (c + 4 <= dim) {
@@ -83,16 +101,15 @@ __global__ __launch_bounds__(kMixThreads) void mix_kernel(MixArgs a, uint32_t ns
   for (int r = row0 + wave; r < row1; r += kMixThreads / 64) {
     if (!a.row_ok[r]) continue;
     if (c < a.dim) {
-      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      Acc4 acc;
       const int p0 = a.nbr_ptr[r], p1 = a.nbr_ptr[r + 1];
       for (int p = p0; p < p1; ++p) {
         const int j = a.nbr_idx[p];
-        float wt = a.nbr_w[p];
-        if (a.scale) wt *= a.scale[j];
-        const float4 x = *reinterpret_cast<const float4*>(a.src + int64_t(j) * a.ld + c);
-        fma4(acc, wt, x);
+        double wt = a.nbr_w[p];
+        if (a.scale) wt *= double(a.scale[j]);
+        acc.fma(wt, *reinterpret_cast<const float4*>(a.src + int64_t(j) * a.ld + c));
       }
-      store_tail(a.dst + int64_t(r) * a.ld + c, acc, c, a.dim);
+      store_tail(a.dst + int64_t(r) * a.ld + c, acc.round(), c, a.dim);
     }
     if (seg == 0 && lane == 0) a.tag_dst[r] = a.next;
   }
@@ -101,9 +118,9 @@ __global__ __launch_bounds__(kMixThreads) void mix_kernel(MixArgs a, uint32_t ns
 // Complete graph with uniform weights (all-reduce, Figure 2a): every output
 // row is the same weighted column sum, so compute it once per column and
 // broadcast it: n reads and n writes per column instead of n^2 reads.  The
-// sum runs over j ascending with the same fused multiply-adds as mix_kernel,
-// so both kernels produce identical bits on this graph.  On the complete
-// graph one stale worker makes every row stale.
+// sum runs over j ascending with the same fp64 fused multiply-adds as
+// mix_kernel, so both kernels produce identical bits on this graph.  On the
+// complete graph one stale worker makes every row stale.
 __global__ __launch_bounds__(64) void mean_kernel(MixArgs a, uint32_t nseg) {
   const uint32_t seg = xcd_tile(blockIdx.x, nseg);
   const int lane = threadIdx.x;
@@ -112,17 +129,17 @@ __global__ __launch_bounds__(64) void mean_kernel(MixArgs a, uint32_t nseg) {
   if (__ballot(stale) != 0ull) return;
   const int64_t c = int64_t(seg) * kSegFloats + lane * 4;
   if (c < a.dim) {
-    const float w0 = a.nbr_w[0];
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    const double w0 = a.nbr_w[0];
+    Acc4 acc;
 #pragma unroll 8
     for (int j = 0; j < a.n; ++j) {
-      float wt = w0;
-      if (a.scale) wt *= a.scale[j];
-      const float4 x = *reinterpret_cast<const float4*>(a.src + int64_t(j) * a.ld + c);
-      fma4(acc, wt, x);
+      double wt = w0;
+      if (a.scale) wt *= double(a.scale[j]);
+      acc.fma(wt, *reinterpret_cast<const float4*>(a.src + int64_t(j) * a.ld + c));
     }
+    const float4 out = acc.round();
 #pragma unroll 4
-    for (int j = 0; j < a.n; ++j) store_tail(a.dst + int64_t(j) * a.ld + c, acc, c, a.dim);
+    for (int j = 0; j < a.n; ++j) store_tail(a.dst + int64_t(j) * a.ld + c, out, c, a.dim);
   }
   if (seg == 0)
     for (int j = lane; j < a.n; j += 64) a.tag_dst[j] = a.next;

@@ -173,6 +173,37 @@ def test_dense_shapes(torch, n, dim, S, B, l2):
     _free_run(torch, wl, "complete", 0, 3, W0=W0)
 
 
+# dim in (1024, 8192] takes the wide dense kernel: several workgroups per
+# worker (up to 8) split every minibatch and meet once per step
+@pytest.mark.parametrize("n,dim,S,B,l2,loss", [
+    (3, 1025, 40, 5, 0.0, "logistic"),    # one float4 per thread, ragged dim, B < members
+    (2, 2048, 33, 8, 0.05, "logistic"),   # ragged last minibatch, L2
+    (6, 3001, 100, 16, 0.0, "hinge"),     # two float4 per thread, hinge
+    (2, 8192, 24, 3, 0.0, "logistic"),    # four float4 per thread, B < members
+    (300, 1500, 16, 4, 0.0, "logistic"),  # more workers than compute units: one workgroup each
+])
+def test_dense_wide_kernel_shapes(torch, n, dim, S, B, l2, loss):
+    wl = synth.DENSE_LR_32W.with_(n_workers=n, dim=dim, samples=S, batch=B, l2=l2, loss=loss,
+                                  lr_kind="inv_sqrt", lr0=0.3)
+    W0 = synth.initial_models(wl.with_(seed=5)) * np.float32(0.01)
+    _free_run(torch, wl, "complete" if n > 8 else "ring" if n >= 3 else "complete", 2, 3, W0=W0)
+
+
+def test_dense_wide_run_twice_is_bitwise_identical(torch):
+    wl = synth.DENSE_LR_32W.with_(n_workers=4, samples=96, batch=32)
+    p, i, w = graph("ring", 4)
+    X, y = synth.dense_data(wl)
+    out = []
+    for _ in range(2):
+        sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
+        sess.bind_dense(X, y)
+        for _ in range(2):
+            sess.round(params(wl))
+        out.append(sess.models().cpu().numpy().copy())
+        sess.close()
+    assert np.array_equal(out[0].view(np.uint32), out[1].view(np.uint32))
+
+
 def test_dense_32w_launch_shape_reduced_samples(torch):
     # the 32-worker dense workload's launch shape (D = 4096, B = 256, 6-regular)
     # with 2048 samples per worker instead of 65536
