@@ -69,7 +69,7 @@ struct asap_ctx {
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_sched = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
-         off_rowinfo = 0, off_code = 0, off_lut = 0, off_hot = 0, off_dpart = 0, off_dcount = 0,
+         off_rowinfo = 0, off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dcount = 0,
          total = 0;
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
@@ -131,7 +131,7 @@ void layout(asap_ctx* c) {
   const int cpq = c->kind == kDense ? dense_wide_cpq(c->dim) : 0;
   c->dense_k = cpq ? std::max(1, std::min(kDenseMaxMembers, kDenseCus / std::max(1, c->n))) : 1;
   const size_t ldp = size_t(cpq) * 2048;
-  c->off_dpart = o;   o = align_up(o + (c->dense_k > 1 ? n * c->dense_k * 2 * ldp * 8 : 0));
+  c->off_dacc = o;    o = align_up(o + (c->dense_k > 1 ? 3 * n * ldp * 8 : 0));
   c->off_dcount = o;  o = align_up(o + (cpq ? n * 4 : 0));
   c->total = o;
 }
@@ -528,6 +528,20 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
       (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)))
     return hip_fail(c, e, "workspace init");
+  if (c->kind == kDense && dense_wide_cpq(c->dim)) {
+    // max |x| per shard (the fixed-point scale of the member exchange),
+    // labels and finiteness
+    int64_t* scan = at<int64_t>(c, c->off_scan);
+    if ((e = launch_fill_i64(scan, 8, 0, s)) || (e = launch_fill_f32(at<float>(c, c->off_vmax), c->n, 0.0f, s)) ||
+        (e = launch_dense_scan(c->X, c->y, c->n, c->S, c->dim, c->ldx, at<float>(c, c->off_vmax),
+                               reinterpret_cast<unsigned long long*>(scan), s)))
+      return hip_fail(c, e, "dense scan");
+    int64_t h[2];
+    if ((e = hipMemcpyAsync(h, scan, sizeof h, hipMemcpyDeviceToHost, s)) || (e = hipStreamSynchronize(s)))
+      return hip_fail(c, e, "dense scan readback");
+    if (h[0]) return fail(c, ASAP_E_INVALID_ARG, "%lld labels outside {-1, +1}", (long long)h[0]);
+    if (h[1]) return fail(c, ASAP_E_INVALID_ARG, "%lld feature values are not finite", (long long)h[1]);
+  }
   if (c->kind == kCsr) {
     int64_t* scan = at<int64_t>(c, c->off_scan);
     if ((e = launch_fill_i64(scan, 8, 0, s)) ||
@@ -602,13 +616,15 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
   }
   if (c->kind == kDense && dense_wide_cpq(c->dim)) {
     DenseSync ds{};
-    ds.part = at<double>(c, c->off_dpart);
+    ds.acc = at<int64_t>(c, c->off_dacc);
+    ds.xmax = at<float>(c, c->off_vmax);
     ds.count = at<uint32_t>(c, c->off_dcount);
     ds.ldp = int64_t(dense_wide_cpq(c->dim)) * 2048;
     ds.K = std::max(1, std::min(c->dense_k, dense_wide_max_members(a, c->n_cu) / c->n));
     ds.spin_limit = kDenseSpinLimit;
     ds.err = at<int32_t>(c, c->off_err) + kErrRendezvous;
     e = launch_fill_i32(reinterpret_cast<int32_t*>(ds.count), c->n, 0, s);
+    if (e == hipSuccess && ds.K > 1) e = launch_fill_i64(ds.acc, 3 * int64_t(c->n) * ds.ldp, 0, s);
     if (e == hipSuccess) e = launch_sgd_dense_wide(a, ds, s);
   } else {
     e = (c->kind == kDense) ? launch_sgd_dense(a, s) : launch_sgd_csr(a, s);

@@ -81,18 +81,22 @@ hipError_t launch_schedule(uint64_t seed, int64_t round, int32_t n, int64_t S, i
                            hipStream_t s);
 hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s);
 
-// Dense SGD for dim in (1024, 8192]: K workgroups per worker exchange
-// partial gradients once per step through `part` ([n][K][2][ldp] doubles)
-// and the arrival counters `count` ([n], zero at launch).  A rendezvous that
+// Dense SGD for dim in (1024, 8192]: K workgroups per worker sum their
+// partial gradients once per step as 64-bit fixed point in `acc`
+// ([3][n][ldp], zero at launch), scaled from xmax ([n], max |x| of each
+// shard); `count` ([n], zero at launch) counts arrivals.  A rendezvous that
 // waits longer than spin_limit polls adds 1 to *err and ends the pass.
 struct DenseSync {
-  double* part;
+  int64_t* acc;
+  const float* xmax;
   uint32_t* count;
   int64_t ldp;
   int32_t K;
   uint32_t spin_limit;
   int32_t* err;
 };
+hipError_t launch_dense_scan(const float* X, const float* y, int32_t n, int64_t S, int64_t dim, int64_t ldx,
+                             float* xmax, unsigned long long* out, hipStream_t s);
 int dense_wide_cpq(int64_t dim);                               // 0: not handled
 int dense_wide_max_members(const SgdArgs& a, int n_cu);        // co-resident workgroups
 hipError_t launch_sgd_dense_wide(const SgdArgs& a, const DenseSync& ds, hipStream_t s);

@@ -7,8 +7,9 @@
 // MFMA is not used.  One workgroup per worker would leave most of the chip
 // idle when workers are few, so K workgroups share a worker: each holds the
 // whole model slice in registers, takes a contiguous K-th of every
-// minibatch, and the K partial gradients are exchanged once per step through
-// the workspace (written, counted in, read back and summed in member order).
+// minibatch, and the K partial gradients are summed once per step in the
+// workspace as exact 64-bit fixed point (device-scope integer atomics), so
+// the sum is the same whatever the order the members arrive in.
 // The launch is cooperative, so every member is resident and the rendezvous
 // cannot wait on a workgroup that has not started; the wait is bounded
 // anyway and reports a timeout instead of spinning for ever.
@@ -18,9 +19,9 @@
 // loaded while the current one is reduced, and one LDS barrier per sub-batch
 // suffices (per-wave partial margins are double-buffered in LDS).
 //
-// Determinism: a thread's partial dot is an fp32 sum of its 4*CPQ products;
-// partials are summed in fp64 by a fixed lane tree, then over the rows of a
-// wave and over waves in index order; the gradient is accumulated in fp64 in
+// Determinism: a thread's partial dot is an fp64 sum of its 4*CPQ products;
+// partials are summed in fp64 by a fixed transposed butterfly over each
+// 16-lane row, then over rows and waves in index order; the gradient is accumulated in fp64 in
 // batch order and the K partials are added in member order.  Every member
 // applies the same update, so the K copies of the model stay identical.
 #include <cmath>
@@ -34,43 +35,63 @@ constexpr int kThreads = 512;  // 8 waves: 256 registers per lane for the row pr
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxBatch = 512;  // minibatch limit of asap_sgd_params
 
-__device__ __forceinline__ double loss_coef(double m, double y, int loss) {
-  const double ym = y * m;
-  if (loss == 1) return ym < 1.0 ? -y : 0.0;  // hinge
-  return -y / (1.0 + exp(ym));                // logistic
+// d loss(y m) / d m from an fp64 margin: the hinge decision y m < 1 is taken
+// in fp64; the logistic factor 1 / (1 + e^{y m}) needs only fp32 accuracy.
+__device__ __forceinline__ float loss_coef(double m, float y, int loss) {
+  const double ym = double(y) * m;
+  if (loss == 1) return ym < 1.0 ? -y : 0.f;  // hinge
+  return -y / (1.f + expf(float(ym)));         // logistic
 }
 
 __device__ __forceinline__ double step_size(int lr_kind, float lr0, int64_t t) {
   return lr_kind == 0 ? double(lr0) : double(lr0) / sqrt(double(t));
 }
 
-// sum over the 16 lanes of a DPP row; every lane of the row gets the same
-// bits (the four stages pair lanes symmetrically and fp addition commutes)
-__device__ __forceinline__ double row16_sum(double v) {
-#define ASAP_DPP_STAGE(ctrl)                                                                  \
-  {                                                                                           \
-    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), ctrl, 0xF, 0xF, false); \
-    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), ctrl, 0xF, 0xF, false); \
-    v += __hiloint2double(hi, lo);                                                            \
-  }
-  ASAP_DPP_STAGE(0xB1)   // quad_perm [1,0,3,2]
-  ASAP_DPP_STAGE(0x4E)   // quad_perm [2,3,0,1]
-  ASAP_DPP_STAGE(0x141)  // row_half_mirror
-  ASAP_DPP_STAGE(0x140)  // row_mirror
-#undef ASAP_DPP_STAGE
-  return v;
+template <int CTRL>
+__device__ __forceinline__ int dpp(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
 }
 
-__device__ __forceinline__ double lane_value(double v, int lane) {
-  const int lo = __builtin_amdgcn_readlane(__double2loint(v), lane);
-  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), lane);
+template <int S>
+__device__ __forceinline__ double xor_lane(double v) {
+  int lo = __double2loint(v), hi = __double2hiint(v);
+  if constexpr (S == 1) {
+    lo = dpp<0xB1>(lo); hi = dpp<0xB1>(hi);    // quad_perm [1,0,3,2]
+  } else if constexpr (S == 2) {
+    lo = dpp<0x4E>(lo); hi = dpp<0x4E>(hi);    // quad_perm [2,3,0,1]
+  } else if constexpr (S == 4) {               // i -> i ^ 7 in 8 lanes, then i ^ 3
+    lo = dpp<0x1B>(dpp<0x141>(lo)); hi = dpp<0x1B>(dpp<0x141>(hi));
+  } else {
+    static_assert(S == 8, "xor_lane: S in {1, 2, 4, 8}");
+    lo = dpp<0x128>(lo); hi = dpp<0x128>(hi);  // row_ror:8
+  }
   return __hiloint2double(hi, lo);
 }
 
-// wave total, uniform: rows summed as ((r0 + r1) + r2) + r3
-__device__ __forceinline__ double wave_total(double v) {
-  v = row16_sum(v);
-  return ((lane_value(v, 0) + lane_value(v, 16)) + lane_value(v, 32)) + lane_value(v, 48);
+// One butterfly stage of a transposed reduction: a lane keeps the half of
+// its N values whose index bit matches its lane bit S, sends the other half
+// to lane ^ S, and adds what it receives.  Value j of the result is input
+// value 2j + (lane & S ? 1 : 0) (counting the bits used so far).
+template <int S, int N>
+__device__ __forceinline__ void halve(double (&d)[16], int lane) {
+  const bool hi = lane & S;
+#pragma unroll
+  for (int j = 0; j < N / 2; ++j) {
+    const double keep = hi ? d[2 * j + 1] : d[2 * j];
+    const double send = hi ? d[2 * j] : d[2 * j + 1];
+    d[j] = keep + xor_lane<S>(send);
+  }
+}
+
+// SR values per lane -> lane l holds the sum over its 16-lane DPP row of
+// value (l mod SR); each sum is formed on fixed lanes in a fixed order.
+template <int SR>
+__device__ __forceinline__ double row_reduce(double (&d)[16], int lane) {
+  if constexpr (SR >= 2) halve<1, SR>(d, lane); else d[0] += xor_lane<1>(d[0]);
+  if constexpr (SR >= 4) halve<2, SR / 2>(d, lane); else d[0] += xor_lane<2>(d[0]);
+  if constexpr (SR >= 8) halve<4, SR / 4>(d, lane); else d[0] += xor_lane<4>(d[0]);
+  if constexpr (SR >= 16) halve<8, SR / 8>(d, lane); else d[0] += xor_lane<8>(d[0]);
+  return d[0];
 }
 
 __device__ __forceinline__ void lds_barrier() {
@@ -79,13 +100,9 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-__device__ __forceinline__ float dot4(const float4& a, const float4& b) {
-  return fmaf(a.w, b.w, fmaf(a.z, b.z, fmaf(a.y, b.y, a.x * b.x)));
-}
-
 template <int CPQ, int SR>
 __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, DenseSync ds) {
-  __shared__ double red[2][kWaves][SR];
+  __shared__ double red[2][kWaves][4][SR];  // per-row partial margins
   __shared__ int ridx[2][kMaxBatch];  // this member's row indices of steps t, t+1 (slot t & 1)
   __shared__ int abort_flag;
   const int K = ds.K;
@@ -125,9 +142,27 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     }
     w[q] = v;
   }
+  double wd[CPQ][4];  // the model slice widened once per step for the dots
+  auto widen = [&]() {
+#pragma unroll
+    for (int q = 0; q < CPQ; ++q) {
+      wd[q][0] = w[q].x; wd[q][1] = w[q].y; wd[q][2] = w[q].z; wd[q][3] = w[q].w;
+    }
+  };
+  widen();
 
   const int B = a.batch, S = int(a.S);  // S < 2^31 (checked at bind)
   const int KS = (S + B - 1) / B;
+  // fixed-point scale of the member exchange: |gradient entry| <= B max|x|
+  // <= 2^ex, so 2^(62 - ex) keeps every partial and every sum below 2^62
+  double fx = 1.0, inv_fx = 1.0;
+  if (K > 1) {
+    int ex = 0;
+    const double bound = double(B) * double(ds.xmax[i]);
+    if (bound > 0.0) frexp(bound, &ex);
+    fx = ldexp(1.0, 62 - ex);
+    inv_fx = ldexp(1.0, ex - 62);
+  }
   // valid components of the thread's last float4 of each q (entries of X
   // past dim are never used)
   int nv[CPQ];
@@ -142,10 +177,16 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   struct Pos {
     int t, sb, lo, hi;
   };
+  // member offsets of a full step and of the (possibly shorter) last one,
+  // computed once (Bp <= 512, so 32-bit products are exact)
+  const int Blast = S - (KS - 1) * B;
+  const int off0 = (B * k) / K, off1 = (B * (k + 1)) / K;
+  const int last0 = (Blast * k) / K, last1 = (Blast * (k + 1)) / K;
   auto share = [&](int t, int& lo_, int& hi_) {
-    const int b0 = t * B, Bp = min(B, S - b0);
-    lo_ = b0 + int((int64_t(Bp) * k) / K);
-    hi_ = b0 + int((int64_t(Bp) * (k + 1)) / K);
+    const int b0 = t * B;
+    const bool last = t == KS - 1;
+    lo_ = b0 + (last ? last0 : off0);
+    hi_ = b0 + (last ? last1 : off1);
   };
   auto settle = [&](Pos p) {  // move past steps in which this member has no samples
     while (p.t < KS && p.sb >= p.hi) {
@@ -207,36 +248,83 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
 
   // margins, coefficients and gradient of the sub-batch held in xc
   auto process = [&](float4 (&xc)[SR][CPQ], float yl, Pos p) {
-    double mine = 0.0;  // lane s < SR: this wave's part of row s's margin
+    // fp64 partial dots of the SR rows (single products of scaled columns
+    // can dwarf the margin), then one transposed fp64 reduction over each
+    // 16-lane DPP row; lanes 16r + s (s < SR) hold row r's share
+    double d[16];
 #pragma unroll
     for (int s = 0; s < SR; ++s) {
-      float d = 0.f;
+      double dd = 0.0;
 #pragma unroll
-      for (int q = 0; q < CPQ; ++q) d += dot4(w[q], xc[s][q]);
-      const double t = wave_total(double(d));
-      mine = lane == s ? t : mine;
+      for (int q = 0; q < CPQ; ++q) {
+        dd = fma(wd[q][0], double(xc[s][q].x), dd);
+        dd = fma(wd[q][1], double(xc[s][q].y), dd);
+        dd = fma(wd[q][2], double(xc[s][q].z), dd);
+        dd = fma(wd[q][3], double(xc[s][q].w), dd);
+      }
+      d[s] = dd;
     }
-    if (lane < SR) red[par][wave][lane] = mine;
+    const double part = row_reduce<SR>(d, lane);
+    if ((lane & 15) < SR) red[par][wave][lane >> 4][lane & 15] = part;
     lds_barrier();
-    double cf = 0.0;
+    float cf = 0.f;
     if (lane < SR && lane < p.hi - p.sb) {
       double m = 0.0;
 #pragma unroll
-      for (int v = 0; v < kWaves; ++v) m += red[par][v][lane];
-      cf = loss_coef(m, double(yl), a.loss);
+      for (int v = 0; v < kWaves; ++v)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) m += red[par][v][r][lane];
+      cf = loss_coef(m, yl, a.loss);
     }
     par ^= 1;
+    // the sub-batch's contribution in fp32 (at most SR terms), added to the
+    // step's fp64 gradient
+    float4 gs[CPQ];
+#pragma unroll
+    for (int q = 0; q < CPQ; ++q) gs[q] = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int s = 0; s < SR; ++s) {
-      const double c = lane_value(cf, s);
+      const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cf), s));
 #pragma unroll
       for (int q = 0; q < CPQ; ++q) {
-        g[q][0] = fma(c, double(xc[s][q].x), g[q][0]);
-        g[q][1] = fma(c, double(xc[s][q].y), g[q][1]);
-        g[q][2] = fma(c, double(xc[s][q].z), g[q][2]);
-        g[q][3] = fma(c, double(xc[s][q].w), g[q][3]);
+        gs[q].x = fmaf(c, xc[s][q].x, gs[q].x);
+        gs[q].y = fmaf(c, xc[s][q].y, gs[q].y);
+        gs[q].z = fmaf(c, xc[s][q].z, gs[q].z);
+        gs[q].w = fmaf(c, xc[s][q].w, gs[q].w);
       }
     }
+#pragma unroll
+    for (int q = 0; q < CPQ; ++q) {
+      g[q][0] += double(gs[q].x);
+      g[q][1] += double(gs[q].y);
+      g[q][2] += double(gs[q].z);
+      g[q][3] += double(gs[q].w);
+    }
+  };
+
+  // Members of a worker meet here.  Everything they share is written and
+  // read with relaxed device-scope atomics (coherent for the whole device
+  // without cache write-back or invalidation); a wave's writes are
+  // acknowledged before the barrier, and one thread counts the workgroup in
+  // and waits, for a bounded time, until all K members have arrived.
+  auto rendezvous = [&](uint32_t target) -> bool {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+      __hip_atomic_fetch_add(ds.count + i, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      uint32_t spins = 0;
+      while (__hip_atomic_load(ds.count + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        if (++spins > ds.spin_limit) {
+          abort_flag = 1;
+          __hip_atomic_fetch_add(ds.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+    __syncthreads();
+    return abort_flag == 0;
   };
 
   // end of step t: exchange (K > 1) and update; false when the rendezvous
@@ -244,44 +332,39 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   auto finish_step = [&](int t) -> bool {
     const int Bp = min(B, S - t * B);
     if (K > 1) {
-      double* mine = ds.part + ((int64_t(i) * K + k) * 2 + (t & 1)) * ds.ldp;
+      // members add their partials as exact 64-bit fixed point into
+      // acc[t mod 3] (integer addition commutes: the sum does not depend on
+      // arrival order), each clears its column slice of acc[(t+1) mod 3]
+      // (last read before the previous rendezvous, next written after this
+      // one), then all read the sum back
+      int64_t* acc = ds.acc + (int64_t(t % 3) * a.n + i) * ds.ldp;
 #pragma unroll
       for (int q = 0; q < CPQ; ++q) {
         const int64_t c = 4 * (int64_t(tid) + int64_t(kThreads) * q);
-        *reinterpret_cast<double2*>(mine + c) = make_double2(g[q][0], g[q][1]);
-        *reinterpret_cast<double2*>(mine + c + 2) = make_double2(g[q][2], g[q][3]);
-      }
-      __threadfence();
-      __syncthreads();
-      if (tid == 0) {
-        __hip_atomic_fetch_add(ds.count + i, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        const uint32_t target = uint32_t(K) * uint32_t(t + 1);
-        uint32_t spins = 0;
-        while (__hip_atomic_load(ds.count + i, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
-          if (++spins > ds.spin_limit) {
-            abort_flag = 1;
-            __hip_atomic_fetch_add(ds.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            break;
-          }
-          __builtin_amdgcn_s_sleep(2);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const long long v = __double2ll_rn(g[q][e] * fx);
+          if (v != 0)
+            __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(acc + c + e), static_cast<unsigned long long>(v),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
       }
-      __syncthreads();
-      if (abort_flag) return false;
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      {
+        int64_t* nxt = ds.acc + (int64_t((t + 1) % 3) * a.n + i) * ds.ldp;
+        const int64_t L = (ds.ldp + K - 1) / K, c0 = k * L, c1 = min(c0 + L, ds.ldp);
+        for (int64_t c = c0 + tid; c < c1; c += kThreads)
+          __hip_atomic_store(reinterpret_cast<unsigned long long*>(nxt + c), 0ull, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+      }
+      if (!rendezvous(uint32_t(K) * uint32_t(t + 1))) return false;
 #pragma unroll
-      for (int q = 0; q < CPQ; ++q)
+      for (int q = 0; q < CPQ; ++q) {
+        const int64_t c = 4 * (int64_t(tid) + int64_t(kThreads) * q);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) g[q][e] = 0.0;
-      for (int m = 0; m < K; ++m) {
-        const double* pm = ds.part + ((int64_t(i) * K + m) * 2 + (t & 1)) * ds.ldp;
-#pragma unroll
-        for (int q = 0; q < CPQ; ++q) {
-          const int64_t c = 4 * (int64_t(tid) + int64_t(kThreads) * q);
-          const double2 u = *reinterpret_cast<const double2*>(pm + c);
-          const double2 v = *reinterpret_cast<const double2*>(pm + c + 2);
-          g[q][0] += u.x; g[q][1] += u.y; g[q][2] += v.x; g[q][3] += v.y;
-        }
+        for (int e = 0; e < 4; ++e)
+          g[q][e] = double(static_cast<long long>(__hip_atomic_load(
+                        reinterpret_cast<unsigned long long*>(acc + c + e), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) *
+                    inv_fx;
       }
     }
     const double eta = step_size(a.lr_kind, a.lr0, a.round * KS + t + 1);
@@ -295,8 +378,12 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
 #pragma unroll
       for (int e = 0; e < 4; ++e) g[q][e] = 0.0;
     }
-    // every wave has passed a barrier since its last read of slot t & 1
+    widen();
+    // every wave has passed a barrier since its last read of slot t & 1;
+    // the barrier after the write orders it before the first read of step
+    // t + 2, which can come right after this step when steps are short
     stage(t + 2);
+    lds_barrier();
     fetch(t + 3);
     return true;
   };
@@ -367,7 +454,50 @@ hipError_t launch_wide(const SgdArgs& a, const DenseSync& ds, hipStream_t s) {
                                     args, 0, s);
 }
 
+// Bind-time scan of dense shards: xmax[i] = max |x| over worker i's shard
+// (columns < dim); out[0] += labels outside {-1, +1}, out[1] += entries that
+// are not finite.  Grid: n x blocks_per_worker blocks of 256 threads.
+__global__ __launch_bounds__(256) void dense_scan_kernel(const float* X, const float* y, int64_t S, int64_t dim,
+                                                        int64_t ldx, uint32_t bpw, float* xmax,
+                                                        unsigned long long* out) {
+  const int i = int(blockIdx.x / bpw);
+  const int64_t part = blockIdx.x % bpw;
+  const int64_t r0 = S * part / bpw, r1 = S * (part + 1) / bpw;
+  float m = 0.f;
+  unsigned long long nonfinite = 0, bady = 0;
+  for (int64_t r = r0; r < r1; ++r) {
+    const float* row = X + (int64_t(i) * S + r) * ldx;
+    for (int64_t c = threadIdx.x; c < dim; c += 256) {
+      const float v = row[c];
+      nonfinite += !isfinite(v);
+      m = fmaxf(m, fabsf(v));
+    }
+    if (threadIdx.x == 0) {
+      const float yy = y[int64_t(i) * S + r];
+      bady += (yy != 1.0f && yy != -1.0f);
+    }
+  }
+  __shared__ float sm[256];
+  sm[threadIdx.x] = m;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) sm[threadIdx.x] = fmaxf(sm[threadIdx.x], sm[threadIdx.x + o]);
+    __syncthreads();
+  }
+  // non-negative floats order like their bit patterns
+  if (threadIdx.x == 0) atomicMax(reinterpret_cast<unsigned int*>(xmax + i), __float_as_uint(sm[0]));
+  if (bady) atomicAdd(out, bady);
+  if (nonfinite) atomicAdd(out + 1, nonfinite);
+}
+
 }  // namespace
+
+hipError_t launch_dense_scan(const float* X, const float* y, int32_t n, int64_t S, int64_t dim, int64_t ldx,
+                             float* xmax, unsigned long long* out, hipStream_t s) {
+  const uint32_t bpw = uint32_t(std::max<int64_t>(1, std::min<int64_t>(64, S / 16)));
+  hipLaunchKernelGGL(dense_scan_kernel, dim3(uint32_t(n) * bpw), dim3(256), 0, s, X, y, S, dim, ldx, bpw, xmax, out);
+  return hipGetLastError();
+}
 
 int dense_wide_cpq(int64_t dim) {
   if (dim <= 1024 || dim > 8192) return 0;
@@ -377,9 +507,9 @@ int dense_wide_cpq(int64_t dim) {
 int dense_wide_max_members(const SgdArgs& a, int n_cu) {
   int per = 0;
   switch (dense_wide_cpq(a.dim)) {
-    case 1: hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, sgd_dense_wide_kernel<1, 8>, kThreads, 0); break;
-    case 2: hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, sgd_dense_wide_kernel<2, 8>, kThreads, 0); break;
-    case 4: hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, sgd_dense_wide_kernel<4, 2>, kThreads, 0); break;
+    case 1: (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, sgd_dense_wide_kernel<1, 8>, kThreads, 0); break;
+    case 2: (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, sgd_dense_wide_kernel<2, 8>, kThreads, 0); break;
+    case 4: (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, sgd_dense_wide_kernel<4, 1>, kThreads, 0); break;
     default: return 1;
   }
   return std::max(1, per) * n_cu;
@@ -389,7 +519,7 @@ hipError_t launch_sgd_dense_wide(const SgdArgs& a, const DenseSync& ds, hipStrea
   switch (dense_wide_cpq(a.dim)) {
     case 1: return launch_wide<1, 8>(a, ds, s);
     case 2: return launch_wide<2, 8>(a, ds, s);
-    case 4: return launch_wide<4, 2>(a, ds, s);
+    case 4: return launch_wide<4, 1>(a, ds, s);
     default: return hipErrorInvalidValue;
   }
 }
