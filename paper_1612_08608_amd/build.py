@@ -22,7 +22,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libasap.so")
 
 SOURCES = ["asap_host.cpp", "kernels_mix.hip", "kernels_sgd.hip", "kernels_dense.hip", "kernels_csr.hip",
-           "kernels_metrics.hip"]
+           "kernels_csr_plan.hip", "kernels_metrics.hip"]
 
 ARCH = "gfx950"
 FLAGS = [

@@ -70,6 +70,7 @@ struct asap_ctx {
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_sched = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
          off_rowinfo = 0, off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dcount = 0,
+         off_soff = 0, off_coder = 0, off_clist = 0, off_clink = 0, off_hlist = 0, off_cnt = 0, off_pflag = 0,
          total = 0;
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
@@ -128,6 +129,15 @@ void layout(asap_ctx* c) {
   c->off_code = o;    o = align_up(o + (csr ? size_t(c->nnz) * 4 : 0));
   c->off_lut = o;     o = align_up(o + (csr ? size_t(c->dim) * 2 : 0));
   c->off_hot = o;     o = align_up(o + (csr ? size_t(kHotMax) * 4 : 0));
+  // per-round plan of the CSR pass: one entry per nonzero per list
+  const size_t nz = csr ? size_t(c->nnz) : 0, nS = csr ? n * size_t(c->S) : 0;
+  c->off_soff = o;    o = align_up(o + (csr ? n * (size_t(c->S) + 1) * 4 : 0));
+  c->off_coder = o;   o = align_up(o + nz * 4);
+  c->off_clist = o;   o = align_up(o + nz * 4);
+  c->off_clink = o;   o = align_up(o + nz * 4);
+  c->off_hlist = o;   o = align_up(o + nz * 4);
+  c->off_cnt = o;     o = align_up(o + nS * 2 * 4);
+  c->off_pflag = o;   o = align_up(o + (csr ? 4 : 0));
   const int cpq = c->kind == kDense ? dense_wide_cpq(c->dim) : 0;
   c->dense_k = cpq ? std::max(1, std::min(kDenseMaxMembers, kDenseCus / std::max(1, c->n))) : 1;
   const size_t ldp = size_t(cpq) * 2048;
@@ -614,7 +624,31 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
     e = launch_rowinfo(a.sched, c->row_ptr, c->y, c->n, c->S, at<RowInfo>(c, c->off_rowinfo), s);
     if (e != hipSuccess) return hip_fail(c, e, "row descriptor kernel");
   }
-  if (c->kind == kDense && dense_wide_cpq(c->dim)) {
+  if (c->kind == kCsr && csr_plan_fits(a)) {
+    // plan the round's column bookkeeping for all workers and steps, then
+    // run the planned pass; the general kernel runs only if the plan says a
+    // step does not fit
+    PlanArgs pa{};
+    pa.rowinfo = a.rowinfo;
+    pa.code = a.code;
+    pa.row_ptr = c->row_ptr;
+    pa.n = c->n;
+    pa.S = c->S;
+    pa.batch = p->batch;
+    pa.K = int32_t((c->S + p->batch - 1) / p->batch);
+    pa.step_off = at<int32_t>(c, c->off_soff);
+    pa.code_r = at<int32_t>(c, c->off_coder);
+    pa.clist = at<int32_t>(c, c->off_clist);
+    pa.clink = at<int32_t>(c, c->off_clink);
+    pa.hlist = at<int32_t>(c, c->off_hlist);
+    pa.cnt = at<int32_t>(c, c->off_cnt);
+    pa.flag = at<int32_t>(c, c->off_pflag);
+    e = launch_fill_i32(pa.flag, 1, 0, s);
+    if (e == hipSuccess) e = launch_csr_plan(pa, c->max_row, s);
+    if (e == hipSuccess) e = launch_sgd_csr_fast(a, pa, s);
+    a.run_if = pa.flag;
+    if (e == hipSuccess) e = launch_sgd_csr(a, s);
+  } else if (c->kind == kDense && dense_wide_cpq(c->dim)) {
     DenseSync ds{};
     ds.acc = at<int64_t>(c, c->off_dacc);
     ds.xmax = at<float>(c, c->off_vmax);

@@ -75,7 +75,32 @@ struct SgdArgs {
   float* scale;     // [n] out: final L2 scale (CSR)
   int64_t* tag;     // [n] tags of the current buffer
   int64_t tag_value;
+  const int32_t* run_if;  // CSR general kernel: when set, run only if *run_if != 0
 };
+
+// Per-round plan of a CSR pass (see kernels_csr_plan.hip).  The per-step
+// lists live in the region of the worker's nonzeros where that step's
+// nonzeros start in schedule order (step_off), so each list array has one
+// entry per nonzero.
+struct PlanArgs {
+  const RowInfo* rowinfo;   // [n][S] this round's rows in schedule order
+  const int32_t* code;      // [nnz] static codes: -(hot slot + 2) or column
+  const int64_t* row_ptr;   // [n*S+1]
+  int32_t n;
+  int64_t S;
+  int32_t batch;
+  int32_t K;                // steps per pass
+  int32_t* step_off;        // [n][S+1]
+  int32_t* code_r;          // [nnz] this round: -(hot slot + 2) or cold slot
+  int32_t* clist;           // [nnz] cold columns of each step, by slot
+  int32_t* clink;           // [nnz] slot of the same column in the previous step, or -1
+  int32_t* hlist;           // [nnz] distinct hot slots of each step
+  int32_t* cnt;             // [n][S][2] distinct cold, hot per step
+  int32_t* flag;            // [1] set when some step does not fit the fast kernel
+};
+bool csr_plan_fits(const SgdArgs& a);
+hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s);
+hipError_t launch_sgd_csr_fast(const SgdArgs& a, const PlanArgs& p, hipStream_t s);
 
 hipError_t launch_schedule(uint64_t seed, int64_t round, int32_t n, int64_t S, int32_t* out,
                            hipStream_t s);

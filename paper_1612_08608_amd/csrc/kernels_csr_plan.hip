@@ -1,0 +1,545 @@
+// kernels_csr_plan.hip -- the CSR SGD pass with its column bookkeeping done
+// ahead of time (Appendix A, update (A.2), first line; Section 5: each
+// replica trains on its own data partition).
+//
+// The steps of a worker's pass form a dependency chain, but which columns a
+// step touches is known once the round's schedule is: it does not depend on
+// the model.  So the bookkeeping that a step would otherwise do on the chain
+// -- finding the distinct columns of its minibatch, giving each a slot, and
+// finding which of them the previous step also changed -- runs before the
+// pass, for all workers and all steps at once:
+//
+//  * step_scan: per worker, where each step's nonzeros start in schedule
+//    order (its region in the per-nonzero plan arrays);
+//  * csr_plan: per (worker, step), the distinct cold columns (slots 0..Uc-1,
+//    in `clist`), the distinct hot slots (`hlist`), and for every nonzero
+//    its "code" for this round: -(hot slot + 2) or its cold slot;
+//  * csr_link: per (worker, step), the slot each cold column had in the
+//    previous step, or -1.
+//
+// The pass (sgd_csr_fast_kernel) then keeps the step's cold values in LDS
+// slots: they are gathered from the model a step ahead, and a value the
+// previous step changed is taken from that step's slot through the link.
+// Margins read LDS, gradients are added to slot accumulators with integer
+// atomics (no hashing, no CAS), and the update walks the step's slot lists.
+//
+// If any step has more distinct cold columns than the LDS slots, more hot
+// slots than the list registers, or a hash table overflowed, the plan raises
+// a flag: the fast kernel then does nothing and the general kernel runs.
+#include <cmath>
+
+#include "asap_launch.h"
+#include "csr_device.h"
+
+namespace asap {
+namespace {
+
+using namespace csr;
+
+constexpr int kCMax = 2048;                  // cold slots per step held in LDS
+constexpr int kHList = 4096;                 // hot slots per step applied from registers
+constexpr int kColdPer = kCMax / kThreads;   // 2
+constexpr int kHotPer = kHList / kThreads;   // 4
+constexpr int kHotWords = (kHotMax + 31) / 32;
+
+constexpr int kPlanThreads = 512;
+constexpr int kPlanWaves = kPlanThreads / 64;
+constexpr int kLinkBits = 12;
+constexpr int kLinkTab = 1 << kLinkBits;     // link hash positions (>= 2 kCMax)
+
+__device__ __forceinline__ uint32_t mult_hash(int c, int bits) {
+  return (uint32_t(c) * 2654435761u) >> (32 - bits);
+}
+
+// Open-addressed tables of 2^bits ints (linear probing).  Insert returns
+// the key's position, or -1 when the table is full.
+__device__ __forceinline__ int table_insert(int* keys, int bits, int c) {
+  const uint32_t mask = (1u << bits) - 1;
+  uint32_t h = mult_hash(c, bits);
+  for (uint32_t n = 0; n <= mask; ++n) {
+    const int old = atomicCAS(&keys[h], -1, c);
+    if (old == -1 || old == c) return int(h);
+    h = (h + 1) & mask;
+  }
+  return -1;
+}
+
+__device__ __forceinline__ int table_find(const int* keys, int bits, int c) {
+  const uint32_t mask = (1u << bits) - 1;
+  uint32_t h = mult_hash(c, bits);
+  for (uint32_t n = 0; n <= mask; ++n) {
+    const int k = keys[h];
+    if (k == c) return int(h);
+    if (k == -1) return -1;
+    h = (h + 1) & mask;
+  }
+  return -1;
+}
+
+// exclusive prefix sum over the threads of a plan block (wave scans, then
+// the wave totals); *total gets the sum
+__device__ __forceinline__ int block_scan(int v, int* sc, int* total) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sc[wave] = x;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kPlanWaves; ++w) {
+    base += w < wave ? sc[w] : 0;
+    tot += sc[w];
+  }
+  *total = tot;
+  __syncthreads();  // sc is reused by the next scan
+  return base + x - v;
+}
+
+// ----------------------------------------------------------------------------
+// step offsets: step_off[i][k] = nonzeros of worker i's steps before k, in
+// schedule order (stride S + 1 per worker); one 1024-thread block per worker
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void step_scan_kernel(PlanArgs p) {
+  __shared__ int sc[1024];
+  __shared__ int carry;
+  const int i = blockIdx.x, t = threadIdx.x;
+  const int64_t S = p.S;
+  const int B = p.batch, K = p.K;
+  const RowInfo* ri = p.rowinfo + int64_t(i) * S;
+  int32_t* so = p.step_off + int64_t(i) * (S + 1);
+  if (t == 0) carry = 0;
+  __syncthreads();
+  for (int base = 0; base < K; base += 1024) {
+    const int k = base + t;
+    int tot = 0;
+    if (k < K) {
+      const int64_t b0 = int64_t(k) * B;
+      const int Bp = int(min<int64_t>(B, S - b0));
+      for (int b = 0; b < Bp; ++b) tot += ri[b0 + b].len;
+    }
+    sc[t] = tot;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int add = t >= o ? sc[t - o] : 0;
+      __syncthreads();
+      sc[t] += add;
+      __syncthreads();
+    }
+    if (k < K) so[k] = carry + sc[t] - tot;
+    __syncthreads();
+    if (t == 0) carry += sc[1023];
+    __syncthreads();
+  }
+  if (t == 0) so[K] = carry;
+}
+
+// ----------------------------------------------------------------------------
+// plan of one (worker, step): distinct columns, slots, per-nonzero codes
+// ----------------------------------------------------------------------------
+template <int TB>  // table positions: 2^TB >= 2 * (the step's nonzeros), LDS sized to match
+__global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
+  __shared__ int keys[1 << TB];
+  __shared__ uint16_t ids[1 << TB];  // slots < 2^TB <= 2^13
+  __shared__ uint32_t hot[kHotWords];
+  __shared__ int sc[kPlanWaves];
+  __shared__ long long rstart[kFastRows];
+  __shared__ int rlen[kFastRows];
+  __shared__ int overflow;
+  constexpr int kRowsPerWave = kFastRows / kPlanWaves;  // 8
+  const int K = p.K, B = p.batch;
+  const int i = int(blockIdx.x) / K, k = int(blockIdx.x) % K;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int64_t S = p.S;
+  const int64_t seg = p.row_ptr[int64_t(i) * S];
+  const int64_t b0 = int64_t(k) * B;
+  const int Bp = int(min<int64_t>(B, S - b0));  // <= kFastRows
+  const int32_t* so = p.step_off + int64_t(i) * (S + 1);
+  const int64_t lbase = seg + so[k];
+  // a table of at least twice the step's nonzeros (at most 2^TB)
+  const int T = so[k + 1] - so[k];
+  int bits = 8;
+  while (bits < TB && (1 << bits) < 2 * T) ++bits;
+  const int tab = 1 << bits;
+  if (t < Bp) {
+    const RowInfo r = p.rowinfo[int64_t(i) * S + b0 + t];
+    rstart[t] = r.start;
+    rlen[t] = r.len;
+  }
+  for (int q = t; q < tab; q += kPlanThreads) keys[q] = -1;
+  for (int q = t; q < kHotWords; q += kPlanThreads) hot[q] = 0u;
+  if (t == 0) overflow = 0;
+  __syncthreads();
+  // every code of the step in registers (rows of at most 128 nonzeros: two
+  // per lane), all loads issued before any is used; -1 marks no entry
+  int cc[kRowsPerWave][2];
+#pragma unroll
+  for (int j = 0; j < kRowsPerWave; ++j) {
+    const int b = wave + j * kPlanWaves;
+    const int len = b < Bp ? rlen[b] : 0;
+    const long long st = b < Bp ? rstart[b] : 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int e = lane + 64 * h;
+      cc[j][h] = e < len ? p.code[st + e] : -1;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kRowsPerWave; ++j)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = cc[j][h];
+      if (c == -1) continue;
+      if (is_hot(c)) {
+        const int hs = hot_slot(c);
+        atomicOr(&hot[hs >> 5], 1u << (hs & 31));
+      } else if (table_insert(keys, bits, c) < 0) {
+        overflow = 1;
+      }
+    }
+  __syncthreads();
+  // cold slots in table order: thread t numbers a contiguous run of positions
+  const int per = tab / kPlanThreads > 0 ? tab / kPlanThreads : 1;
+  const int q0 = t * per, q1 = min(q0 + per, tab);
+  int cnt = 0;
+  for (int q = q0; q < q1; ++q) cnt += keys[q] >= 0;
+  int Uc = 0;
+  int id = block_scan(cnt, sc, &Uc);
+  for (int q = q0; q < q1; ++q) {
+    const int key = keys[q];
+    if (key >= 0) {
+      ids[q] = uint16_t(id);
+      p.clist[lbase + id] = key;
+      ++id;
+    }
+  }
+  // hot slots in slot order
+  const uint32_t word = t < kHotWords ? hot[t] : 0u;
+  int Uh = 0;
+  int hid = block_scan(__popc(word), sc, &Uh);
+  for (uint32_t w = word; w; w &= w - 1) p.hlist[lbase + hid++] = t * 32 + __ffs(w) - 1;
+  __syncthreads();  // ids complete
+#pragma unroll
+  for (int j = 0; j < kRowsPerWave; ++j) {
+    const int b = wave + j * kPlanWaves;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = cc[j][h];
+      if (c == -1) continue;
+      int out = c;
+      if (!is_hot(c)) {
+        const int pos = table_find(keys, bits, c);
+        out = pos >= 0 ? int(ids[pos]) : 0;
+      }
+      p.code_r[rstart[b] + lane + 64 * h] = out;
+    }
+  }
+  if (t == 0) {
+    p.cnt[(int64_t(i) * K + k) * 2 + 0] = Uc;
+    p.cnt[(int64_t(i) * K + k) * 2 + 1] = Uh;
+    if (overflow || Uc > kCMax || Uh > kHList) atomicOr(p.flag, 1);
+  }
+}
+
+// ----------------------------------------------------------------------------
+// links: slot of each cold column of step k in step k-1, or -1
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(kPlanThreads) void csr_link_kernel(PlanArgs p) {
+  __shared__ int keys[kLinkTab];
+  __shared__ int vals[kLinkTab];
+  const int K = p.K;
+  const int i = int(blockIdx.x) / K, k = int(blockIdx.x) % K;
+  const int t = threadIdx.x;
+  const int64_t S = p.S;
+  const int64_t seg = p.row_ptr[int64_t(i) * S];
+  const int32_t* so = p.step_off + int64_t(i) * (S + 1);
+  const int Uc = min(p.cnt[(int64_t(i) * K + k) * 2], kCMax);
+  const int64_t lbase = seg + so[k];
+  const int Up = k > 0 ? min(p.cnt[(int64_t(i) * K + k - 1) * 2], kCMax) : 0;
+  for (int q = t; q < kLinkTab; q += kPlanThreads) keys[q] = -1;
+  __syncthreads();
+  if (k > 0) {
+    const int64_t pbase = seg + so[k - 1];
+    for (int u = t; u < Up; u += kPlanThreads) {
+      const int pos = table_insert(keys, kLinkBits, p.clist[pbase + u]);
+      if (pos >= 0) vals[pos] = u;  // columns are distinct within a step
+    }
+  }
+  __syncthreads();
+  for (int u = t; u < Uc; u += kPlanThreads) {
+    const int pos = k > 0 ? table_find(keys, kLinkBits, p.clist[lbase + u]) : -1;
+    p.clink[lbase + u] = pos >= 0 ? vals[pos] : -1;
+  }
+}
+
+// ----------------------------------------------------------------------------
+// the pass on the plan
+// ----------------------------------------------------------------------------
+struct FastShared {
+  float vhot[kHotMax];
+  unsigned long long acch[kHotMax];
+  float cval[2][kCMax];  // cold values of steps k (slot k & 1) and k - 1
+  unsigned long long cacc[kCMax];
+};
+static_assert(sizeof(FastShared) <= 160 * 1024, "LDS budget of one workgroup");
+
+// per-step constants: region start (within the worker), cold and hot counts
+struct Meta {
+  int soff, uc, uh;
+};
+
+__device__ __forceinline__ Meta load_meta(const PlanArgs& p, int i, int64_t k, int64_t K) {
+  Meta m{0, 0, 0};
+  if (k < K) {
+    m.soff = p.step_off[int64_t(i) * (p.S + 1) + k];
+    m.uc = p.cnt[(int64_t(i) * K + k) * 2];
+    m.uh = p.cnt[(int64_t(i) * K + k) * 2 + 1];
+  }
+  return m;
+}
+
+template <int E>
+__global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanArgs p) {
+  if (*p.flag) return;  // the general kernel takes this round
+  __shared__ FastShared sh;
+  const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane & (kRowLanes - 1);
+  const int brow = wave * (64 / kRowLanes) + (lane / kRowLanes);
+  float* vrow = a.models + int64_t(i) * a.ld;
+  const RowInfo* ri = a.rowinfo + int64_t(i) * a.S;
+  const int H = a.n_hot;
+  const int64_t K = (a.S + a.batch - 1) / a.batch;
+  Views w;
+  w.seg = a.row_ptr[int64_t(i) * a.S];
+  const uint32_t nnz_w = uint32_t(a.row_ptr[int64_t(i + 1) * a.S] - w.seg);
+  w.code = rsrc(p.code_r + w.seg, nnz_w * 4u);
+  w.val = rsrc(a.val + w.seg, nnz_w * 4u);
+  w.model = rsrc(vrow, uint32_t(a.dim) * 4u);
+  const auto clist = rsrc(p.clist + w.seg, nnz_w * 4u);
+  const auto clink = rsrc(p.clink + w.seg, nnz_w * 4u);
+  const auto hlist = rsrc(p.hlist + w.seg, nnz_w * 4u);
+
+  for (int h = tid; h < H; h += kThreads) {
+    sh.vhot[h] = vrow[a.hot_cols[h]];
+    sh.acch[h] = 0ull;
+  }
+  for (int q = tid; q < kCMax; q += kThreads) sh.cacc[q] = 0ull;
+  // fixed point as in the general kernel: |column sum| <= B vmax < 2^e
+  int e2 = 0;
+  frexp(double(a.batch) * double(a.vmax[i]), &e2);
+  const double to_fx = ldexp(1.0, 61 - e2), from_fx = ldexp(1.0, e2 - 61);
+  double s = 1.0;  // w = s * v
+
+  // Pipeline at the top of step k: d0 = nonzeros of step k, r1 = row of
+  // step k+1; m0..m2 = constants of steps k..k+2; cl0/lk0/g0 = cold columns,
+  // links and gathered values of step k, cl1 = cold columns of step k+1.
+  // Step k loads d1, r2, m3, g1 (from cl1), cl2, lk1 and its own hot slots
+  // hl0 (needed only at its update), rotated in after the end-of-step fence.
+  RowInfo r1, r2;
+  DataReg<E> d0, d1;
+  Meta m0, m1, m2, m3;
+  int cl0[kColdPer], lk0[kColdPer], cl1[kColdPer], lk1[kColdPer], cl2[kColdPer];
+  float g0[kColdPer], g1[kColdPer];
+  int hl0[kHotPer];
+  auto load_cols = [&](const Meta& m, int (&cl)[kColdPer]) {
+#pragma unroll
+    for (int j = 0; j < kColdPer; ++j) {
+      const int u = tid + j * kThreads;
+      cl[j] = ld_i32(clist, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
+    }
+  };
+  auto load_links = [&](const Meta& m, int (&lk)[kColdPer]) {
+#pragma unroll
+    for (int j = 0; j < kColdPer; ++j) {
+      const int u = tid + j * kThreads;
+      lk[j] = ld_i32(clink, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
+    }
+  };
+  auto load_hot = [&](const Meta& m, int (&hl)[kHotPer]) {
+#pragma unroll
+    for (int j = 0; j < kHotPer; ++j) {
+      const int u = tid + j * kThreads;
+      hl[j] = ld_i32(hlist, uint32_t(m.soff + (u < m.uh ? u : 0)) * 4u);
+    }
+  };
+  auto gather = [&](const Meta& m, const int (&cl)[kColdPer], float (&g)[kColdPer]) {
+#pragma unroll
+    for (int j = 0; j < kColdPer; ++j) {
+      const int u = tid + j * kThreads;
+      g[j] = ld_f32(w.model, uint32_t(u < m.uc ? cl[j] : 0) * 4u);
+    }
+  };
+  {
+    const RowInfo ra = load_row(a, ri, 0, K, brow);
+    r1 = load_row(a, ri, 1, K, brow);
+    m0 = load_meta(p, i, 0, K);
+    m1 = load_meta(p, i, 1, K);
+    m2 = load_meta(p, i, 2, K);
+    __syncthreads();
+    load_data<E>(w, ra, row_valid(a, 0, K, brow), sub, d0);
+    load_cols(m0, cl0);
+    load_links(m0, lk0);
+    load_cols(m1, cl1);
+    __syncthreads();
+    gather(m0, cl0, g0);
+  }
+  __syncthreads();
+
+  for (int64_t k = 0; k < K; ++k) {
+    if (k > 0) {  // rotate what the previous step loaded
+      d0 = d1;
+      r1 = r2;
+      m0 = m1;
+      m1 = m2;
+      m2 = m3;
+#pragma unroll
+      for (int j = 0; j < kColdPer; ++j) {
+        cl0[j] = cl1[j];
+        lk0[j] = lk1[j];
+        g0[j] = g1[j];
+        cl1[j] = cl2[j];
+      }
+    }
+    const int64_t b0 = k * a.batch;
+    const int Bp = int(min(int64_t(a.batch), a.S - b0));
+    const double eta = step_size(a.lr_kind, a.lr0, a.round * K + k + 1);
+    const double s_new = s * (1.0 - eta * double(a.l2));
+    const double coefA = eta / (double(Bp) * s_new);
+    float* cv = sh.cval[k & 1];
+    const float* cvp = sh.cval[(k + 1) & 1];
+
+    // cold values of this step: changed by the previous step -> its slot,
+    // else the value gathered a step ago
+#pragma unroll
+    for (int j = 0; j < kColdPer; ++j) {
+      const int u = tid + j * kThreads;
+      if (u < m0.uc) cv[u] = (k > 0 && lk0[j] >= 0) ? cvp[lk0[j]] : g0[j];
+    }
+    // prefetch: nonzeros, links and values of k+1, row and columns of k+2
+    load_data<E>(w, r1, row_valid(a, k + 1, K, brow), sub, d1);
+    r2 = load_row(a, ri, k + 2, K, brow);
+    m3 = load_meta(p, i, k + 3, K);
+    gather(m1, cl1, g1);
+    load_links(m1, lk1);
+    load_cols(m2, cl2);
+    load_hot(m0, hl0);
+    lds_barrier();
+
+    double part = 0.0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int code = code_at(d0, j);
+      float v = 0.f;
+      if (is_hot(code))
+        v = sh.vhot[hot_slot(code)];
+      else if (code >= 0)
+        v = cv[code];
+      part = fma(double(d0.val[j]), double(v), part);
+    }
+    const double dot = row16_sum(part);
+    const double cf = (d0.ok & kRowExists) ? loss_coef(s * dot, double(d0.y), a.loss) : 0.0;
+    if (cf != 0.0) {
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const int code = code_at(d0, j);
+        if (code == -1) continue;
+        const long long q = llrint(cf * double(d0.val[j]) * to_fx);
+        if (is_hot(code))
+          atomicAdd(&sh.acch[hot_slot(code)], static_cast<unsigned long long>(q));
+        else
+          atomicAdd(&sh.cacc[code], static_cast<unsigned long long>(q));
+      }
+    }
+    lds_barrier();
+
+#pragma unroll
+    for (int j = 0; j < kHotPer; ++j) {
+      const int u = tid + j * kThreads;
+      if (u < m0.uh) {
+        const int h = hl0[j];
+        const unsigned long long acc = sh.acch[h];
+        if (acc != 0ull) {
+          sh.vhot[h] = float(double(sh.vhot[h]) - coefA * double(static_cast<long long>(acc)) * from_fx);
+          sh.acch[h] = 0ull;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kColdPer; ++j) {
+      const int u = tid + j * kThreads;
+      if (u < m0.uc) {
+        const unsigned long long acc = sh.cacc[u];
+        if (acc != 0ull) {
+          const float nv = float(double(cv[u]) - coefA * double(static_cast<long long>(acc)) * from_fx);
+          cv[u] = nv;
+          sh.cacc[u] = 0ull;
+          st_f32(w.model, uint32_t(cl0[j]) * 4u, nv);
+        }
+      }
+    }
+
+    s = s_new;
+    if (s < 1e-6) {  // fold the scale back into v before it underflows
+      const float sf = float(s);
+      __syncthreads();
+      for (int h = tid; h < H; h += kThreads) sh.vhot[h] *= sf;
+      for (int64_t c = tid; c < a.dim; c += kThreads) vrow[c] *= sf;
+#pragma unroll
+      for (int j = 0; j < kColdPer; ++j) {
+        const int u = tid + j * kThreads;
+        if (u < m0.uc) cv[u] *= sf;  // the next step links to these
+        g1[j] *= sf;                 // gathered before the fold
+      }
+      s = 1.0;
+    }
+    __syncthreads();  // full fence: model stores complete, LDS updates visible
+  }
+
+  for (int h = tid; h < H; h += kThreads) vrow[a.hot_cols[h]] = sh.vhot[h];
+  if (tid == 0) {
+    a.scale[i] = float(s);
+    a.tag[i] = a.tag_value;
+  }
+}
+
+template <int E>
+hipError_t launch_fast_e(const SgdArgs& a, const PlanArgs& p, hipStream_t s) {
+  hipLaunchKernelGGL((sgd_csr_fast_kernel<E>), dim3(uint32_t(a.n)), dim3(kThreads), 0, s, a, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool csr_plan_fits(const SgdArgs& a) {
+  return a.batch <= kFastRows && a.max_row <= kRowLanes * 8 && a.n_hot <= kHotMax;
+}
+
+hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
+  const uint32_t blocks = uint32_t(int64_t(p.n) * p.K);
+  hipLaunchKernelGGL(step_scan_kernel, dim3(uint32_t(p.n)), dim3(1024), 0, s, p);
+  // the largest step holds at most batch * max_row nonzeros
+  const int64_t most = 2 * int64_t(std::min(p.batch, kFastRows)) * max_row;
+  if (most <= (1 << 10))
+    hipLaunchKernelGGL(csr_plan_kernel<10>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  else if (most <= (1 << 11))
+    hipLaunchKernelGGL(csr_plan_kernel<11>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  else if (most <= (1 << 12))
+    hipLaunchKernelGGL(csr_plan_kernel<12>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL(csr_plan_kernel<13>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  hipLaunchKernelGGL(csr_link_kernel, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd_csr_fast(const SgdArgs& a, const PlanArgs& p, hipStream_t s) {
+  if (a.max_row <= kRowLanes * 2) return launch_fast_e<2>(a, p, s);
+  if (a.max_row <= kRowLanes * 3) return launch_fast_e<3>(a, p, s);
+  if (a.max_row <= kRowLanes * 4) return launch_fast_e<4>(a, p, s);
+  if (a.max_row <= kRowLanes * 6) return launch_fast_e<6>(a, p, s);
+  return launch_fast_e<8>(a, p, s);
+}
+
+}  // namespace asap

@@ -227,6 +227,14 @@ def test_csr_hinge_complete_graph(torch):
     _free_run(torch, wl, "complete", 0, 3, loss_curve=True)
 
 
+def test_csr_many_distinct_cold_columns_fall_back(torch):
+    # 64 rows of ~110 nearly uniform columns of 2^20: a step holds more
+    # distinct rarely used columns than the planned pass keeps on chip, so
+    # the round runs on the general kernel
+    wl = synth.SPARSE_LR_64W.with_(n_workers=4, samples=256, nnz_mean=110.0, zipf_s=0.3)
+    _free_run(torch, wl, "ring", 2, 2, loss_curve=True)
+
+
 def test_csr_long_rows_and_large_batch_general_path(torch):
     # rows of ~200 nonzeros (> 128) and minibatches of 100 and 300 rows (> 64):
     # every step goes through the chunked general path
