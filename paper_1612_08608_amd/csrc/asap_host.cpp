@@ -132,7 +132,7 @@ void layout(asap_ctx* c) {
   // per-round plan of the CSR pass: one entry per nonzero per list
   const size_t nz = csr ? size_t(c->nnz) : 0, nS = csr ? n * size_t(c->S) : 0;
   c->off_soff = o;    o = align_up(o + (csr ? n * (size_t(c->S) + 1) * 4 : 0));
-  c->off_coder = o;   o = align_up(o + nz * 4);
+  c->off_coder = o;   o = align_up(o + nz * 8);
   c->off_clist = o;   o = align_up(o + nz * 4);
   c->off_clink = o;   o = align_up(o + nz * 4);
   c->off_hlist = o;   o = align_up(o + nz * 4);
@@ -637,7 +637,8 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
     pa.batch = p->batch;
     pa.K = int32_t((c->S + p->batch - 1) / p->batch);
     pa.step_off = at<int32_t>(c, c->off_soff);
-    pa.code_r = at<int32_t>(c, c->off_coder);
+    pa.val = c->val;
+    pa.pack = at<int2>(c, c->off_coder);
     pa.clist = at<int32_t>(c, c->off_clist);
     pa.clink = at<int32_t>(c, c->off_clink);
     pa.hlist = at<int32_t>(c, c->off_hlist);

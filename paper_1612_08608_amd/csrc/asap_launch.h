@@ -91,7 +91,8 @@ struct PlanArgs {
   int32_t batch;
   int32_t K;                // steps per pass
   int32_t* step_off;        // [n][S+1]
-  int32_t* code_r;          // [nnz] this round: -(hot slot + 2) or cold slot
+  const float* val;         // [nnz] values
+  int2* pack;               // [nnz] this round: (-(hot slot + 2) or cold slot, value bits)
   int32_t* clist;           // [nnz] cold columns of each step, by slot
   int32_t* clink;           // [nnz] slot of the same column in the previous step, or -1
   int32_t* hlist;           // [nnz] distinct hot slots of each step

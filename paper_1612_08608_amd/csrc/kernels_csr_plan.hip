@@ -13,7 +13,8 @@
 //    order (its region in the per-nonzero plan arrays);
 //  * csr_plan: per (worker, step), the distinct cold columns (slots 0..Uc-1,
 //    in `clist`), the distinct hot slots (`hlist`), and for every nonzero
-//    its "code" for this round: -(hot slot + 2) or its cold slot;
+//    its "code" for this round, -(hot slot + 2) or its cold slot, packed
+//    with its value so that the pass loads both at once;
 //  * csr_link: per (worker, step), the slot each cold column had in the
 //    previous step, or -1.
 //
@@ -176,6 +177,7 @@ __global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
   // every code of the step in registers (rows of at most 128 nonzeros: two
   // per lane), all loads issued before any is used; -1 marks no entry
   int cc[kRowsPerWave][2];
+  float vv[kRowsPerWave][2];
 #pragma unroll
   for (int j = 0; j < kRowsPerWave; ++j) {
     const int b = wave + j * kPlanWaves;
@@ -185,6 +187,7 @@ __global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
     for (int h = 0; h < 2; ++h) {
       const int e = lane + 64 * h;
       cc[j][h] = e < len ? p.code[st + e] : -1;
+      vv[j][h] = e < len ? p.val[st + e] : 0.f;
     }
   }
 #pragma unroll
@@ -234,7 +237,7 @@ __global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
         const int pos = table_find(keys, bits, c);
         out = pos >= 0 ? int(ids[pos]) : 0;
       }
-      p.code_r[rstart[b] + lane + 64 * h] = out;
+      p.pack[rstart[b] + lane + 64 * h] = make_int2(out, __float_as_int(vv[j][h]));
     }
   }
   if (t == 0) {
@@ -291,14 +294,49 @@ struct Meta {
   int soff, uc, uh;
 };
 
-__device__ __forceinline__ Meta load_meta(const PlanArgs& p, int i, int64_t k, int64_t K) {
-  Meta m{0, 0, 0};
-  if (k < K) {
-    m.soff = p.step_off[int64_t(i) * (p.S + 1) + k];
-    m.uc = p.cnt[(int64_t(i) * K + k) * 2];
-    m.uh = p.cnt[(int64_t(i) * K + k) * 2 + 1];
-  }
+// Loaded with vector (buffer) loads: a scalar load would be waited for by
+// the next LDS wait (both count in lgkmcnt).  Offsets past the end read 0.
+__device__ __forceinline__ Meta load_meta(__amdgpu_buffer_rsrc_t so, __amdgpu_buffer_rsrc_t cn, int64_t k) {
+  Meta m;
+  m.soff = ld_i32(so, uint32_t(k) * 4u);
+  m.uc = ld_i32(cn, uint32_t(k) * 8u);
+  m.uh = ld_i32(cn, uint32_t(k) * 8u + 4u);
   return m;
+}
+
+__device__ __forceinline__ Meta uniform(const Meta& m) {
+  return Meta{__builtin_amdgcn_readfirstlane(m.soff), __builtin_amdgcn_readfirstlane(m.uc),
+              __builtin_amdgcn_readfirstlane(m.uh)};
+}
+
+// One lane's share of a fast-path row from the packed (code, value) plan:
+// entries sub, sub+16, ...; an entry that no row of the wave reaches is not
+// loaded at all (wmax = longest row of the wave).
+template <int E>
+__device__ __forceinline__ void load_packed(__amdgpu_buffer_rsrc_t pk, long long seg, const RowInfo& r, bool valid,
+                                            int sub, DataReg<E>& d) {
+  const int len = valid ? r.len : 0;
+  int wmax = max(max(__builtin_amdgcn_readlane(len, 0), __builtin_amdgcn_readlane(len, 16)),
+                 max(__builtin_amdgcn_readlane(len, 32), __builtin_amdgcn_readlane(len, 48)));
+  const uint32_t st = uint32_t(r.start - seg);
+  d.ok = len > 0 ? kRowExists : 0u;
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const int e = sub + kRowLanes * j;
+    d.code[j] = -1;
+    d.val[j] = 0.f;
+    if (kRowLanes * j < wmax) {
+      const uint32_t q = e < len ? st + uint32_t(e) : 0u;
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(pk, q * 8u, 0, 0);
+      // element values are copied out before any reinterpretation: a
+      // __builtin_bit_cast of a vector element reads element 0's bytes
+      const unsigned int c0 = v[0], v1 = v[1];
+      d.code[j] = int(c0);
+      d.val[j] = __uint_as_float(v1);
+    }
+    d.ok |= uint32_t(e < len) << j;
+  }
+  d.y = r.y;
 }
 
 template <int E>
@@ -315,12 +353,13 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   Views w;
   w.seg = a.row_ptr[int64_t(i) * a.S];
   const uint32_t nnz_w = uint32_t(a.row_ptr[int64_t(i + 1) * a.S] - w.seg);
-  w.code = rsrc(p.code_r + w.seg, nnz_w * 4u);
-  w.val = rsrc(a.val + w.seg, nnz_w * 4u);
+  const auto pk = rsrc(p.pack + w.seg, nnz_w * 8u);
   w.model = rsrc(vrow, uint32_t(a.dim) * 4u);
   const auto clist = rsrc(p.clist + w.seg, nnz_w * 4u);
   const auto clink = rsrc(p.clink + w.seg, nnz_w * 4u);
   const auto hlist = rsrc(p.hlist + w.seg, nnz_w * 4u);
+  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(K) * 4u);  // steps >= K read 0
+  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(K) * 8u);
 
   for (int h = tid; h < H; h += kThreads) {
     sh.vhot[h] = vrow[a.hot_cols[h]];
@@ -344,42 +383,51 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   int cl0[kColdPer], lk0[kColdPer], cl1[kColdPer], lk1[kColdPer], cl2[kColdPer];
   float g0[kColdPer], g1[kColdPer];
   int hl0[kHotPer];
+  // list loads: a wave whose first slot is past the count issues nothing
+  const int wave0 = wave * 64;
   auto load_cols = [&](const Meta& m, int (&cl)[kColdPer]) {
 #pragma unroll
     for (int j = 0; j < kColdPer; ++j) {
       const int u = tid + j * kThreads;
-      cl[j] = ld_i32(clist, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
+      cl[j] = 0;
+      if (wave0 + j * kThreads < m.uc) cl[j] = ld_i32(clist, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
     }
   };
   auto load_links = [&](const Meta& m, int (&lk)[kColdPer]) {
 #pragma unroll
     for (int j = 0; j < kColdPer; ++j) {
       const int u = tid + j * kThreads;
-      lk[j] = ld_i32(clink, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
+      lk[j] = -1;
+      if (wave0 + j * kThreads < m.uc) lk[j] = ld_i32(clink, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
     }
   };
   auto load_hot = [&](const Meta& m, int (&hl)[kHotPer]) {
 #pragma unroll
     for (int j = 0; j < kHotPer; ++j) {
       const int u = tid + j * kThreads;
-      hl[j] = ld_i32(hlist, uint32_t(m.soff + (u < m.uh ? u : 0)) * 4u);
+      hl[j] = 0;
+      if (wave0 + j * kThreads < m.uh) hl[j] = ld_i32(hlist, uint32_t(m.soff + (u < m.uh ? u : 0)) * 4u);
     }
   };
   auto gather = [&](const Meta& m, const int (&cl)[kColdPer], float (&g)[kColdPer]) {
 #pragma unroll
     for (int j = 0; j < kColdPer; ++j) {
       const int u = tid + j * kThreads;
-      g[j] = ld_f32(w.model, uint32_t(u < m.uc ? cl[j] : 0) * 4u);
+      g[j] = 0.f;
+      if (wave0 + j * kThreads < m.uc) g[j] = ld_f32(w.model, uint32_t(u < m.uc ? cl[j] : 0) * 4u);
     }
   };
   {
     const RowInfo ra = load_row(a, ri, 0, K, brow);
     r1 = load_row(a, ri, 1, K, brow);
-    m0 = load_meta(p, i, 0, K);
-    m1 = load_meta(p, i, 1, K);
-    m2 = load_meta(p, i, 2, K);
+    m0 = load_meta(so_v, cn_v, 0);
+    m1 = load_meta(so_v, cn_v, 1);
+    m2 = load_meta(so_v, cn_v, 2);
+    m0 = uniform(m0);
+    m1 = uniform(m1);
+    m2 = uniform(m2);
     __syncthreads();
-    load_data<E>(w, ra, row_valid(a, 0, K, brow), sub, d0);
+    load_packed<E>(pk, w.seg, ra, row_valid(a, 0, K, brow), sub, d0);
     load_cols(m0, cl0);
     load_links(m0, lk0);
     load_cols(m1, cl1);
@@ -394,7 +442,7 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
       r1 = r2;
       m0 = m1;
       m1 = m2;
-      m2 = m3;
+      m2 = uniform(m3);  // loaded by the previous step, landed at its fence
 #pragma unroll
       for (int j = 0; j < kColdPer; ++j) {
         cl0[j] = cl1[j];
@@ -419,9 +467,9 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
       if (u < m0.uc) cv[u] = (k > 0 && lk0[j] >= 0) ? cvp[lk0[j]] : g0[j];
     }
     // prefetch: nonzeros, links and values of k+1, row and columns of k+2
-    load_data<E>(w, r1, row_valid(a, k + 1, K, brow), sub, d1);
+    load_packed<E>(pk, w.seg, r1, row_valid(a, k + 1, K, brow), sub, d1);
     r2 = load_row(a, ri, k + 2, K, brow);
-    m3 = load_meta(p, i, k + 3, K);
+    m3 = load_meta(so_v, cn_v, k + 3);
     gather(m1, cl1, g1);
     load_links(m1, lk1);
     load_cols(m2, cl2);
