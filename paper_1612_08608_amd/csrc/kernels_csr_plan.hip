@@ -38,9 +38,9 @@ namespace {
 using namespace csr;
 
 constexpr int kCMax = 2048;                  // cold slots per step held in LDS
-constexpr int kHList = 4096;                 // hot slots per step applied from registers
+constexpr int kHList = 2048;                 // hot slots per step applied from registers
 constexpr int kColdPer = kCMax / kThreads;   // 2
-constexpr int kHotPer = kHList / kThreads;   // 4
+constexpr int kHotPer = kHList / kThreads;   // 2
 constexpr int kHotWords = (kHotMax + 31) / 32;
 
 constexpr int kPlanThreads = 512;
@@ -296,11 +296,15 @@ struct Meta {
 
 // Loaded with vector (buffer) loads: a scalar load would be waited for by
 // the next LDS wait (both count in lgkmcnt).  Offsets past the end read 0.
-__device__ __forceinline__ Meta load_meta(__amdgpu_buffer_rsrc_t so, __amdgpu_buffer_rsrc_t cn, int64_t k) {
-  Meta m;
-  m.soff = ld_i32(so, uint32_t(k) * 4u);
-  m.uc = ld_i32(cn, uint32_t(k) * 8u);
-  m.uh = ld_i32(cn, uint32_t(k) * 8u + 4u);
+// Only lane 0 loads (the value is the same for every lane; uniform() reads
+// lane 0 once the loads have landed).
+__device__ __forceinline__ Meta load_meta(__amdgpu_buffer_rsrc_t so, __amdgpu_buffer_rsrc_t cn, int64_t k, int lane) {
+  Meta m{0, 0, 0};
+  if (lane == 0) {
+    m.soff = ld_i32(so, uint32_t(k) * 4u);
+    m.uc = ld_i32(cn, uint32_t(k) * 8u);
+    m.uh = ld_i32(cn, uint32_t(k) * 8u + 4u);
+  }
   return m;
 }
 
@@ -339,6 +343,23 @@ __device__ __forceinline__ void load_packed(__amdgpu_buffer_rsrc_t pk, long long
   d.y = r.y;
 }
 
+// Empty asm that takes every element: the loads that produce them are all
+// issued before it, and their results are waited for once.
+template <int N>
+__device__ __forceinline__ void hold(float (&v)[N]) {
+  static_assert(N >= 1 && N <= 8, "hold: 1..8 values");
+  if constexpr (N == 1) asm volatile("" : "+v"(v[0]));
+  if constexpr (N == 2) asm volatile("" : "+v"(v[0]), "+v"(v[1]));
+  if constexpr (N == 3) asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]));
+  if constexpr (N == 4) asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
+  if constexpr (N == 5) asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]));
+  if constexpr (N == 6) asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]));
+  if constexpr (N == 7)
+    asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]));
+  if constexpr (N == 8)
+    asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7]));
+}
+
 template <int E>
 __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanArgs p) {
   if (*p.flag) return;  // the general kernel takes this round
@@ -373,18 +394,20 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   double s = 1.0;  // w = s * v
 
   // Pipeline at the top of step k: d0 = nonzeros of step k, r1 = row of
-  // step k+1; m0..m2 = constants of steps k..k+2; cl0/lk0/g0 = cold columns,
-  // links and gathered values of step k, cl1 = cold columns of step k+1.
-  // Step k loads d1, r2, m3, g1 (from cl1), cl2, lk1 and its own hot slots
-  // hl0 (needed only at its update), rotated in after the end-of-step fence.
+  // step k+1; m0..m2 = constants of steps k..k+2; cl0/lk0/g0/hl0 = cold
+  // columns, links, gathered values and hot slots of step k, cl1 = cold
+  // columns of step k+1.  Step k loads d1, r2, m3, g1 (from cl1), cl2, lk1
+  // and hl1, rotated in after the end-of-step fence.  Nothing a step loads
+  // is used in the same step: vector loads complete in order, so waiting
+  // for any of them would also wait for that step's model gathers.
   RowInfo r1, r2;
   DataReg<E> d0, d1;
   Meta m0, m1, m2, m3;
   int cl0[kColdPer], lk0[kColdPer], cl1[kColdPer], lk1[kColdPer], cl2[kColdPer];
   float g0[kColdPer], g1[kColdPer];
-  int hl0[kHotPer];
+  int hl0[kHotPer], hl1[kHotPer];
   // list loads: a wave whose first slot is past the count issues nothing
-  const int wave0 = wave * 64;
+  const int wave0 = __builtin_amdgcn_readfirstlane(wave * 64);
   auto load_cols = [&](const Meta& m, int (&cl)[kColdPer]) {
 #pragma unroll
     for (int j = 0; j < kColdPer; ++j) {
@@ -420,9 +443,9 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   {
     const RowInfo ra = load_row(a, ri, 0, K, brow);
     r1 = load_row(a, ri, 1, K, brow);
-    m0 = load_meta(so_v, cn_v, 0);
-    m1 = load_meta(so_v, cn_v, 1);
-    m2 = load_meta(so_v, cn_v, 2);
+    m0 = load_meta(so_v, cn_v, 0, lane);
+    m1 = load_meta(so_v, cn_v, 1, lane);
+    m2 = load_meta(so_v, cn_v, 2, lane);
     m0 = uniform(m0);
     m1 = uniform(m1);
     m2 = uniform(m2);
@@ -431,6 +454,7 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
     load_cols(m0, cl0);
     load_links(m0, lk0);
     load_cols(m1, cl1);
+    load_hot(m0, hl0);
     __syncthreads();
     gather(m0, cl0, g0);
   }
@@ -450,6 +474,8 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
         g0[j] = g1[j];
         cl1[j] = cl2[j];
       }
+#pragma unroll
+      for (int j = 0; j < kHotPer; ++j) hl0[j] = hl1[j];
     }
     const int64_t b0 = k * a.batch;
     const int Bp = int(min(int64_t(a.batch), a.S - b0));
@@ -466,27 +492,33 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
       const int u = tid + j * kThreads;
       if (u < m0.uc) cv[u] = (k > 0 && lk0[j] >= 0) ? cvp[lk0[j]] : g0[j];
     }
-    // prefetch: nonzeros, links and values of k+1, row and columns of k+2
+    lds_barrier();
+    // prefetch, issued after the barrier so that the address work of some
+    // waves overlaps the LDS work of others: nonzeros, links, hot slots and
+    // values of k+1, row and columns of k+2
+    load_hot(m1, hl1);
     load_packed<E>(pk, w.seg, r1, row_valid(a, k + 1, K, brow), sub, d1);
     r2 = load_row(a, ri, k + 2, K, brow);
-    m3 = load_meta(so_v, cn_v, k + 3);
+    m3 = load_meta(so_v, cn_v, k + 3, lane);
     gather(m1, cl1, g1);
     load_links(m1, lk1);
     load_cols(m2, cl2);
-    load_hot(m0, hl0);
-    lds_barrier();
+    asm volatile("" ::: "memory");  // keep the prefetch issued here, ahead of the LDS work
 
-    double part = 0.0;
+    // one LDS read per entry, its address chosen by the code (a read per
+    // branch would serialise on the shared destination register); all reads
+    // are issued before the first is used.  An absent entry reads cold slot 0,
+    // which may hold anything, and its value is replaced by zero.
+    float v[E];
 #pragma unroll
     for (int j = 0; j < E; ++j) {
       const int code = code_at(d0, j);
-      float v = 0.f;
-      if (is_hot(code))
-        v = sh.vhot[hot_slot(code)];
-      else if (code >= 0)
-        v = cv[code];
-      part = fma(double(d0.val[j]), double(v), part);
+      v[j] = is_hot(code) ? sh.vhot[hot_slot(code)] : cv[code < 0 ? 0 : code];
     }
+    hold(v);
+    double part = 0.0;
+#pragma unroll
+    for (int j = 0; j < E; ++j) part = fma(double(d0.val[j]), double(code_at(d0, j) == -1 ? 0.f : v[j]), part);
     const double dot = row16_sum(part);
     const double cf = (d0.ok & kRowExists) ? loss_coef(s * dot, double(d0.y), a.loss) : 0.0;
     if (cf != 0.0) {
@@ -495,33 +527,54 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
         const int code = code_at(d0, j);
         if (code == -1) continue;
         const long long q = llrint(cf * double(d0.val[j]) * to_fx);
-        if (is_hot(code))
-          atomicAdd(&sh.acch[hot_slot(code)], static_cast<unsigned long long>(q));
-        else
-          atomicAdd(&sh.cacc[code], static_cast<unsigned long long>(q));
+        unsigned long long* dst = is_hot(code) ? &sh.acch[hot_slot(code)] : &sh.cacc[code];
+        atomicAdd(dst, static_cast<unsigned long long>(q));
       }
     }
     lds_barrier();
 
+    // update: all accumulator and value reads of a thread first, then the
+    // writes (a wave whose first slot is past the count skips a slot)
+    {
+      unsigned long long acc[kHotPer + kColdPer];
+      float old[kHotPer + kColdPer];
 #pragma unroll
-    for (int j = 0; j < kHotPer; ++j) {
-      const int u = tid + j * kThreads;
-      if (u < m0.uh) {
-        const int h = hl0[j];
-        const unsigned long long acc = sh.acch[h];
-        if (acc != 0ull) {
-          sh.vhot[h] = float(double(sh.vhot[h]) - coefA * double(static_cast<long long>(acc)) * from_fx);
+      for (int j = 0; j < kHotPer; ++j) {
+        acc[j] = 0ull;
+        old[j] = 0.f;
+        if (wave0 + j * kThreads < m0.uh) {
+          acc[j] = sh.acch[hl0[j]];
+          old[j] = sh.vhot[hl0[j]];
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kColdPer; ++j) {
+        const int u = tid + j * kThreads;
+        acc[kHotPer + j] = 0ull;
+        old[kHotPer + j] = 0.f;
+        if (wave0 + j * kThreads < m0.uc) {
+          acc[kHotPer + j] = sh.cacc[u];
+          old[kHotPer + j] = cv[u];
+        }
+      }
+      static_assert(kHotPer + kColdPer == 4, "update batch holds four slots");
+      asm volatile("" : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(old[0]), "+v"(old[1]),
+                   "+v"(old[2]), "+v"(old[3]));
+#pragma unroll
+      for (int j = 0; j < kHotPer; ++j) {
+        const int u = tid + j * kThreads;
+        if (u < m0.uh && acc[j] != 0ull) {
+          const int h = hl0[j];
+          sh.vhot[h] = float(double(old[j]) - coefA * double(static_cast<long long>(acc[j])) * from_fx);
           sh.acch[h] = 0ull;
         }
       }
-    }
 #pragma unroll
-    for (int j = 0; j < kColdPer; ++j) {
-      const int u = tid + j * kThreads;
-      if (u < m0.uc) {
-        const unsigned long long acc = sh.cacc[u];
-        if (acc != 0ull) {
-          const float nv = float(double(cv[u]) - coefA * double(static_cast<long long>(acc)) * from_fx);
+      for (int j = 0; j < kColdPer; ++j) {
+        const int u = tid + j * kThreads;
+        if (u < m0.uc && acc[kHotPer + j] != 0ull) {
+          const float nv =
+              float(double(old[kHotPer + j]) - coefA * double(static_cast<long long>(acc[kHotPer + j])) * from_fx);
           cv[u] = nv;
           sh.cacc[u] = 0ull;
           st_f32(w.model, uint32_t(cl0[j]) * 4u, nv);
