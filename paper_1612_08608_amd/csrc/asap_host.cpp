@@ -34,6 +34,13 @@ constexpr int kDenseMaxMembers = 8;
 constexpr int kDenseCus = 256;
 constexpr uint32_t kDenseSpinLimit = 1u << 20;
 
+// Per-round buffers of the CSR pass: the sample schedule, row descriptors
+// and the column plan.  CSR workspaces hold two, so that the next round can
+// be planned while this one runs.
+struct RoundPlan {
+  size_t sched = 0, rowinfo = 0, soff = 0, pack = 0, clist = 0, clink = 0, hlist = 0, cnt = 0, flag = 0;
+};
+
 }  // namespace
 
 struct asap_ctx {
@@ -68,10 +75,9 @@ struct asap_ctx {
 
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
-         off_vmax = 0, off_scan = 0, off_sched = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
-         off_rowinfo = 0, off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dcount = 0,
-         off_soff = 0, off_coder = 0, off_clist = 0, off_clink = 0, off_hlist = 0, off_cnt = 0, off_pflag = 0,
-         total = 0;
+         off_vmax = 0, off_scan = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
+         off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dcount = 0, total = 0;
+  RoundPlan plan[2];
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
   // round state
@@ -80,6 +86,18 @@ struct asap_ctx {
   bool half_done = false;
   bool half_scaled = false;  // the half-step left per-worker L2 scales to fold
   bool tags_ready = false;
+
+  // look-ahead planning of the CSR pass: after launching round r, the plan
+  // of round r + 1 (same seed and batch) is built on a stream of the
+  // library's own into the other RoundPlan; the next call uses it when its
+  // round, seed and batch match
+  hipStream_t ahead = nullptr;
+  hipEvent_t ev_start = nullptr, ev_ready[2] = {nullptr, nullptr}, ev_used[2] = {nullptr, nullptr};
+  bool ahead_valid = false;
+  int ahead_slot = 0;
+  uint64_t ahead_seed = 0;
+  int64_t ahead_round = -1;
+  int32_t ahead_batch = 0;
 
   std::string err;
 };
@@ -120,24 +138,28 @@ void layout(asap_ctx* c) {
   c->off_vmax = o;  o = align_up(o + n * 4);
   c->off_scan = o;  o = align_up(o + 8 * 8);
   c->off_rowok = o; o = align_up(o + n * 4);
-  c->off_sched = o; o = align_up(o + n * size_t(c->S) * 4);
+  c->plan[0].sched = o; o = align_up(o + n * size_t(c->S) * 4);
   c->off_wbar = o;  o = align_up(o + size_t(c->dim) * 8);
   c->off_part = o;  o = align_up(o + (2 * 4096 + 3 * n) * 8);
   c->off_out = o;   o = align_up(o + 8 * 8);
   const bool csr = c->kind == kCsr;
-  c->off_rowinfo = o; o = align_up(o + (csr ? n * size_t(c->S) * sizeof(RowInfo) : 0));
   c->off_code = o;    o = align_up(o + (csr ? size_t(c->nnz) * 4 : 0));
   c->off_lut = o;     o = align_up(o + (csr ? size_t(c->dim) * 2 : 0));
   c->off_hot = o;     o = align_up(o + (csr ? size_t(kHotMax) * 4 : 0));
-  // per-round plan of the CSR pass: one entry per nonzero per list
+  // per-round buffers of the CSR pass, twice: one entry per nonzero per list
   const size_t nz = csr ? size_t(c->nnz) : 0, nS = csr ? n * size_t(c->S) : 0;
-  c->off_soff = o;    o = align_up(o + (csr ? n * (size_t(c->S) + 1) * 4 : 0));
-  c->off_coder = o;   o = align_up(o + nz * 8);
-  c->off_clist = o;   o = align_up(o + nz * 4);
-  c->off_clink = o;   o = align_up(o + nz * 4);
-  c->off_hlist = o;   o = align_up(o + nz * 4);
-  c->off_cnt = o;     o = align_up(o + nS * 2 * 4);
-  c->off_pflag = o;   o = align_up(o + (csr ? 4 : 0));
+  for (int k = 0; k < 2; ++k) {
+    RoundPlan& r = c->plan[k];
+    if (k == 1) { r.sched = o; o = align_up(o + (csr ? nS * 4 : 0)); }
+    r.rowinfo = o; o = align_up(o + nS * sizeof(RowInfo));
+    r.soff = o;    o = align_up(o + (csr ? n * (size_t(c->S) + 1) * 4 : 0));
+    r.pack = o;    o = align_up(o + nz * 8);
+    r.clist = o;   o = align_up(o + nz * 4);
+    r.clink = o;   o = align_up(o + nz * 4);
+    r.hlist = o;   o = align_up(o + nz * 4);
+    r.cnt = o;     o = align_up(o + nS * 2 * 4);
+    r.flag = o;    o = align_up(o + (csr ? 4 : 0));
+  }
   const int cpq = c->kind == kDense ? dense_wide_cpq(c->dim) : 0;
   c->dense_k = cpq ? std::max(1, std::min(kDenseMaxMembers, kDenseCus / std::max(1, c->n))) : 1;
   const size_t ldp = size_t(cpq) * 2048;
@@ -146,7 +168,27 @@ void layout(asap_ctx* c) {
   c->total = o;
 }
 
+// Waits for look-ahead planning still in flight and forgets it.  Every call
+// that may precede a release or rebinding of memory the planning reads or
+// writes comes here first.
+void drain_ahead(asap_ctx* c) {
+  if (c->ahead) (void)hipStreamSynchronize(c->ahead);
+  c->ahead_valid = false;
+}
+
+void release_ahead(asap_ctx* c) {
+  drain_ahead(c);
+  if (c->ahead) (void)hipStreamDestroy(c->ahead);
+  for (hipEvent_t* ev : {&c->ev_start, &c->ev_ready[0], &c->ev_ready[1], &c->ev_used[0], &c->ev_used[1]})
+    if (*ev) {
+      (void)hipEventDestroy(*ev);
+      *ev = nullptr;
+    }
+  c->ahead = nullptr;
+}
+
 void unbind_workspace(asap_ctx* c) {
+  drain_ahead(c);
   c->ws = nullptr;
   c->ws_bytes = 0;
   c->tags_ready = false;
@@ -515,6 +557,7 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
   if (bytes < c->total)
     return fail(c, ASAP_E_INVALID_ARG, "workspace too small: %zu < %zu bytes", bytes, c->total);
   if (!c->buf[0]) return fail(c, ASAP_E_STATE, "bind the models before the workspace");
+  drain_ahead(c);
   hipStream_t s = static_cast<hipStream_t>(stream);
   {
     int dev_id = 0, cus = 0;
@@ -577,19 +620,26 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     c->max_row = int32_t(h[0]);
     asap_status hs = choose_hot_columns(c, s);
     if (hs != ASAP_OK) return hs;
+    if (!c->ahead) {
+      if ((e = hipStreamCreateWithFlags(&c->ahead, hipStreamNonBlocking))) {
+        c->ahead = nullptr;
+        return hip_fail(c, e, "look-ahead stream");
+      }
+      for (hipEvent_t* ev : {&c->ev_start, &c->ev_ready[0], &c->ev_ready[1], &c->ev_used[0], &c->ev_used[1]})
+        if ((e = hipEventCreateWithFlags(ev, hipEventDisableTiming))) {
+          *ev = nullptr;
+          release_ahead(c);
+          return hip_fail(c, e, "look-ahead events");
+        }
+    }
   }
   c->tags_ready = true;
   return ASAP_OK;
 }
 
-extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, void* stream) {
-  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
-  asap_status st = need_device(c);
-  if (st != ASAP_OK) return st;
-  if (c->kind == kNoData) return fail(c, ASAP_E_STATE, "no data bound");
-  if (c->half_done) return fail(c, ASAP_E_STATE, "the half-step of round %lld already ran", (long long)c->round);
-  if ((st = check_params(c, p)) != ASAP_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+namespace {
+
+SgdArgs sgd_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
   SgdArgs a{};
   a.models = c->buf[c->cur];
   a.ld = c->ld;
@@ -603,7 +653,7 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
   a.col = c->col;
   a.val = c->val;
   a.vmax = at<float>(c, c->off_vmax);
-  a.sched = at<int32_t>(c, c->off_sched);
+  a.sched = at<int32_t>(c, rp.sched);
   a.loss = p->loss;
   a.lr_kind = p->lr_kind;
   a.lr0 = p->lr0;
@@ -613,58 +663,119 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
   a.scale = at<float>(c, c->off_scale);
   a.tag = at<int64_t>(c, c->off_tag) + size_t(c->cur) * c->n;
   a.tag_value = tag_half(c->round);
-  a.rowinfo = at<RowInfo>(c, c->off_rowinfo);
+  a.rowinfo = at<RowInfo>(c, rp.rowinfo);
   a.code = at<int32_t>(c, c->off_code);
   a.hot_cols = at<int32_t>(c, c->off_hot);
   a.n_hot = int32_t(c->hot_cols.size());
   a.max_row = c->max_row;
-  hipError_t e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->off_sched), s);
-  if (e != hipSuccess) return hip_fail(c, e, "schedule kernel");
-  if (c->kind == kCsr) {
-    e = launch_rowinfo(a.sched, c->row_ptr, c->y, c->n, c->S, at<RowInfo>(c, c->off_rowinfo), s);
-    if (e != hipSuccess) return hip_fail(c, e, "row descriptor kernel");
-  }
-  if (c->kind == kCsr && csr_plan_fits(a)) {
-    // plan the round's column bookkeeping for all workers and steps, then
-    // run the planned pass; the general kernel runs only if the plan says a
-    // step does not fit
-    PlanArgs pa{};
-    pa.rowinfo = a.rowinfo;
-    pa.code = a.code;
-    pa.row_ptr = c->row_ptr;
-    pa.n = c->n;
-    pa.S = c->S;
-    pa.batch = p->batch;
-    pa.K = int32_t((c->S + p->batch - 1) / p->batch);
-    pa.step_off = at<int32_t>(c, c->off_soff);
-    pa.val = c->val;
-    pa.pack = at<int2>(c, c->off_coder);
-    pa.clist = at<int32_t>(c, c->off_clist);
-    pa.clink = at<int32_t>(c, c->off_clink);
-    pa.hlist = at<int32_t>(c, c->off_hlist);
-    pa.cnt = at<int32_t>(c, c->off_cnt);
-    pa.flag = at<int32_t>(c, c->off_pflag);
-    e = launch_fill_i32(pa.flag, 1, 0, s);
+  return a;
+}
+
+PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
+  PlanArgs pa{};
+  pa.rowinfo = at<RowInfo>(c, rp.rowinfo);
+  pa.code = at<int32_t>(c, c->off_code);
+  pa.row_ptr = c->row_ptr;
+  pa.n = c->n;
+  pa.S = c->S;
+  pa.batch = p->batch;
+  pa.K = int32_t((c->S + p->batch - 1) / p->batch);
+  pa.step_off = at<int32_t>(c, rp.soff);
+  pa.val = c->val;
+  pa.pack = at<int2>(c, rp.pack);
+  pa.clist = at<int32_t>(c, rp.clist);
+  pa.clink = at<int32_t>(c, rp.clink);
+  pa.hlist = at<int32_t>(c, rp.hlist);
+  pa.cnt = at<int32_t>(c, rp.cnt);
+  pa.flag = at<int32_t>(c, rp.flag);
+  return pa;
+}
+
+// Everything a CSR round needs before its SGD pass, on stream s: the sample
+// schedule of (seed, round), the row descriptors and, when the planned pass
+// applies, the column plan of every worker and step.
+hipError_t prepare_csr_round(asap_ctx* c, const asap_sgd_params* p, int64_t round, const RoundPlan& rp, bool planned,
+                             hipStream_t s) {
+  hipError_t e = launch_schedule(p->seed, round, c->n, c->S, at<int32_t>(c, rp.sched), s);
+  if (e == hipSuccess)
+    e = launch_rowinfo(at<int32_t>(c, rp.sched), c->row_ptr, c->y, c->n, c->S, at<RowInfo>(c, rp.rowinfo), s);
+  if (planned) {
+    const PlanArgs pa = plan_args(c, p, rp);
+    if (e == hipSuccess) e = launch_fill_i32(pa.flag, 1, 0, s);
     if (e == hipSuccess) e = launch_csr_plan(pa, c->max_row, s);
-    if (e == hipSuccess) e = launch_sgd_csr_fast(a, pa, s);
-    a.run_if = pa.flag;
-    if (e == hipSuccess) e = launch_sgd_csr(a, s);
-  } else if (c->kind == kDense && dense_wide_cpq(c->dim)) {
-    DenseSync ds{};
-    ds.acc = at<int64_t>(c, c->off_dacc);
-    ds.xmax = at<float>(c, c->off_vmax);
-    ds.count = at<uint32_t>(c, c->off_dcount);
-    ds.ldp = int64_t(dense_wide_cpq(c->dim)) * 2048;
-    ds.K = std::max(1, std::min(c->dense_k, dense_wide_max_members(a, c->n_cu) / c->n));
-    ds.spin_limit = kDenseSpinLimit;
-    ds.err = at<int32_t>(c, c->off_err) + kErrRendezvous;
-    e = launch_fill_i32(reinterpret_cast<int32_t*>(ds.count), c->n, 0, s);
-    if (e == hipSuccess && ds.K > 1) e = launch_fill_i64(ds.acc, 3 * int64_t(c->n) * ds.ldp, 0, s);
-    if (e == hipSuccess) e = launch_sgd_dense_wide(a, ds, s);
-  } else {
-    e = (c->kind == kDense) ? launch_sgd_dense(a, s) : launch_sgd_csr(a, s);
   }
-  if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
+  return e;
+}
+
+}  // namespace
+
+extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  asap_status st = need_device(c);
+  if (st != ASAP_OK) return st;
+  if (c->kind == kNoData) return fail(c, ASAP_E_STATE, "no data bound");
+  if (c->half_done) return fail(c, ASAP_E_STATE, "the half-step of round %lld already ran", (long long)c->round);
+  if ((st = check_params(c, p)) != ASAP_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipSuccess;
+  if (c->kind == kCsr) {
+    // this round's buffers: planned ahead by the previous call when round,
+    // seed and batch match, else prepared here
+    const bool hit = c->ahead_valid && c->ahead_round == c->round && c->ahead_seed == p->seed &&
+                     c->ahead_batch == p->batch;
+    int slot = 0;
+    if (c->ahead_valid) {
+      slot = c->ahead_slot;
+      e = hipStreamWaitEvent(s, c->ev_ready[slot], 0);  // a miss rewrites that slot after it
+    }
+    c->ahead_valid = false;
+    SgdArgs a = sgd_args(c, p, c->plan[slot]);
+    const bool planned = csr_plan_fits(a);
+    if (e == hipSuccess && !hit) e = prepare_csr_round(c, p, c->round, c->plan[slot], planned, s);
+    if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_start, s);
+    if (planned) {
+      const PlanArgs pa = plan_args(c, p, c->plan[slot]);
+      if (e == hipSuccess) e = launch_sgd_csr_fast(a, pa, s);
+      a.run_if = pa.flag;  // the general kernel runs only if the plan says a step does not fit
+    }
+    if (e == hipSuccess) e = launch_sgd_csr(a, s);
+    if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_used[slot], s);
+    if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
+    if (planned && c->ahead) {
+      // plan the next round into the other slot, concurrently with this
+      // pass: after this call's inputs are ready (ev_start) and after the
+      // slot's last reader (ev_used)
+      const int o = slot ^ 1;
+      if ((e = hipStreamWaitEvent(c->ahead, c->ev_start, 0)) || (e = hipStreamWaitEvent(c->ahead, c->ev_used[o], 0)) ||
+          (e = prepare_csr_round(c, p, c->round + 1, c->plan[o], true, c->ahead)) ||
+          (e = hipEventRecord(c->ev_ready[o], c->ahead)))
+        return hip_fail(c, e, "look-ahead planning");
+      c->ahead_valid = true;
+      c->ahead_slot = o;
+      c->ahead_seed = p->seed;
+      c->ahead_round = c->round + 1;
+      c->ahead_batch = p->batch;
+    }
+  } else {
+    SgdArgs a = sgd_args(c, p, c->plan[0]);
+    e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->plan[0].sched), s);
+    if (e == hipSuccess && dense_wide_cpq(c->dim)) {
+      DenseSync ds{};
+      ds.acc = at<int64_t>(c, c->off_dacc);
+      ds.xmax = at<float>(c, c->off_vmax);
+      ds.count = at<uint32_t>(c, c->off_dcount);
+      ds.ldp = int64_t(dense_wide_cpq(c->dim)) * 2048;
+      ds.K = std::max(1, std::min(c->dense_k, dense_wide_max_members(a, c->n_cu) / c->n));
+      ds.spin_limit = kDenseSpinLimit;
+      ds.err = at<int32_t>(c, c->off_err) + kErrRendezvous;
+      e = launch_fill_i32(reinterpret_cast<int32_t*>(ds.count), c->n, 0, s);
+      if (e == hipSuccess && ds.K > 1) e = launch_fill_i64(ds.acc, 3 * int64_t(c->n) * ds.ldp, 0, s);
+      if (e == hipSuccess) e = launch_sgd_dense_wide(a, ds, s);
+    } else if (e == hipSuccess) {
+      e = launch_sgd_dense(a, s);
+    }
+    if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
+  }
   c->half_done = true;
   c->half_scaled = (c->kind == kCsr) && p->l2 > 0.0f;
   return ASAP_OK;
@@ -831,4 +942,8 @@ extern "C" const char* asap_last_error(const asap_ctx* c) {
   return c ? c->err.c_str() : g_free_error.c_str();
 }
 
-extern "C" void asap_destroy(asap_ctx* c) { delete c; }
+extern "C" void asap_destroy(asap_ctx* c) {
+  if (!c) return;
+  release_ahead(c);
+  delete c;
+}

@@ -266,6 +266,33 @@ def test_csr_run_twice_is_bitwise_identical(torch):
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
 
 
+def test_csr_plan_ahead_follows_changing_params(torch):
+    """The next round is planned while one runs; a call whose batch or seed
+    differs from the planned one must not use that plan."""
+    wl = synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 14, samples=300)
+    p, i, w = graph("random", 8, 4)
+    rp, col, val, yy = synth.csr_data(wl)
+    shards = csr_shards(wl, rp, col, val, yy)
+    sess = asap.Session(8, wl.dim, p, i, w)
+    sess.bind_csr(rp, col, val, yy, wl.samples)
+    W = np.zeros((8, wl.dim))
+    # (batch, seed) per round: hit, batch change, seed change, hit, hit
+    plan = [(64, 0), (64, 0), (37, 0), (37, 5), (37, 5), (37, 5)]
+    for r, (B, seed) in enumerate(plan):
+        sess.round(asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, B, seed))
+        got = sess.models().cpu().numpy()
+        kw = dict(oracle_kw(wl), batch=B)
+        halves = []
+        for k in range(8):
+            _, rpk, ck, vk, yk = shards[k]
+            sched = oracle.prng.schedule(wl.samples, seed, k, r)
+            halves.append(oracle.sgd.sgd_pass_csr(W[k], rpk, ck, vk, yk, sched, rnd=r, **kw))
+        W = oracle.mix.stochastic_reduce(np.stack(halves), p, i, w)
+        assert_models_close(got, W, what=f"round {r} (batch {B}, seed {seed})")
+    assert sess.check()[0] == asap.OK
+    sess.close()
+
+
 def _cone_round0(wl, shards, p, i, w, rows):
     """Oracle round 0 from zero models for the listed output rows only.
 
