@@ -280,12 +280,20 @@ def main():
         out["reduce"] = reduce_info
         if wl.features == "csr":
             alg, reads, writes = csr_algorithmic_bytes(wl, rp, col)
-            kernel, src = "sgd_csr_kernel", os.path.join(csrc, "kernels_csr.hip")
+            # the planned pass takes minibatches of up to 64 rows of up to 128
+            # nonzeros; anything else runs the general kernel
+            if wl.batch <= 64 and int(np.diff(rp).max()) <= 128:
+                kernel, src = "sgd_csr_fast_kernel", os.path.join(csrc, "kernels_csr_plan.hip")
+            else:
+                kernel, src = "sgd_csr_kernel", os.path.join(csrc, "kernels_csr.hip")
         else:
             S, B = wl.samples, wl.batch
             steps_per_pass = -(-S // B)
             alg = n * (S * (4 * D + 4 + 4) + steps_per_pass * 8 * D)
-            kernel, src = "sgd_dense_kernel", os.path.join(csrc, "kernels_sgd.hip")
+            if 1024 < D <= 8192:
+                kernel, src = "sgd_dense_wide_kernel", os.path.join(csrc, "kernels_dense.hip")
+            else:
+                kernel, src = "sgd_dense_kernel", os.path.join(csrc, "kernels_sgd.hip")
         ach = alg / (sgd_ms * 1e-3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                            "frac": ach / HBM_PEAK_GBPS, "kernel": kernel, "algorithmic_bytes": alg,

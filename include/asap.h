@@ -26,6 +26,9 @@
  *  - The library never allocates device memory: the caller owns the
  *    workspace, the two model buffers and the data shards (device pointers,
  *    e.g. from torch tensors) and keeps them alive until asap_destroy.
+ *  - With CSR data bound, the library also owns one non-blocking stream
+ *    (default priority) and a few events, created at asap_bind_workspace
+ *    and released by asap_destroy; see asap_local_sgd.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    All device work is asynchronous on that stream, in call order.
  *  - A context is not thread-safe; use one per host thread.
@@ -144,7 +147,8 @@ asap_status asap_create(int32_t n_workers, int64_t dim, const int32_t* nbr_ptr,
 asap_status asap_workspace_size(const asap_ctx* ctx, size_t* bytes);
 
 /* Bind caller-owned device workspace (256-byte aligned, >= the size above)
- * and upload the graph on `stream`.  Must precede every device call. */
+ * and upload the graph on `stream`.  Must precede every device call.  Waits
+ * for look-ahead work on the previous workspace (asap_local_sgd) first. */
 asap_status asap_bind_workspace(asap_ctx* ctx, void* dev, size_t bytes, void* stream);
 
 /* Bind the two model buffers, each [n][ld] fp32 row-major on the device,
@@ -186,7 +190,16 @@ asap_status asap_bind_csr(asap_ctx* ctx, const int64_t* row_ptr, const int32_t* 
  * use the pre-step model; the gradient is the batch mean (1/B') sum c_b x_b
  * + l2 w; t = round * ceil(S/B) + k + 1.  At most once per round, before
  * the reduce.  Errors: ASAP_E_STATE (no data/models/workspace bound or SGD
- * already done this round), ASAP_E_INVALID_ARG. */
+ * already done this round), ASAP_E_INVALID_ARG.
+ * CSR look-ahead: the per-round sample schedule and column plan do not
+ * depend on the models, so after enqueueing round r on `stream` the call
+ * also plans round r + 1 (same seed and batch) on the library's own stream,
+ * concurrently with round r, into a second plan area of the workspace; a
+ * later call for that round, seed and batch waits for it (an event) instead
+ * of planning, any other call plans afresh.  That work reads the bound
+ * shards and writes only the workspace, and every asap_bind_* call and
+ * asap_destroy waits for it before returning: until then the workspace and
+ * the shards must stay allocated. */
 asap_status asap_local_sgd(asap_ctx* ctx, const asap_sgd_params* p, void* stream);
 
 /* Stochastic reduce of (A.2), all workers: W'[i] = sum_j P_ij W[j] from the

@@ -163,7 +163,7 @@ void layout(asap_ctx* c) {
   const int cpq = c->kind == kDense ? dense_wide_cpq(c->dim) : 0;
   c->dense_k = cpq ? std::max(1, std::min(kDenseMaxMembers, kDenseCus / std::max(1, c->n))) : 1;
   const size_t ldp = size_t(cpq) * 2048;
-  c->off_dacc = o;    o = align_up(o + (c->dense_k > 1 ? 3 * n * ldp * 8 : 0));
+  c->off_dacc = o;    o = align_up(o + (c->dense_k > 1 ? 2 * n * size_t(c->dense_k) * ldp * 4 : 0));
   c->off_dcount = o;  o = align_up(o + (cpq ? n * 4 : 0));
   c->total = o;
 }
@@ -761,15 +761,13 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
     e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->plan[0].sched), s);
     if (e == hipSuccess && dense_wide_cpq(c->dim)) {
       DenseSync ds{};
-      ds.acc = at<int64_t>(c, c->off_dacc);
-      ds.xmax = at<float>(c, c->off_vmax);
+      ds.part = at<float>(c, c->off_dacc);
       ds.count = at<uint32_t>(c, c->off_dcount);
       ds.ldp = int64_t(dense_wide_cpq(c->dim)) * 2048;
       ds.K = std::max(1, std::min(c->dense_k, dense_wide_max_members(a, c->n_cu) / c->n));
       ds.spin_limit = kDenseSpinLimit;
       ds.err = at<int32_t>(c, c->off_err) + kErrRendezvous;
       e = launch_fill_i32(reinterpret_cast<int32_t*>(ds.count), c->n, 0, s);
-      if (e == hipSuccess && ds.K > 1) e = launch_fill_i64(ds.acc, 3 * int64_t(c->n) * ds.ldp, 0, s);
       if (e == hipSuccess) e = launch_sgd_dense_wide(a, ds, s);
     } else if (e == hipSuccess) {
       e = launch_sgd_dense(a, s);

@@ -113,8 +113,7 @@ hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s);
 // shard); `count` ([n], zero at launch) counts arrivals.  A rendezvous that
 // waits longer than spin_limit polls adds 1 to *err and ends the pass.
 struct DenseSync {
-  int64_t* acc;
-  const float* xmax;
+  float* part;  // [2][n][K][ldp]: fp32 member partial gradients of step t (slot t & 1)
   uint32_t* count;
   int64_t ldp;
   int32_t K;

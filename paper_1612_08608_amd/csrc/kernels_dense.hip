@@ -7,9 +7,11 @@
 // MFMA is not used.  One workgroup per worker would leave most of the chip
 // idle when workers are few, so K workgroups share a worker: each holds the
 // whole model slice in registers, takes a contiguous K-th of every
-// minibatch, and the K partial gradients are summed once per step in the
-// workspace as exact 64-bit fixed point (device-scope integer atomics), so
-// the sum is the same whatever the order the members arrive in.
+// minibatch, and once per step every member publishes its partial gradient
+// (rounded to fp32) in the workspace and sums all K of them in fp64 in
+// member order (plain device-scope stores and loads; integer atomics on the
+// shared lines, and a reduce-scatter with a second meeting, were slower),
+// so every member gets the same sum whatever the order they arrive in.
 // The launch is cooperative, so every member is resident and the rendezvous
 // cannot wait on a workgroup that has not started; the wait is bounded
 // anyway and reports a timeout instead of spinning for ever.
@@ -153,16 +155,6 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
 
   const int B = a.batch, S = int(a.S);  // S < 2^31 (checked at bind)
   const int KS = (S + B - 1) / B;
-  // fixed-point scale of the member exchange: |gradient entry| <= B max|x|
-  // <= 2^ex, so 2^(62 - ex) keeps every partial and every sum below 2^62
-  double fx = 1.0, inv_fx = 1.0;
-  if (K > 1) {
-    int ex = 0;
-    const double bound = double(B) * double(ds.xmax[i]);
-    if (bound > 0.0) frexp(bound, &ex);
-    fx = ldexp(1.0, 62 - ex);
-    inv_fx = ldexp(1.0, ex - 62);
-  }
   // valid components of the thread's last float4 of each q (entries of X
   // past dim are never used)
   int nv[CPQ];
@@ -307,12 +299,16 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   // without cache write-back or invalidation); a wave's writes are
   // acknowledged before the barrier, and one thread counts the workgroup in
   // and waits, for a bounded time, until all K members have arrived.
-  auto rendezvous = [&](uint32_t target) -> bool {
+  // Work issued between arrive() and gather() overlaps the wait: loads
+  // issued there land while the members gather.
+  auto arrive = [&]() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    if (tid == 0) __hip_atomic_fetch_add(ds.count + i, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+  auto gather = [&](uint32_t target) -> bool {
     if (tid == 0) {
-      __hip_atomic_fetch_add(ds.count + i, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       uint32_t spins = 0;
       while (__hip_atomic_load(ds.count + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
         if (++spins > ds.spin_limit) {
@@ -328,43 +324,44 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   };
 
   // end of step t: exchange (K > 1) and update; false when the rendezvous
-  // timed out
-  auto finish_step = [&](int t) -> bool {
+  // timed out.  `during` issues the next sub-batch's loads (see rendezvous).
+  auto finish_step = [&](int t, auto&& during) -> bool {
     const int Bp = min(B, S - t * B);
+    // member partials of step t: slot t & 1 (a member writes slot t & 1
+    // again at step t + 2, after every member has passed the rendezvous of
+    // step t + 1, which each reaches only after reading step t's partials)
+    const int64_t slot = (int64_t(t & 1) * a.n + i) * K;
     if (K > 1) {
-      // members add their partials as exact 64-bit fixed point into
-      // acc[t mod 3] (integer addition commutes: the sum does not depend on
-      // arrival order), each clears its column slice of acc[(t+1) mod 3]
-      // (last read before the previous rendezvous, next written after this
-      // one), then all read the sum back
-      int64_t* acc = ds.acc + (int64_t(t % 3) * a.n + i) * ds.ldp;
+      // every member publishes its partial gradient, rounded to fp32, with
+      // plain device-scope stores (one writer per word: no atomic
+      // read-modify-write on shared lines), component-major
+      // ([q][e][thread]) so that every wave access is contiguous, ...
+      uint32_t* mine = reinterpret_cast<uint32_t*>(ds.part + (slot + k) * ds.ldp);
 #pragma unroll
-      for (int q = 0; q < CPQ; ++q) {
-        const int64_t c = 4 * (int64_t(tid) + int64_t(kThreads) * q);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const long long v = __double2ll_rn(g[q][e] * fx);
-          if (v != 0)
-            __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(acc + c + e), static_cast<unsigned long long>(v),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
-      {
-        int64_t* nxt = ds.acc + (int64_t((t + 1) % 3) * a.n + i) * ds.ldp;
-        const int64_t L = (ds.ldp + K - 1) / K, c0 = k * L, c1 = min(c0 + L, ds.ldp);
-        for (int64_t c = c0 + tid; c < c1; c += kThreads)
-          __hip_atomic_store(reinterpret_cast<unsigned long long*>(nxt + c), 0ull, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-      }
-      if (!rendezvous(uint32_t(K) * uint32_t(t + 1))) return false;
-#pragma unroll
-      for (int q = 0; q < CPQ; ++q) {
-        const int64_t c = 4 * (int64_t(tid) + int64_t(kThreads) * q);
+      for (int q = 0; q < CPQ; ++q)
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          g[q][e] = double(static_cast<long long>(__hip_atomic_load(
-                        reinterpret_cast<unsigned long long*>(acc + c + e), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) *
-                    inv_fx;
+          __hip_atomic_store(mine + (q * 4 + e) * kThreads + tid, __float_as_uint(float(g[q][e])), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+      arrive();
+    }
+    during();
+    if (K > 1) {
+      if (!gather(uint32_t(K) * uint32_t(t + 1))) return false;
+      // ... and every member sums all K partials in fp64 in member order,
+      // so all members get the same gradient bit for bit
+      uint32_t* all = reinterpret_cast<uint32_t*>(ds.part + slot * ds.ldp);
+#pragma unroll
+      for (int q = 0; q < CPQ; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) g[q][e] = 0.0;
+      for (int m = 0; m < K; ++m) {
+#pragma unroll
+        for (int q = 0; q < CPQ; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            g[q][e] += double(__uint_as_float(__hip_atomic_load(all + m * ds.ldp + (q * 4 + e) * kThreads + tid,
+                                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)));
       }
     }
     const double eta = step_size(a.lr_kind, a.lr0, a.round * KS + t + 1);
@@ -388,10 +385,13 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     return true;
   };
 
-  // Rows of the next sub-batch load into xb while xa is processed; the copy
-  // xa = xb then waits for loads that had the whole sub-batch to land.
-  // Every member finishes every step (exchange + update), also the steps in
-  // which it has no samples.
+  // Rows of the next sub-batch of the same step load into xb while xa is
+  // processed; the copy xa = xb then waits for loads that had the whole
+  // sub-batch to land.  The first sub-batch of a new step loads into xa
+  // during the exchange that ends the step before it (its row indices are
+  // staged by then), so the members' wait overlaps HBM reads and a member
+  // arrives without waiting for them.  Every member finishes every step
+  // (exchange + update), also the steps in which it has no samples.
   float4 xa[SR][CPQ], xb[SR][CPQ];
   float ya = 0.f, yb = 0.f;
   bool ok = true;
@@ -407,18 +407,27 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   cur.sb = cur.lo;
   cur = settle(cur);
   if (cur.t < KS) load(xa, ya, cur);
-  for (;;) {
-    while (ok && done < min(cur.t, KS)) ok = finish_step(done++);
-    if (!ok || cur.t >= KS) break;
+  while (ok && done < min(cur.t, KS)) ok = finish_step(done++, [] {});  // steps without samples
+  while (ok && cur.t < KS) {
     const Pos nx = settle(Pos{cur.t, cur.sb + SR, cur.lo, cur.hi});
-    if (nx.t < KS) load(xb, yb, nx);
+    const bool same = nx.t == cur.t;
+    if (same) load(xb, yb, nx);
     process(xa, ya, cur);
+    if (same) {
+#pragma unroll
+      for (int s2 = 0; s2 < SR; ++s2)
+#pragma unroll
+        for (int q = 0; q < CPQ; ++q) xa[s2][q] = xb[s2][q];
+      ya = yb;
+    } else {
+      while (ok && done < min(nx.t, KS)) {
+        const int t = done++;
+        ok = finish_step(t, [&]() {
+          if (t + 1 == nx.t && nx.t < KS) load(xa, ya, nx);
+        });
+      }
+    }
     cur = nx;
-#pragma unroll
-    for (int s2 = 0; s2 < SR; ++s2)
-#pragma unroll
-      for (int q = 0; q < CPQ; ++q) xa[s2][q] = xb[s2][q];
-    ya = yb;
   }
 
   if (k == 0) {

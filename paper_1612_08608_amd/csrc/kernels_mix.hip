@@ -220,7 +220,10 @@ __device__ __forceinline__ void store_partial(float* d, float4 v, int k) {
 template <int DEG> constexpr int slab_group() { return DEG <= 5 ? DEG : 4; }
 
 // PF float4 per thread per chunk: a chunk is PF*16 KiB of LDS and PF
-// registers' worth of loads in flight per thread.
+// registers' worth of loads in flight per thread.  Outputs are computed and
+// stored kOut float4 at a time.
+constexpr int kOut = 4;
+
 template <int DEG, int PF>
 __global__ __launch_bounds__(kSlabThreads) void mix_slab_kernel(MixArgs a, int nchunks) {
   constexpr int kVec = PF * kSlabThreads;    // float4 slots per chunk
@@ -231,6 +234,7 @@ __global__ __launch_bounds__(kSlabThreads) void mix_slab_kernel(MixArgs a, int n
   const int X = min(Q, 8) - 1;               // swizzle mask
   const int tid = threadIdx.x;
   const int row = tid % n, grp = tid / n;    // compute: row, float4 [grp*PF, grp*PF+PF)
+  static_assert(PF % kOut == 0, "outputs go kOut float4 at a time");
   constexpr int G = slab_group<DEG>();
   // jq = j*Q | (j & X): the slot of float4 q of row j is jq ^ q, because
   // X < Q and Q is a power of two (see the staging writes below).
@@ -297,11 +301,12 @@ __global__ __launch_bounds__(kSlabThreads) void mix_slab_kernel(MixArgs a, int n
     return acc;
   };
   // Stores: lane = row is the natural compute layout, but then every store
-  // instruction would scatter 16 bytes to each of 64 rows.  The PF outputs
-  // of PF consecutive lanes are transposed across those lanes instead, so
-  // that store k of lane i writes float4 slot grp*PF + i of row
-  // (row & ~(PF-1)) + k: PF lanes fill PF*16 contiguous bytes of one row.
-  const int lane_in = row & (PF - 1), row_base = row & ~(PF - 1);
+  // instruction would scatter 16 bytes to each of 64 rows.  Each group of
+  // kOut outputs of kOut consecutive lanes is transposed across those lanes
+  // instead, so that store k of lane i writes float4 slot base + i of row
+  // (row & ~(kOut-1)) + k: kOut lanes fill kOut*16 contiguous bytes of one
+  // row.
+  const int lane_in = row & (kOut - 1), row_base = row & ~(kOut - 1);
   const uint64_t okmask = __ballot(ok);
   const int lane = int(threadIdx.x) & 63;
   if (ch0 < ch1) load(ch0);
@@ -314,22 +319,25 @@ __global__ __launch_bounds__(kSlabThreads) void mix_slab_kernel(MixArgs a, int n
     }
     lds_barrier();
     if (ch + 1 < ch1) load(ch + 1);
-    float4 res[PF];
+#pragma unroll 1
+    for (int h = 0; h < PF / kOut; ++h) {
+      float4 res[kOut];
 #pragma unroll
-    for (int u = 0; u < PF; ++u) res[u] = slab_row(grp * PF + u);
-    transpose_lanes<PF>(res, lane_in);
-    const int64_t c = int64_t(ch) * C + 4 * (grp * PF + lane_in);
-    if (c < a.dim) {
-      const bool full = c + 4 <= a.dim;
-      const int k_tail = int(min<int64_t>(a.dim - c, 4));
+      for (int u = 0; u < kOut; ++u) res[u] = slab_row(grp * PF + h * kOut + u);
+      transpose_lanes<kOut>(res, lane_in);
+      const int64_t c = int64_t(ch) * C + 4 * (grp * PF + h * kOut + lane_in);
+      if (c < a.dim) {
+        const bool full = c + 4 <= a.dim;
+        const int k_tail = int(min<int64_t>(a.dim - c, 4));
 #pragma unroll
-      for (int k = 0; k < PF; ++k) {
-        if ((okmask >> (lane - lane_in + k)) & 1) {
-          float* d = a.dst + int64_t(row_base + k) * a.ld + c;
-          if (full) {
-            *reinterpret_cast<float4*>(d) = res[k];
-          } else {
-            store_partial(d, res[k], k_tail);
+        for (int k = 0; k < kOut; ++k) {
+          if ((okmask >> (lane - lane_in + k)) & 1) {
+            float* d = a.dst + int64_t(row_base + k) * a.ld + c;
+            if (full) {
+              *reinterpret_cast<float4*>(d) = res[k];
+            } else {
+              store_partial(d, res[k], k_tail);
+            }
           }
         }
       }
@@ -380,9 +388,14 @@ hipError_t launch_slab(const MixArgs& a, int n_cu, hipStream_t s) {
 hipError_t launch_mix_slab(const MixArgs& a, int max_deg, int n_cu, hipStream_t s) {
   const int n = a.n;
   if (n < 8 || n > kSlabThreads || (n & (n - 1)) || max_deg > 17) return hipErrorNotSupported;
-  if (max_deg <= 3) return launch_slab<3, 4>(a, n_cu, s);
-  if (max_deg <= 5) return launch_slab<5, 4>(a, n_cu, s);
-  if (max_deg <= 9) return launch_slab<9, 4>(a, n_cu, s);
+  // With more than 512 rows a 64 KiB chunk holds under 128 bytes of each
+  // row, half a cache line, and the other half is fetched again for the
+  // next chunk; a 128 KiB chunk (8 float4 per thread) reads whole lines.
+  // Rows of 17 entries keep 4 (8 would not fit the registers).
+  const bool wide = n > 512;
+  if (max_deg <= 3) return wide ? launch_slab<3, 8>(a, n_cu, s) : launch_slab<3, 4>(a, n_cu, s);
+  if (max_deg <= 5) return wide ? launch_slab<5, 8>(a, n_cu, s) : launch_slab<5, 4>(a, n_cu, s);
+  if (max_deg <= 9) return wide ? launch_slab<9, 8>(a, n_cu, s) : launch_slab<9, 4>(a, n_cu, s);
   return launch_slab<17, 4>(a, n_cu, s);
 }
 
