@@ -224,6 +224,10 @@ def main():
 
     def step(ev=None):
         if prm is not None:
+            # the round's schedule and plan first (waits for the plan made
+            # during the previous round), so that the event pair brackets the
+            # SGD kernels alone
+            sess.prepare_sgd(prm)
             if ev:
                 ev[0].record(stream)
             sess.local_sgd(prm)

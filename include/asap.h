@@ -202,6 +202,15 @@ asap_status asap_bind_csr(asap_ctx* ctx, const int64_t* row_ptr, const int32_t* 
  * the shards must stay allocated. */
 asap_status asap_local_sgd(asap_ctx* ctx, const asap_sgd_params* p, void* stream);
 
+/* Optional first half of asap_local_sgd: enqueue on `stream` the current
+ * round's sample schedule (asap_schedule of Section 5's per-worker pass
+ * order; for CSR data also the row descriptors and the column plan, or a
+ * wait for the look-ahead plan of this round), so that the SGD kernels of
+ * the following asap_local_sgd with the same round, seed and batch start at
+ * once.  asap_local_sgd does this itself when it was not done (or was done
+ * for other parameters).  Same errors as asap_local_sgd. */
+asap_status asap_prepare_sgd(asap_ctx* ctx, const asap_sgd_params* p, void* stream);
+
 /* Stochastic reduce of (A.2), all workers: W'[i] = sum_j P_ij W[j] from the
  * current buffer into the other one, after checking that every neighbour's
  * tag says "published this round" (a mismatch skips that worker's row and

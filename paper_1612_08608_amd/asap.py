@@ -30,7 +30,7 @@ EXPORTS = (
     "asap_graph_ring", "asap_graph_complete", "asap_graph_random_regular",
     "asap_metropolis_weights", "asap_schedule", "asap_create", "asap_workspace_size",
     "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr",
-    "asap_local_sgd", "asap_stochastic_reduce", "asap_round", "asap_current",
+    "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_current",
     "asap_set_round", "asap_schedule_device", "asap_metrics", "asap_check",
     "asap_debug_set_tag", "asap_last_error", "asap_destroy",
 )
@@ -73,6 +73,7 @@ def lib():
         "asap_bind_dense": [p, p, p, i64, i64],
         "asap_bind_csr": [p, p, p, p, p, i64, i64, p],
         "asap_local_sgd": [p, C.POINTER(SgdParams), p],
+        "asap_prepare_sgd": [p, C.POINTER(SgdParams), p],
         "asap_stochastic_reduce": [p, p],
         "asap_round": [p, C.POINTER(SgdParams), p],
         "asap_current": [p, C.POINTER(i32), C.POINTER(i64), C.POINTER(i32)],
@@ -209,6 +210,10 @@ def asap_local_sgd(ctx, params: SgdParams, stream=None):
     _check(lib().asap_local_sgd(ctx, C.byref(params), _stream(stream)), ctx)
 
 
+def asap_prepare_sgd(ctx, params: SgdParams, stream=None):
+    _check(lib().asap_prepare_sgd(ctx, C.byref(params), _stream(stream)), ctx)
+
+
 def asap_stochastic_reduce(ctx, stream=None):
     _check(lib().asap_stochastic_reduce(ctx, _stream(stream)), ctx)
 
@@ -334,6 +339,9 @@ class Session:
     # hot path -----------------------------------------------------------
     def local_sgd(self, params, stream=None):
         asap_local_sgd(self.ready().ctx, params, stream)
+
+    def prepare_sgd(self, params, stream=None):
+        asap_prepare_sgd(self.ready().ctx, params, stream)
 
     def stochastic_reduce(self, stream=None):
         asap_stochastic_reduce(self.ready().ctx, stream)

@@ -99,6 +99,14 @@ struct asap_ctx {
   int64_t ahead_round = -1;
   int32_t ahead_batch = 0;
 
+  // the half-step inputs enqueued by asap_prepare_sgd (or by asap_local_sgd
+  // itself): which RoundPlan holds them and for which round, seed and batch
+  bool prep_valid = false;
+  int prep_slot = 0;
+  uint64_t prep_seed = 0;
+  int64_t prep_round = -1;
+  int32_t prep_batch = 0;
+
   std::string err;
 };
 
@@ -174,6 +182,7 @@ void layout(asap_ctx* c) {
 void drain_ahead(asap_ctx* c) {
   if (c->ahead) (void)hipStreamSynchronize(c->ahead);
   c->ahead_valid = false;
+  c->prep_valid = false;
 }
 
 void release_ahead(asap_ctx* c) {
@@ -707,31 +716,66 @@ hipError_t prepare_csr_round(asap_ctx* c, const asap_sgd_params* p, int64_t roun
   return e;
 }
 
-}  // namespace
-
-extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, void* stream) {
-  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
-  asap_status st = need_device(c);
-  if (st != ASAP_OK) return st;
-  if (c->kind == kNoData) return fail(c, ASAP_E_STATE, "no data bound");
-  if (c->half_done) return fail(c, ASAP_E_STATE, "the half-step of round %lld already ran", (long long)c->round);
-  if ((st = check_params(c, p)) != ASAP_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+// The current round's half-step inputs on stream s (the schedule; for CSR
+// also the row descriptors and the plan), unless already enqueued for this
+// round, seed and batch.  A CSR round planned ahead by the previous
+// asap_local_sgd is waited for instead of planned again.
+hipError_t prepare_half_step(asap_ctx* c, const asap_sgd_params* p, hipStream_t s) {
+  if (c->prep_valid && c->prep_round == c->round && c->prep_seed == p->seed && c->prep_batch == p->batch)
+    return hipSuccess;
   hipError_t e = hipSuccess;
+  int slot = 0;
   if (c->kind == kCsr) {
-    // this round's buffers: planned ahead by the previous call when round,
-    // seed and batch match, else prepared here
     const bool hit = c->ahead_valid && c->ahead_round == c->round && c->ahead_seed == p->seed &&
                      c->ahead_batch == p->batch;
-    int slot = 0;
     if (c->ahead_valid) {
       slot = c->ahead_slot;
       e = hipStreamWaitEvent(s, c->ev_ready[slot], 0);  // a miss rewrites that slot after it
     }
     c->ahead_valid = false;
+    const bool planned = csr_plan_fits(sgd_args(c, p, c->plan[slot]));
+    if (e == hipSuccess && !hit) e = prepare_csr_round(c, p, c->round, c->plan[slot], planned, s);
+  } else {
+    e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->plan[0].sched), s);
+  }
+  c->prep_valid = e == hipSuccess;
+  c->prep_slot = slot;
+  c->prep_round = c->round;
+  c->prep_seed = p->seed;
+  c->prep_batch = p->batch;
+  return e;
+}
+
+asap_status check_half_step(asap_ctx* c, const asap_sgd_params* p) {
+  asap_status st = need_device(c);
+  if (st != ASAP_OK) return st;
+  if (c->kind == kNoData) return fail(c, ASAP_E_STATE, "no data bound");
+  if (c->half_done) return fail(c, ASAP_E_STATE, "the half-step of round %lld already ran", (long long)c->round);
+  return check_params(c, p);
+}
+
+}  // namespace
+
+extern "C" asap_status asap_prepare_sgd(asap_ctx* c, const asap_sgd_params* p, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  asap_status st = check_half_step(c, p);
+  if (st != ASAP_OK) return st;
+  const hipError_t e = prepare_half_step(c, p, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ASAP_OK : hip_fail(c, e, "half-step preparation");
+}
+
+extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  asap_status st = check_half_step(c, p);
+  if (st != ASAP_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = prepare_half_step(c, p, s);
+  if (e != hipSuccess) return hip_fail(c, e, "half-step preparation");
+  const int slot = c->prep_slot;
+  c->prep_valid = false;
+  if (c->kind == kCsr) {
     SgdArgs a = sgd_args(c, p, c->plan[slot]);
     const bool planned = csr_plan_fits(a);
-    if (e == hipSuccess && !hit) e = prepare_csr_round(c, p, c->round, c->plan[slot], planned, s);
     if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_start, s);
     if (planned) {
       const PlanArgs pa = plan_args(c, p, c->plan[slot]);
@@ -744,7 +788,9 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
     if (planned && c->ahead) {
       // plan the next round into the other slot, concurrently with this
       // pass: after this call's inputs are ready (ev_start) and after the
-      // slot's last reader (ev_used)
+      // slot's last reader (ev_used).  With fewer workers than compute
+      // units it runs beside the pass; otherwise it fills the pass's tail
+      // and overlaps the reduce.
       const int o = slot ^ 1;
       if ((e = hipStreamWaitEvent(c->ahead, c->ev_start, 0)) || (e = hipStreamWaitEvent(c->ahead, c->ev_used[o], 0)) ||
           (e = prepare_csr_round(c, p, c->round + 1, c->plan[o], true, c->ahead)) ||
@@ -758,8 +804,7 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
     }
   } else {
     SgdArgs a = sgd_args(c, p, c->plan[0]);
-    e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->plan[0].sched), s);
-    if (e == hipSuccess && dense_wide_cpq(c->dim)) {
+    if (dense_wide_cpq(c->dim)) {
       DenseSync ds{};
       ds.part = at<float>(c, c->off_dacc);
       ds.count = at<uint32_t>(c, c->off_dcount);
@@ -769,7 +814,7 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
       ds.err = at<int32_t>(c, c->off_err) + kErrRendezvous;
       e = launch_fill_i32(reinterpret_cast<int32_t*>(ds.count), c->n, 0, s);
       if (e == hipSuccess) e = launch_sgd_dense_wide(a, ds, s);
-    } else if (e == hipSuccess) {
+    } else {
       e = launch_sgd_dense(a, s);
     }
     if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");

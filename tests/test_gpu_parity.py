@@ -123,6 +123,8 @@ def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False):
         sess.bind_csr(rp, col, val, yy, wl.samples)
     prm = params(wl)
     for r in range(rounds):
+        if r % 2:
+            sess.prepare_sgd(prm)  # optional; asap_local_sgd prepares by itself on even rounds
         sess.round(prm)
         got = sess.models().cpu().numpy()
         amb = []
@@ -276,10 +278,15 @@ def test_csr_plan_ahead_follows_changing_params(torch):
     sess = asap.Session(8, wl.dim, p, i, w)
     sess.bind_csr(rp, col, val, yy, wl.samples)
     W = np.zeros((8, wl.dim))
-    # (batch, seed) per round: hit, batch change, seed change, hit, hit
-    plan = [(64, 0), (64, 0), (37, 0), (37, 5), (37, 5), (37, 5)]
-    for r, (B, seed) in enumerate(plan):
-        sess.round(asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, B, seed))
+    # (batch, seed, what asap_prepare_sgd is called with first) per round:
+    # look-ahead hit, batch change, seed change, prepared with the same
+    # parameters, prepared with other ones (ignored), hit
+    plan = [(64, 0, None), (64, 0, None), (37, 0, None), (37, 5, (37, 5)), (37, 5, (64, 1)), (37, 5, None)]
+    for r, (B, seed, prep) in enumerate(plan):
+        prm = asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, B, seed)
+        if prep is not None:
+            sess.prepare_sgd(asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, prep[0], prep[1]))
+        sess.round(prm)
         got = sess.models().cpu().numpy()
         kw = dict(oracle_kw(wl), batch=B)
         halves = []
