@@ -76,7 +76,7 @@ struct asap_ctx {
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
-         off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dcount = 0, total = 0;
+         off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dxcd = 0, off_dcount = 0, total = 0;
   RoundPlan plan[2];
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
@@ -172,6 +172,7 @@ void layout(asap_ctx* c) {
   c->dense_k = cpq ? std::max(1, std::min(kDenseMaxMembers, kDenseCus / std::max(1, c->n))) : 1;
   const size_t ldp = size_t(cpq) * 2048;
   c->off_dacc = o;    o = align_up(o + (c->dense_k > 1 ? 2 * n * size_t(c->dense_k) * ldp * 4 : 0));
+  c->off_dxcd = o;    o = align_up(o + (c->dense_k > 1 ? n * size_t(c->dense_k) * 4 : 0));
   c->off_dcount = o;  o = align_up(o + (cpq ? n * 4 : 0));
   c->total = o;
 }
@@ -808,6 +809,7 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
       DenseSync ds{};
       ds.part = at<float>(c, c->off_dacc);
       ds.count = at<uint32_t>(c, c->off_dcount);
+      ds.xcd = at<int32_t>(c, c->off_dxcd);
       ds.ldp = int64_t(dense_wide_cpq(c->dim)) * 2048;
       ds.K = std::max(1, std::min(c->dense_k, dense_wide_max_members(a, c->n_cu) / c->n));
       ds.spin_limit = kDenseSpinLimit;

@@ -114,6 +114,7 @@ hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s);
 // waits longer than spin_limit polls adds 1 to *err and ends the pass.
 struct DenseSync {
   float* part;  // [2][n][K][ldp]: fp32 member partial gradients of step t (slot t & 1)
+  int32_t* xcd;  // [n][K]: the XCD each member runs on
   uint32_t* count;
   int64_t ldp;
   int32_t K;

@@ -9,9 +9,13 @@
 // whole model slice in registers, takes a contiguous K-th of every
 // minibatch, and once per step every member publishes its partial gradient
 // (rounded to fp32) in the workspace and sums all K of them in fp64 in
-// member order (plain device-scope stores and loads; integer atomics on the
-// shared lines, and a reduce-scatter with a second meeting, were slower),
-// so every member gets the same sum whatever the order they arrive in.
+// member order, so every member gets the same sum whatever the order they
+// arrive in.  Members of a worker are placed on one XCD when the grid
+// allows (workgroups are dealt to the XCDs round-robin; each member checks
+// the XCD it runs on), and then meet in that XCD's L2: 16-byte stores and
+// loads that only bypass the CU's L1.  Device-scope accesses, which go past
+// the L2, made the exchange cost a third of the pass; integer atomics on
+// shared lines and a reduce-scatter with a second meeting were slower still.
 // The launch is cooperative, so every member is resident and the rendezvous
 // cannot wait on a workgroup that has not started; the wait is bounded
 // anyway and reports a timeout instead of spinning for ever.
@@ -95,6 +99,18 @@ __device__ __forceinline__ double row_reduce(double (&d)[16], int lane) {
   if constexpr (SR >= 16) halve<8, SR / 8>(d, lane); else d[0] += xor_lane<8>(d[0]);
   return d[0];
 }
+
+// The XCD (accelerator complex die) this wave runs on: hardware register
+// XCC_ID, bits [3:0].  Workgroups are dealt to the XCDs round-robin.
+__device__ __forceinline__ int xcd_id() {
+  return int(__builtin_amdgcn_s_getreg(20 | (0 << 6) | ((16 - 1) << 11)) & 0xfu);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
+}
+
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
@@ -237,6 +253,7 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
 #pragma unroll
     for (int e = 0; e < 4; ++e) g[q][e] = 0.0;
   int par = 0;
+  bool local = false;  // all members on this XCD (set before the first step)
 
   // margins, coefficients and gradient of the sub-batch held in xc
   auto process = [&](float4 (&xc)[SR][CPQ], float yl, Pos p) {
@@ -330,38 +347,49 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     // member partials of step t: slot t & 1 (a member writes slot t & 1
     // again at step t + 2, after every member has passed the rendezvous of
     // step t + 1, which each reaches only after reading step t's partials)
-    const int64_t slot = (int64_t(t & 1) * a.n + i) * K;
+    // this worker's K partials of slot t & 1, [K][CPQ][thread][4] fp32
+    const auto prs =
+        buf_rsrc(ds.part + (int64_t(t & 1) * a.n + i) * K * ds.ldp, uint32_t(K * ds.ldp) * 4u);
     if (K > 1) {
       // every member publishes its partial gradient, rounded to fp32, with
-      // plain device-scope stores (one writer per word: no atomic
-      // read-modify-write on shared lines), component-major
-      // ([q][e][thread]) so that every wave access is contiguous, ...
-      uint32_t* mine = reinterpret_cast<uint32_t*>(ds.part + (slot + k) * ds.ldp);
+      // one 16-byte store per q (one writer per word: no atomic
+      // read-modify-write on shared lines), ...
 #pragma unroll
-      for (int q = 0; q < CPQ; ++q)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          __hip_atomic_store(mine + (q * 4 + e) * kThreads + tid, __float_as_uint(float(g[q][e])), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
+      for (int q = 0; q < CPQ; ++q) {
+        const v4f v = {float(g[q][0]), float(g[q][1]), float(g[q][2]), float(g[q][3])};
+        const uint32_t off = uint32_t((k * ds.ldp + (q * kThreads + tid) * 4) * 4);
+        if (local)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, v),
+                                                 prs, off, 0, 0);
+        else
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, v),
+                                                 prs, off, 0, 16);  // sc1: device scope
+      }
       arrive();
     }
     during();
     if (K > 1) {
-      if (!gather(uint32_t(K) * uint32_t(t + 1))) return false;
+      if (!gather(uint32_t(K) * uint32_t(t + 2))) return false;
       // ... and every member sums all K partials in fp64 in member order,
-      // so all members get the same gradient bit for bit
-      uint32_t* all = reinterpret_cast<uint32_t*>(ds.part + slot * ds.ldp);
+      // so all members get the same gradient bit for bit.  Members on one
+      // XCD meet in its L2 (loads that bypass only the CU's L1); otherwise
+      // the accesses are device-scope.
 #pragma unroll
       for (int q = 0; q < CPQ; ++q)
 #pragma unroll
         for (int e = 0; e < 4; ++e) g[q][e] = 0.0;
       for (int m = 0; m < K; ++m) {
 #pragma unroll
-        for (int q = 0; q < CPQ; ++q)
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            g[q][e] += double(__uint_as_float(__hip_atomic_load(all + m * ds.ldp + (q * 4 + e) * kThreads + tid,
-                                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)));
+        for (int q = 0; q < CPQ; ++q) {
+          const uint32_t off = uint32_t((m * ds.ldp + (q * kThreads + tid) * 4) * 4);
+          const auto u = local ? __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, 1)    // sc0: past the L1
+                               : __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, 16);  // sc1: device scope
+          const unsigned u0 = u[0], u1 = u[1], u2 = u[2], u3 = u[3];
+          g[q][0] += double(__uint_as_float(u0));
+          g[q][1] += double(__uint_as_float(u1));
+          g[q][2] += double(__uint_as_float(u2));
+          g[q][3] += double(__uint_as_float(u3));
+        }
       }
     }
     const double eta = step_size(a.lr_kind, a.lr0, a.round * KS + t + 1);
@@ -396,6 +424,18 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   float ya = 0.f, yb = 0.f;
   bool ok = true;
   int done = 0;  // steps finished
+  // Whether all members of the worker run on this XCD: they publish their
+  // XCD and meet once before the first step (count K; step t meets at
+  // K (t + 2)).
+  if (K > 1) {
+    const int me = xcd_id();
+    if (tid == 0) __hip_atomic_store(ds.xcd + i * K + k, me, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    arrive();
+    ok = gather(uint32_t(K));
+    local = ok;
+    for (int m = 0; m < K; ++m)
+      local = local && __hip_atomic_load(ds.xcd + i * K + m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == me;
+  }
   fetch(0);
   stage(0);
   fetch(1);
