@@ -77,8 +77,9 @@ __device__ __forceinline__ int table_find(const int* keys, int bits, int c) {
   return -1;
 }
 
-// exclusive prefix sum over the threads of a plan block (wave scans, then
-// the wave totals); *total gets the sum
+// exclusive prefix sum over the NW waves of a block (wave scans, then the
+// wave totals); *total gets the sum
+template <int NW>
 __device__ __forceinline__ int block_scan(int v, int* sc, int* total) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   int x = v;
@@ -91,7 +92,7 @@ __device__ __forceinline__ int block_scan(int v, int* sc, int* total) {
   __syncthreads();
   int base = 0, tot = 0;
 #pragma unroll
-  for (int w = 0; w < kPlanWaves; ++w) {
+  for (int w = 0; w < NW; ++w) {
     base += w < wave ? sc[w] : 0;
     tot += sc[w];
   }
@@ -141,16 +142,20 @@ __global__ __launch_bounds__(1024) void step_scan_kernel(PlanArgs p) {
 // ----------------------------------------------------------------------------
 // plan of one (worker, step): distinct columns, slots, per-nonzero codes
 // ----------------------------------------------------------------------------
-template <int TB>  // table positions: 2^TB >= 2 * (the step's nonzeros), LDS sized to match
-__global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
+// TB: table positions 2^TB >= 2 * (the step's nonzeros), LDS sized to
+// match; NT threads; H nonzeros per lane and row (rows of at most 64 H).
+template <int TB, int NT, int H>
+__global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
+  constexpr int NW = NT / 64;
+  static_assert(NT >= kHotWords, "one hot-bitmap word per thread");
   __shared__ int keys[1 << TB];
   __shared__ uint16_t ids[1 << TB];  // slots < 2^TB <= 2^13
   __shared__ uint32_t hot[kHotWords];
-  __shared__ int sc[kPlanWaves];
+  __shared__ int sc[NW];
   __shared__ long long rstart[kFastRows];
   __shared__ int rlen[kFastRows];
   __shared__ int overflow;
-  constexpr int kRowsPerWave = kFastRows / kPlanWaves;  // 8
+  constexpr int kRowsPerWave = kFastRows / NW;
   const int K = p.K, B = p.batch;
   const int i = int(blockIdx.x) / K, k = int(blockIdx.x) % K;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -170,21 +175,21 @@ __global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
     rstart[t] = r.start;
     rlen[t] = r.len;
   }
-  for (int q = t; q < tab; q += kPlanThreads) keys[q] = -1;
-  for (int q = t; q < kHotWords; q += kPlanThreads) hot[q] = 0u;
+  for (int q = t; q < tab; q += NT) keys[q] = -1;
+  for (int q = t; q < kHotWords; q += NT) hot[q] = 0u;
   if (t == 0) overflow = 0;
   __syncthreads();
-  // every code of the step in registers (rows of at most 128 nonzeros: two
+  // every code of the step in registers (rows of at most 64 H nonzeros: H
   // per lane), all loads issued before any is used; -1 marks no entry
-  int cc[kRowsPerWave][2];
-  float vv[kRowsPerWave][2];
+  int cc[kRowsPerWave][H];
+  float vv[kRowsPerWave][H];
 #pragma unroll
   for (int j = 0; j < kRowsPerWave; ++j) {
-    const int b = wave + j * kPlanWaves;
+    const int b = wave + j * NW;
     const int len = b < Bp ? rlen[b] : 0;
     const long long st = b < Bp ? rstart[b] : 0;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < H; ++h) {
       const int e = lane + 64 * h;
       cc[j][h] = e < len ? p.code[st + e] : -1;
       vv[j][h] = e < len ? p.val[st + e] : 0.f;
@@ -193,7 +198,7 @@ __global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
 #pragma unroll
   for (int j = 0; j < kRowsPerWave; ++j)
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < H; ++h) {
       const int c = cc[j][h];
       if (c == -1) continue;
       if (is_hot(c)) {
@@ -205,12 +210,12 @@ __global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
     }
   __syncthreads();
   // cold slots in table order: thread t numbers a contiguous run of positions
-  const int per = tab / kPlanThreads > 0 ? tab / kPlanThreads : 1;
+  const int per = tab / NT > 0 ? tab / NT : 1;
   const int q0 = t * per, q1 = min(q0 + per, tab);
   int cnt = 0;
   for (int q = q0; q < q1; ++q) cnt += keys[q] >= 0;
   int Uc = 0;
-  int id = block_scan(cnt, sc, &Uc);
+  int id = block_scan<NW>(cnt, sc, &Uc);
   for (int q = q0; q < q1; ++q) {
     const int key = keys[q];
     if (key >= 0) {
@@ -222,14 +227,14 @@ __global__ __launch_bounds__(kPlanThreads) void csr_plan_kernel(PlanArgs p) {
   // hot slots in slot order
   const uint32_t word = t < kHotWords ? hot[t] : 0u;
   int Uh = 0;
-  int hid = block_scan(__popc(word), sc, &Uh);
+  int hid = block_scan<NW>(__popc(word), sc, &Uh);
   for (uint32_t w = word; w; w &= w - 1) p.hlist[lbase + hid++] = t * 32 + __ffs(w) - 1;
   __syncthreads();  // ids complete
 #pragma unroll
   for (int j = 0; j < kRowsPerWave; ++j) {
-    const int b = wave + j * kPlanWaves;
+    const int b = wave + j * NW;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < H; ++h) {
       const int c = cc[j][h];
       if (c == -1) continue;
       int out = c;
@@ -262,18 +267,23 @@ __global__ __launch_bounds__(kPlanThreads) void csr_link_kernel(PlanArgs p) {
   const int Uc = min(p.cnt[(int64_t(i) * K + k) * 2], kCMax);
   const int64_t lbase = seg + so[k];
   const int Up = k > 0 ? min(p.cnt[(int64_t(i) * K + k - 1) * 2], kCMax) : 0;
-  for (int q = t; q < kLinkTab; q += kPlanThreads) keys[q] = -1;
+  if (Uc == 0) return;
+  // a table of at least four times the previous step's columns (at most
+  // 2^kLinkBits, twice kCMax)
+  int bits = 6;
+  while (bits < kLinkBits && (1 << bits) < 4 * Up) ++bits;
+  for (int q = t; q < (1 << bits); q += kPlanThreads) keys[q] = -1;
   __syncthreads();
   if (k > 0) {
     const int64_t pbase = seg + so[k - 1];
     for (int u = t; u < Up; u += kPlanThreads) {
-      const int pos = table_insert(keys, kLinkBits, p.clist[pbase + u]);
+      const int pos = table_insert(keys, bits, p.clist[pbase + u]);
       if (pos >= 0) vals[pos] = u;  // columns are distinct within a step
     }
   }
   __syncthreads();
   for (int u = t; u < Uc; u += kPlanThreads) {
-    const int pos = k > 0 ? table_find(keys, kLinkBits, p.clist[lbase + u]) : -1;
+    const int pos = k > 0 ? table_find(keys, bits, p.clist[lbase + u]) : -1;
     p.clink[lbase + u] = pos >= 0 ? vals[pos] : -1;
   }
 }
@@ -623,14 +633,27 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   hipLaunchKernelGGL(step_scan_kernel, dim3(uint32_t(p.n)), dim3(1024), 0, s, p);
   // the largest step holds at most batch * max_row nonzeros
   const int64_t most = 2 * int64_t(std::min(p.batch, kFastRows)) * max_row;
-  if (most <= (1 << 10))
-    hipLaunchKernelGGL(csr_plan_kernel<10>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
-  else if (most <= (1 << 11))
-    hipLaunchKernelGGL(csr_plan_kernel<11>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
-  else if (most <= (1 << 12))
-    hipLaunchKernelGGL(csr_plan_kernel<12>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
-  else
-    hipLaunchKernelGGL(csr_plan_kernel<13>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  // rows of at most 64 nonzeros: one per lane and 256 threads (a small
+  // step leaves most of a larger block idle); else two and 512
+  if (max_row <= 64) {
+    if (most <= (1 << 10))
+      hipLaunchKernelGGL((csr_plan_kernel<10, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
+    else if (most <= (1 << 11))
+      hipLaunchKernelGGL((csr_plan_kernel<11, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
+    else if (most <= (1 << 12))
+      hipLaunchKernelGGL((csr_plan_kernel<12, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((csr_plan_kernel<13, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
+  } else {
+    if (most <= (1 << 10))
+      hipLaunchKernelGGL((csr_plan_kernel<10, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
+    else if (most <= (1 << 11))
+      hipLaunchKernelGGL((csr_plan_kernel<11, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
+    else if (most <= (1 << 12))
+      hipLaunchKernelGGL((csr_plan_kernel<12, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
+    else
+      hipLaunchKernelGGL((csr_plan_kernel<13, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  }
   hipLaunchKernelGGL(csr_link_kernel, dim3(blocks), dim3(kPlanThreads), 0, s, p);
   return hipGetLastError();
 }
