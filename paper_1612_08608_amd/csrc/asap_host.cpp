@@ -777,13 +777,19 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
   if (c->kind == kCsr) {
     SgdArgs a = sgd_args(c, p, c->plan[slot]);
     const bool planned = csr_plan_fits(a);
-    if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_start, s);
     if (planned) {
+      // the general kernel runs only if the plan says a step does not fit;
+      // it goes first, so that when it exits at once its launch does not
+      // queue behind the next round's planning (which starts at ev_start)
       const PlanArgs pa = plan_args(c, p, c->plan[slot]);
+      a.run_if = pa.flag;
+      if (e == hipSuccess) e = launch_sgd_csr(a, s);
+      if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_start, s);
       if (e == hipSuccess) e = launch_sgd_csr_fast(a, pa, s);
-      a.run_if = pa.flag;  // the general kernel runs only if the plan says a step does not fit
+    } else {
+      if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_start, s);
+      if (e == hipSuccess) e = launch_sgd_csr(a, s);
     }
-    if (e == hipSuccess) e = launch_sgd_csr(a, s);
     if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_used[slot], s);
     if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
     if (planned && c->ahead) {

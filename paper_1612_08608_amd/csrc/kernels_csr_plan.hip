@@ -103,10 +103,13 @@ __device__ __forceinline__ int block_scan(int v, int* sc, int* total) {
 
 // ----------------------------------------------------------------------------
 // step offsets: step_off[i][k] = nonzeros of worker i's steps before k, in
-// schedule order (stride S + 1 per worker); one 1024-thread block per worker
+// schedule order (stride S + 1 per worker); one 256-thread block per worker
+// (small enough to run beside an SGD pass that still holds the CUs)
 // ----------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void step_scan_kernel(PlanArgs p) {
-  __shared__ int sc[1024];
+constexpr int kScanThreads = 256;
+
+__global__ __launch_bounds__(kScanThreads) void step_scan_kernel(PlanArgs p) {
+  __shared__ int sc[kScanThreads];
   __shared__ int carry;
   const int i = blockIdx.x, t = threadIdx.x;
   const int64_t S = p.S;
@@ -115,7 +118,7 @@ __global__ __launch_bounds__(1024) void step_scan_kernel(PlanArgs p) {
   int32_t* so = p.step_off + int64_t(i) * (S + 1);
   if (t == 0) carry = 0;
   __syncthreads();
-  for (int base = 0; base < K; base += 1024) {
+  for (int base = 0; base < K; base += kScanThreads) {
     const int k = base + t;
     int tot = 0;
     if (k < K) {
@@ -125,7 +128,7 @@ __global__ __launch_bounds__(1024) void step_scan_kernel(PlanArgs p) {
     }
     sc[t] = tot;
     __syncthreads();
-    for (int o = 1; o < 1024; o <<= 1) {
+    for (int o = 1; o < kScanThreads; o <<= 1) {
       const int add = t >= o ? sc[t - o] : 0;
       __syncthreads();
       sc[t] += add;
@@ -133,7 +136,7 @@ __global__ __launch_bounds__(1024) void step_scan_kernel(PlanArgs p) {
     }
     if (k < K) so[k] = carry + sc[t] - tot;
     __syncthreads();
-    if (t == 0) carry += sc[1023];
+    if (t == 0) carry += sc[kScanThreads - 1];
     __syncthreads();
   }
   if (t == 0) so[K] = carry;
@@ -255,7 +258,8 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
 // ----------------------------------------------------------------------------
 // links: slot of each cold column of step k in step k-1, or -1
 // ----------------------------------------------------------------------------
-__global__ __launch_bounds__(kPlanThreads) void csr_link_kernel(PlanArgs p) {
+template <int NT>
+__global__ __launch_bounds__(NT) void csr_link_kernel(PlanArgs p) {
   __shared__ int keys[kLinkTab];
   __shared__ int vals[kLinkTab];
   const int K = p.K;
@@ -272,17 +276,17 @@ __global__ __launch_bounds__(kPlanThreads) void csr_link_kernel(PlanArgs p) {
   // 2^kLinkBits, twice kCMax)
   int bits = 6;
   while (bits < kLinkBits && (1 << bits) < 4 * Up) ++bits;
-  for (int q = t; q < (1 << bits); q += kPlanThreads) keys[q] = -1;
+  for (int q = t; q < (1 << bits); q += NT) keys[q] = -1;
   __syncthreads();
   if (k > 0) {
     const int64_t pbase = seg + so[k - 1];
-    for (int u = t; u < Up; u += kPlanThreads) {
+    for (int u = t; u < Up; u += NT) {
       const int pos = table_insert(keys, bits, p.clist[pbase + u]);
       if (pos >= 0) vals[pos] = u;  // columns are distinct within a step
     }
   }
   __syncthreads();
-  for (int u = t; u < Uc; u += kPlanThreads) {
+  for (int u = t; u < Uc; u += NT) {
     const int pos = k > 0 ? table_find(keys, bits, p.clist[lbase + u]) : -1;
     p.clink[lbase + u] = pos >= 0 ? vals[pos] : -1;
   }
@@ -630,7 +634,7 @@ bool csr_plan_fits(const SgdArgs& a) {
 
 hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   const uint32_t blocks = uint32_t(int64_t(p.n) * p.K);
-  hipLaunchKernelGGL(step_scan_kernel, dim3(uint32_t(p.n)), dim3(1024), 0, s, p);
+  hipLaunchKernelGGL(step_scan_kernel, dim3(uint32_t(p.n)), dim3(kScanThreads), 0, s, p);
   // the largest step holds at most batch * max_row nonzeros
   const int64_t most = 2 * int64_t(std::min(p.batch, kFastRows)) * max_row;
   // rows of at most 64 nonzeros: one per lane and 256 threads (a small
@@ -654,7 +658,10 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
     else
       hipLaunchKernelGGL((csr_plan_kernel<13, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
   }
-  hipLaunchKernelGGL(csr_link_kernel, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  if (max_row <= 64)
+    hipLaunchKernelGGL(csr_link_kernel<256>, dim3(blocks), dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL(csr_link_kernel<kPlanThreads>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
   return hipGetLastError();
 }
 
