@@ -76,7 +76,8 @@ struct asap_ctx {
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
-         off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dxcd = 0, off_dcount = 0, total = 0;
+         off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dxcd = 0, off_dcount = 0, off_progress = 0,
+         total = 0;
   RoundPlan plan[2];
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
@@ -154,6 +155,7 @@ void layout(asap_ctx* c) {
   c->off_code = o;    o = align_up(o + (csr ? size_t(c->nnz) * 4 : 0));
   c->off_lut = o;     o = align_up(o + (csr ? size_t(c->dim) * 2 : 0));
   c->off_hot = o;     o = align_up(o + (csr ? size_t(kHotMax) * 4 : 0));
+  c->off_progress = o; o = align_up(o + (csr ? n * 8 : 0));
   // per-round buffers of the CSR pass, twice: one entry per nonzero per list
   const size_t nz = csr ? size_t(c->nnz) : 0, nS = csr ? n * size_t(c->S) : 0;
   for (int k = 0; k < 2; ++k) {
@@ -589,7 +591,8 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
       (e = launch_fill_f32(at<float>(c, c->off_scale), int64_t(n), 1.0f, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err), 1, 0, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)) ||
-      (e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)))
+      (e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)) ||
+      (c->kind == kCsr && (e = launch_fill_i64(at<int64_t>(c, c->off_progress), int64_t(n), -1, s))))
     return hip_fail(c, e, "workspace init");
   if (c->kind == kDense && dense_wide_cpq(c->dim)) {
     // max |x| per shard (the fixed-point scale of the member exchange),
@@ -698,6 +701,10 @@ PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
   pa.hlist = at<int32_t>(c, rp.hlist);
   pa.cnt = at<int32_t>(c, rp.cnt);
   pa.flag = at<int32_t>(c, rp.flag);
+  pa.progress = at<int64_t>(c, c->off_progress);
+  // a prefetch workgroup per worker when both fit beside each other and
+  // worker i's pair lands on one XCD
+  pa.helpers = (c->n % 8 == 0 && 2 * c->n <= c->n_cu) ? 1 : 0;
   return pa;
 }
 

@@ -98,6 +98,8 @@ struct PlanArgs {
   int32_t* hlist;           // [nnz] distinct hot slots of each step
   int32_t* cnt;             // [n][S][2] distinct cold, hot per step
   int32_t* flag;            // [1] set when some step does not fit the fast kernel
+  int64_t* progress;        // [n] global step the pass of each worker is on (round * K + k)
+  int32_t helpers;          // 1: one prefetch workgroup per worker beside the pass
 };
 bool csr_plan_fits(const SgdArgs& a);
 hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s);

@@ -374,9 +374,74 @@ __device__ __forceinline__ void hold(float (&v)[N]) {
     asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7]));
 }
 
+constexpr uint32_t kPrefetchSpin = 1u << 16;  // polls of the pass's progress per step (bounded)
+constexpr int kPrefetchLead = 3;              // steps ahead of the pass
+
+// Prefetch workgroup of worker i (on the pass's XCD): what step k of the
+// pass reads -- its rows' (code, value) pairs, its lists and the model
+// entries of its cold columns -- is loaded into the XCD's L2 while the pass
+// is at step k - 2, one step before the pass loads it itself.  A random
+// 4-byte model read costs a whole line from memory, and one compute unit
+// only has so many in flight: the pass's step time was bound by them.  This
+// workgroup only loads (the values are discarded) and waits for the pass
+// with a bounded spin, so it cannot change any result.
+template <int E>
+__device__ void prefetch_pass(const SgdArgs& a, const PlanArgs& p, int i) {
+  const int tid = threadIdx.x, sub = tid & (kRowLanes - 1), b = tid / kRowLanes;
+  const int64_t K = (a.S + a.batch - 1) / a.batch;
+  const RowInfo* ri = a.rowinfo + int64_t(i) * a.S;
+  const long long seg = a.row_ptr[int64_t(i) * a.S];
+  const uint32_t nnz_w = uint32_t(a.row_ptr[int64_t(i + 1) * a.S] - seg);
+  const auto pk = rsrc(p.pack + seg, nnz_w * 8u);
+  const auto model = rsrc(a.models + int64_t(i) * a.ld, uint32_t(a.dim) * 4u);
+  const auto clist = rsrc(p.clist + seg, nnz_w * 4u);
+  const auto clink = rsrc(p.clink + seg, nnz_w * 4u);
+  const auto hlist = rsrc(p.hlist + seg, nnz_w * 4u);
+  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(K) * 4u);
+  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(K) * 8u);
+  const int64_t base = a.round * K;
+  float sink = 0.f;
+  for (int64_t k = 2; k < K; ++k) {
+    if (tid == 0) {
+      uint32_t spins = 0;
+      while (__hip_atomic_load(p.progress + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < base + k - kPrefetchLead &&
+             ++spins < kPrefetchSpin)
+        __builtin_amdgcn_s_sleep(4);
+    }
+    __syncthreads();
+    const int soff = ld_i32(so_v, uint32_t(k) * 4u);
+    const int uc = ld_i32(cn_v, uint32_t(k) * 8u), uh = ld_i32(cn_v, uint32_t(k) * 8u + 4u);
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < kColdPer; ++j) {
+      const int u = tid + j * kThreads;
+      if (u < uc) {
+        const int col = ld_i32(clist, uint32_t(soff + u) * 4u);
+        acc += ld_f32(model, uint32_t(col) * 4u) + float(ld_i32(clink, uint32_t(soff + u) * 4u));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kHotPer; ++j) {
+      const int u = tid + j * kThreads;
+      if (u < uh) acc += float(ld_i32(hlist, uint32_t(soff + u) * 4u));
+    }
+    if (b < a.batch && k * a.batch + b < a.S) {
+      const RowInfo r = ri[k * a.batch + b];
+      const uint32_t st = uint32_t(r.start - seg);
+      for (int e = sub; e < r.len; e += kRowLanes) acc += __int_as_float(ld_i32(pk, (st + uint32_t(e)) * 8u));
+    }
+    sink += acc;
+  }
+  asm volatile("" ::"v"(sink));
+}
+
 template <int E>
 __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanArgs p) {
   if (*p.flag) return;  // the general kernel takes this round
+  if (int(blockIdx.x) >= a.n) {
+    prefetch_pass<E>(a, p, int(blockIdx.x) - a.n);
+    return;
+  }
   __shared__ FastShared sh;
   const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane & (kRowLanes - 1);
@@ -475,6 +540,8 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   __syncthreads();
 
   for (int64_t k = 0; k < K; ++k) {
+    if (p.helpers && tid == 0)
+      __hip_atomic_store(p.progress + i, a.round * K + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (k > 0) {  // rotate what the previous step loaded
       d0 = d1;
       r1 = r2;
@@ -617,12 +684,17 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   if (tid == 0) {
     a.scale[i] = float(s);
     a.tag[i] = a.tag_value;
+    if (p.helpers)
+      __hip_atomic_store(p.progress + i, a.round * K + K, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
 template <int E>
 hipError_t launch_fast_e(const SgdArgs& a, const PlanArgs& p, hipStream_t s) {
-  hipLaunchKernelGGL((sgd_csr_fast_kernel<E>), dim3(uint32_t(a.n)), dim3(kThreads), 0, s, a, p);
+  // with helpers, block n + i prefetches for block i: the same XCD when n is
+  // a multiple of the 8 XCDs (blocks are dealt to them round-robin)
+  const uint32_t grid = uint32_t(a.n) * (p.helpers ? 2u : 1u);
+  hipLaunchKernelGGL((sgd_csr_fast_kernel<E>), dim3(grid), dim3(kThreads), 0, s, a, p);
   return hipGetLastError();
 }
 
