@@ -68,6 +68,10 @@ def graph_for(wl, d=None):
         p, i = asap.asap_graph_ring(wl.n_workers)
     elif wl.graph == "complete":
         p, i = asap.asap_graph_complete(wl.n_workers)
+    elif wl.graph == "root_expander":
+        p, i = asap.asap_graph_root_expander(wl.n_workers)
+    elif wl.graph == "chain":
+        p, i = asap.asap_graph_chain(wl.n_workers)
     else:
         p, i = asap.asap_graph_random_regular(wl.n_workers, wl.degree if d is None else d, wl.seed)
     return p, i, asap.asap_metropolis_weights(p, i)
@@ -170,6 +174,51 @@ def traffic_for(kernel_key, source):
     return ent["fetch_bytes"] + ent["write_bytes"]
 
 
+def converge(wl, rounds):
+    """Loss F(w_bar) after every round on three graphs of Figure 2 (all-reduce,
+    root expander, chain), and the bytes a worker sends per round (its
+    out-degree times the model), as in the convergence-versus-network-cost
+    comparisons of Section 6.  Synthetic data shaped like the workload, at
+    1/16 of its samples and dimension so that each graph runs in seconds."""
+    import torch
+    from paper_1612_08608_amd import asap, synth
+    wl = wl.with_(samples=max(wl.samples // 16, wl.batch), dim=max(wl.dim // 16, 64))
+    out = {"metric": "loss F(w_bar) per round and bytes sent per worker", "workload": wl.name,
+           "workers": wl.n_workers, "dim": wl.dim, "samples_per_worker": wl.samples, "graphs": {}}
+    if wl.features == "csr":
+        data = synth.csr_data(wl)
+    else:
+        data = synth.dense_data(wl)
+    for g in ("complete", "root_expander", "chain"):
+        gw = wl.with_(graph=g)
+        p, i, w = graph_for(gw)
+        sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
+        if wl.features == "csr":
+            sess.bind_csr(*data, wl.samples)
+        else:
+            sess.bind_dense(*data)
+        prm = asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, wl.batch, wl.seed)
+        losses, spread = [], []
+        for _ in range(rounds):
+            sess.round(prm)
+            m = sess.metrics(wl.loss, wl.l2)
+            losses.append(float(m[1]))
+            spread.append(float(m[2]))
+        st, _ = sess.check()
+        sess.close()
+        if st != asap.OK:
+            raise RuntimeError(f"epoch-tag check failed on {g}")
+        out_degree = int(p[1] - p[0]) - 1  # every builder here is regular
+        P = np.zeros((wl.n_workers, wl.n_workers))
+        for r in range(wl.n_workers):
+            P[r, i[p[r]:p[r + 1]]] = w[p[r]:p[r + 1]]
+        gap = 1.0 - float(np.linalg.svd(P, compute_uv=False)[1])
+        out["graphs"][g] = {"spectral_gap": gap, "out_degree": out_degree,
+                            "bytes_per_worker_per_round": out_degree * wl.dim * 4, "loss": losses,
+                            "consensus_distance": spread}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -179,6 +228,11 @@ def main():
                     choices=["sparse_lr_64w", "ring8_dense_lr", "sparse_svm_256w", "sparse_svm_256w_complete",
                              "dense_lr_32w", "mix_stress_1024w"])
     ap.add_argument("--degree", type=int, default=None, help="graph degree override (mixing stress)")
+    ap.add_argument("--graph", default=None, choices=["ring", "complete", "random_regular", "root_expander", "chain"],
+                    help="communication graph override")
+    ap.add_argument("--converge", type=int, default=0, metavar="ROUNDS",
+                    help="instead of timing: loss per round on the complete, root-expander and chain graphs "
+                         "(the workload at 1/16 of its samples and dimension), and the bytes each worker sends")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="GIB")
     args = ap.parse_args()
@@ -200,6 +254,11 @@ def main():
         wl = wl.with_(graph="complete")
     if args.degree:
         wl = wl.with_(degree=args.degree)
+    if args.graph:
+        wl = wl.with_(graph=args.graph)
+    if args.converge:
+        converge(wl, args.converge)
+        return
     p, i, w = graph_for(wl)
     log(f"[bench] workload {name}: n={wl.n_workers} D={wl.dim} S={wl.samples} B={wl.batch} "
         f"graph={wl.graph} d={wl.degree}")

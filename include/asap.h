@@ -94,6 +94,20 @@ typedef struct asap_sgd_params {
 /* Ring: N_in(i) = {i-1, i, i+1} mod n.  n >= 3.  nbr_ptr[n+1], nbr_idx[3n]. */
 asap_status asap_graph_ring(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx);
 
+/* Root expander (Figure 2(c); Section 3): every worker sends to its
+ * neighbour i+1, which keeps the graph connected, and to worker i+r with
+ * r = ceil(sqrt(n)), all mod n; so N_in(i) = {i-r, i-1, i} mod n, out- and
+ * in-degree 2 (the graph the paper evaluates).  The rounding of sqrt(n) is
+ * not stated; ceil is used.  n >= 3.  nbr_ptr[n+1], nbr_idx[3n]. */
+asap_status asap_graph_root_expander(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx);
+
+/* Chain (Figure 2(d)): worker i sends to i+1 only, wrapping around at the
+ * end (a directed ring), so N_in(i) = {i-1, i} mod n and P = A/2 is doubly
+ * stochastic; its gap 1 - cos(pi/n) is 0.0079 for 25 workers, the value
+ * Section 6 quotes for its 25-process chain.  n >= 2.  nbr_ptr[n+1],
+ * nbr_idx[2n]. */
+asap_status asap_graph_chain(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx);
+
 /* Complete graph (all-reduce): N_in(i) = all j.  1 <= n <= 46340.
  * nbr_ptr[n+1], nbr_idx[n*n]. */
 asap_status asap_graph_complete(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx);

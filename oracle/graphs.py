@@ -11,6 +11,10 @@ expander and chain topologies.
 Builders (the HIP library's host code implements the same rules on its own):
 
 * ring(n): in-neighbours of i are {i-1, i, i+1} mod n (n >= 3);
+* root_expander(n): i sends to i+1 and i+ceil(sqrt(n)) (Figure 2(c)), so its
+  in-neighbours are {i-ceil(sqrt(n)), i-1, i} mod n (n >= 3);
+* chain(n): i sends to i+1 with wrap-around (Figure 2(d) as a directed ring),
+  in-neighbours {i-1, i} (n >= 2);
 * complete(n): all j;
 * random_regular(n, d, seed): stub pairing on a SplitMix64 stream keyed by
   K(seed, GRAPH, n, d, 0).  Stubs = [v repeated d times for v ascending].  Draw
@@ -31,6 +35,7 @@ simple, connected, doubly stochastic), and a disconnected graph with gap 0.
 """
 from __future__ import annotations
 
+import math
 from collections import deque
 
 import numpy as np
@@ -53,6 +58,26 @@ def ring(n: int):
     if n < 3:
         raise ValueError("ring needs n >= 3")
     return _csr_from_sets([{(i - 1) % n, (i + 1) % n} for i in range(n)])
+
+
+def root_expander(n: int):
+    """Figure 2(c) / Section 3: i sends to i+1 and to i+r, r = ceil(sqrt(n)),
+    mod n; as in-neighbours: {i-r, i-1, i}.  The rounding of sqrt(n) is not
+    stated (reading: ceil)."""
+    if n < 3:
+        raise ValueError("root expander needs n >= 3")
+    r = math.isqrt(n)
+    if r * r < n:
+        r += 1
+    return _csr_from_sets([{(i - 1) % n, (i - r) % n} for i in range(n)])
+
+
+def chain(n: int):
+    """Figure 2(d): i sends to i+1 only; wrapped around (a directed ring) so
+    that P = A/2 is doubly stochastic.  In-neighbours {i-1, i}."""
+    if n < 2:
+        raise ValueError("chain needs n >= 2")
+    return _csr_from_sets([{(i - 1) % n} for i in range(n)])
 
 
 def complete(n: int):

@@ -27,7 +27,8 @@ ALLOW_NON_DS = 1
 
 # Every symbol include/asap.h declares.
 EXPORTS = (
-    "asap_graph_ring", "asap_graph_complete", "asap_graph_random_regular",
+    "asap_graph_ring", "asap_graph_root_expander", "asap_graph_chain", "asap_graph_complete",
+    "asap_graph_random_regular",
     "asap_metropolis_weights", "asap_schedule", "asap_create", "asap_workspace_size",
     "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr",
     "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_current",
@@ -62,6 +63,8 @@ def lib():
     p, i32, i64, u32, u64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_size_t
     sigs = {
         "asap_graph_ring": [i32, p, p],
+        "asap_graph_root_expander": [i32, p, p],
+        "asap_graph_chain": [i32, p, p],
         "asap_graph_complete": [i32, p, p],
         "asap_graph_random_regular": [i32, i32, u64, p, p],
         "asap_metropolis_weights": [i32, p, p, p],
@@ -135,6 +138,20 @@ def asap_graph_ring(n: int):
     ptr = np.zeros(n + 1, np.int32)
     idx = np.zeros(3 * max(n, 0), np.int32)
     _check(lib().asap_graph_ring(n, ptr.ctypes.data_as(C.c_void_p), idx.ctypes.data_as(C.c_void_p)))
+    return ptr, idx
+
+
+def asap_graph_root_expander(n: int):
+    ptr = np.zeros(n + 1, np.int32)
+    idx = np.zeros(3 * max(n, 0), np.int32)
+    _check(lib().asap_graph_root_expander(n, ptr.ctypes.data_as(C.c_void_p), idx.ctypes.data_as(C.c_void_p)))
+    return ptr, idx
+
+
+def asap_graph_chain(n: int):
+    ptr = np.zeros(n + 1, np.int32)
+    idx = np.zeros(2 * max(n, 0), np.int32)
+    _check(lib().asap_graph_chain(n, ptr.ctypes.data_as(C.c_void_p), idx.ctypes.data_as(C.c_void_p)))
     return ptr, idx
 
 

@@ -337,6 +337,41 @@ extern "C" asap_status asap_graph_ring(int32_t n, int32_t* nbr_ptr, int32_t* nbr
   return ASAP_OK;
 }
 
+namespace {
+int32_t ceil_sqrt(int32_t n) {
+  int32_t s = 0;
+  while (int64_t(s) * s < n) ++s;
+  return s;
+}
+}  // namespace
+
+extern "C" asap_status asap_graph_root_expander(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx) {
+  if (n < 3 || n > (1 << 28)) return fail(nullptr, ASAP_E_INVALID_ARG, "root expander needs 3 <= n <= 2^28");
+  if (!nbr_ptr || !nbr_idx) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL output");
+  const int32_t r = ceil_sqrt(n);  // 2 <= r < n, so i, i-1, i-r are distinct
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t v[3] = {i, (i + n - 1) % n, (i + n - r) % n};
+    std::sort(v, v + 3);
+    nbr_ptr[i] = 3 * i;
+    for (int k = 0; k < 3; ++k) nbr_idx[3 * i + k] = v[k];
+  }
+  nbr_ptr[n] = 3 * n;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_graph_chain(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx) {
+  if (n < 2 || n > (1 << 28)) return fail(nullptr, ASAP_E_INVALID_ARG, "chain needs 2 <= n <= 2^28");
+  if (!nbr_ptr || !nbr_idx) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL output");
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t a = (i + n - 1) % n;
+    nbr_ptr[i] = 2 * i;
+    nbr_idx[2 * i] = std::min(a, i);
+    nbr_idx[2 * i + 1] = std::max(a, i);
+  }
+  nbr_ptr[n] = 2 * n;
+  return ASAP_OK;
+}
+
 extern "C" asap_status asap_graph_complete(int32_t n, int32_t* nbr_ptr, int32_t* nbr_idx) {
   if (n < 1 || n > 46340) return fail(nullptr, ASAP_E_INVALID_ARG, "complete needs 1 <= n <= 46340");
   if (!nbr_ptr || !nbr_idx) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL output");

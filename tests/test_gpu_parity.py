@@ -39,6 +39,12 @@ def graph(kind, n, d=0, seed=0):
     elif kind == "complete":
         p, i = oracle.graphs.complete(n)
         lp, li = asap.asap_graph_complete(n)
+    elif kind == "root":
+        p, i = oracle.graphs.root_expander(n)
+        lp, li = asap.asap_graph_root_expander(n)
+    elif kind == "chain":
+        p, i = oracle.graphs.chain(n)
+        lp, li = asap.asap_graph_chain(n)
     else:
         p, i = oracle.graphs.random_regular(n, d, seed)
         lp, li = asap.asap_graph_random_regular(n, d, seed)
@@ -247,6 +253,12 @@ def test_csr_long_rows_and_large_batch_general_path(torch):
         _free_run(torch, wl, "complete", 0, 2, W0=W0)
 
 
+@pytest.mark.parametrize("kind", ["root", "chain"])
+def test_csr_logistic_on_directed_graphs(torch, kind):
+    wl = synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 13, samples=200)
+    _free_run(torch, wl, kind, 0, 4)
+
+
 def test_csr_single_sample_and_full_batch(torch):
     for S, B in ((1, 1), (37, 37), (37, 1)):
         wl = synth.SPARSE_LR_64W.with_(n_workers=3, dim=300, samples=S, batch=B, nnz_mean=10.0)
@@ -436,6 +448,9 @@ REDUCE_SHAPES = [
     (1024, "random", 2, 67), (16, "path", 0, 1003), (128, "chords", 0, 999),
     (100, "random", 4, 777), (64, "random", 20, 1001), (64, "star", 0, 300),
     (3, "ring", 2, 5),
+    # Figure 2's directed topologies (P not symmetric): root expander and chain
+    (64, "root", 0, 1029), (25, "root", 0, 517), (1024, "root", 0, 70), (6, "chain", 0, 301),
+    (1024, "chain", 0, 66),
 ]
 
 

@@ -38,6 +38,18 @@ def test_ring_bit_identical(n):
     assert np.array_equal(p, po) and np.array_equal(i, io)
 
 
+@pytest.mark.parametrize("n", [3, 4, 6, 25, 64, 1000, 1024])
+def test_root_expander_and_chain_bit_identical(n):
+    p, i = asap.asap_graph_root_expander(n)
+    op, oi = oracle.graphs.root_expander(n)
+    assert np.array_equal(p, op) and np.array_equal(i, oi)
+    assert np.array_equal(asap.asap_metropolis_weights(p, i).view(np.uint32),
+                          oracle.graphs.metropolis_weights(op, oi).view(np.uint32))
+    p, i = asap.asap_graph_chain(n)
+    op, oi = oracle.graphs.chain(n)
+    assert np.array_equal(p, op) and np.array_equal(i, oi)
+
+
 @pytest.mark.parametrize("n", [1, 2, 3, 7, 256])
 def test_complete_bit_identical(n):
     p, i = asap.asap_graph_complete(n)
@@ -80,6 +92,7 @@ def test_schedule_bit_identical(S):
 
 def test_builder_argument_errors():
     for call in (lambda: asap.asap_graph_ring(2), lambda: asap.asap_graph_complete(0),
+                 lambda: asap.asap_graph_root_expander(2), lambda: asap.asap_graph_chain(1),
                  lambda: asap.asap_graph_random_regular(5, 3, 0), lambda: asap.asap_graph_random_regular(4, 4, 0),
                  lambda: asap.asap_graph_random_regular(6, 1, 0),
                  lambda: asap.asap_schedule(-1, 0, 0, 0)):

@@ -50,6 +50,61 @@ def test_complete_graph_gap_is_figure2_allreduce(golden_dir):
     assert not any(r[2] for k, r in rows.items() if k != "all-reduce")
 
 
+def _circulant_gap(n, offsets):
+    # P = (1/m) sum_o Z^o with Z the cyclic shift: eigenvalues
+    # (1/m) sum_o exp(2 pi i k o / n), P normal, so its singular values are
+    # their moduli and the gap is 1 - max_{k != 0} |lambda_k|.
+    k = np.arange(1, n)[:, None]
+    lam = np.exp(2j * np.pi * k * np.asarray(offsets)[None, :] / n).sum(axis=1) / len(offsets)
+    return 1.0 - float(np.abs(lam).max())
+
+
+@pytest.mark.parametrize("n", [3, 4, 6, 25, 64, 100, 1024])
+def test_root_expander_structure_and_spectrum(n):
+    ptr, idx = graphs.root_expander(n)
+    r = math.ceil(math.sqrt(n))
+    assert ptr.tolist() == [3 * i for i in range(n + 1)]
+    for i in range(n):
+        assert idx[3 * i:3 * i + 3].tolist() == sorted({i, (i - 1) % n, (i - r) % n})
+    # every worker is read by exactly three rows: out-degree 2 plus itself
+    assert np.bincount(idx, minlength=n).tolist() == [3] * n
+    w = graphs.metropolis_weights(ptr, idx)
+    assert np.all(w == np.float32(1.0 / 3.0))
+    P = _P(ptr, idx, w)
+    assert np.allclose(P.sum(axis=0), 1.0, atol=4 * F32_EPS)
+    assert abs(graphs.spectral_gap(P) - _circulant_gap(n, [0, 1, r])) < 16 * F32_EPS
+
+
+@pytest.mark.parametrize("n", [2, 3, 6, 25, 64, 1000])
+def test_chain_structure_and_closed_form_gap(n):
+    ptr, idx = graphs.chain(n)
+    assert ptr.tolist() == [2 * i for i in range(n + 1)]
+    for i in range(n):
+        assert idx[2 * i:2 * i + 2].tolist() == sorted({i, (i - 1) % n})
+    w = graphs.metropolis_weights(ptr, idx)
+    assert np.all(w == np.float32(0.5))
+    # (I + Z)/2 has singular values |cos(pi k / n)|
+    want = 1.0 - math.cos(math.pi / n) if n > 2 else 1.0
+    assert abs(graphs.spectral_gap(_P(ptr, idx, w)) - want) < 16 * F32_EPS
+
+
+def test_chain_gap_matches_section6(golden_dir):
+    with open(os.path.join(golden_dir, "sec6_chain_gap.txt")) as f:
+        rows = [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+    (name, nodes, gap), = rows
+    assert name == "chain"
+    ptr, idx = graphs.chain(int(nodes))
+    got = graphs.spectral_gap(_P(ptr, idx))
+    assert round(got, 3) == float(gap), got
+
+
+def test_sparser_graphs_have_smaller_gaps():
+    # Section 3: more edges, higher spectral gap (complete > root > chain)
+    for n in (25, 64, 256):
+        gaps = [graphs.spectral_gap(_P(*g(n))) for g in (graphs.complete, graphs.root_expander, graphs.chain)]
+        assert gaps[0] > gaps[1] > gaps[2] > 0.0
+
+
 def test_complete_graph_weights_uniform():
     for n in (1, 2, 4, 256):
         ptr, idx = graphs.complete(n)
