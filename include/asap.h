@@ -69,8 +69,15 @@ enum { ASAP_ALLOW_NON_DS = 1u /* accept weights that are not doubly stochastic *
  *  lr_kind  ASAP_LR_*;   eta_t = lr0 or lr0 / sqrt(t)
  *  lr0      > 0, finite
  *  l2       >= 0, finite; the (l2/2)||w||^2 term of every f_i
- *  batch    minibatch size B >= 1; the pass takes ceil(S/B) steps, the last
- *           one over the S mod B remaining samples when B does not divide S
+ *  batch    minibatch size B >= 1; the pass takes K = ceil(S/B) steps, the
+ *           last one over the S mod B remaining samples when B does not
+ *           divide S
+ *  local_steps  0: a round's half-step is one full pass (K steps).  L >= 1
+ *           dividing K: L steps; the steps of all rounds are the passes one
+ *           after the other, so round r runs steps k0 .. k0 + L - 1 of pass
+ *           q with q = (r L) div K, k0 = (r L) mod K, pass q in the order of
+ *           asap_schedule(S, seed, i, q), and t = q K + k + 1.  L = 1 is
+ *           (A.2) as printed: one gradient step, then the mix.
  *  seed     seed of the sample schedule (see asap_schedule)              */
 typedef struct asap_sgd_params {
   int32_t loss;
@@ -78,7 +85,7 @@ typedef struct asap_sgd_params {
   float lr0;
   float l2;
   int32_t batch;
-  int32_t reserved; /* must be 0 */
+  int32_t local_steps;
   uint64_t seed;
 } asap_sgd_params;
 

@@ -17,7 +17,12 @@ step-size schedule; these come from the workload definitions):
   (1/B') sum_b c_b x_b + l2 w; the update is w <- w - eta_t g with
   t = r * ceil(S / B) + k + 1 counted from 1 per worker across rounds, and
   eta_t = lr0 (constant) or lr0 / sqrt(t);
-* one round = one full pass over the shard.
+* one round = one full pass over the shard (local_steps = 0), or L
+  minibatch steps of the sequence of passes (local_steps = L, L dividing the
+  number of steps K of a pass; L = 1 is (A.2) as printed, one gradient step
+  per mix): round r takes steps k0 .. k0 + L - 1 of pass q, with
+  q = (r L) div K and k0 = (r L) mod K (`round_steps`), and t counts
+  q K + k + 1.
 
 Pins: closed forms at m = 0, central finite differences of the loss on tiny
 inputs, a hand-computed step, the dense-vs-CSR agreement on the same data.
@@ -66,17 +71,30 @@ def n_steps(S: int, B: int) -> int:
     return -(-S // B)
 
 
-def sgd_pass_dense(w0, X, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd):
+def round_steps(rnd: int, local_steps: int, K: int):
+    """(pass q, first step k0, end step k1) of round rnd: the whole pass
+    when local_steps == 0, else local_steps steps (which must divide K)."""
+    if local_steps == 0:
+        return rnd, 0, K
+    if local_steps < 0 or K % local_steps:
+        raise ValueError("local_steps must divide the steps of a pass")
+    g = rnd * local_steps
+    return g // K, g % K, g % K + local_steps
+
+
+def sgd_pass_dense(w0, X, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd, steps=None):
     """One local pass of one worker on dense data; returns the new model (fp64).
 
-    w0 [D], X [S, D], y [S], sched = permutation of [0, S).
+    w0 [D], X [S, D], y [S], sched = permutation of [0, S) (of pass rnd);
+    steps = (k0, k1) runs only steps k0 .. k1 - 1 of the pass.
     """
     w = np.asarray(w0, np.float64).copy()
     X = np.asarray(X, np.float64)
     y = np.asarray(y, np.float64)
     S = X.shape[0]
     K = n_steps(S, batch)
-    for k in range(K):
+    k0, k1 = (0, K) if steps is None else steps
+    for k in range(k0, k1):
         rows = sched[k * batch:min((k + 1) * batch, S)]
         xb, yb = X[rows], y[rows]
         m = xb @ w
@@ -87,7 +105,7 @@ def sgd_pass_dense(w0, X, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd):
 
 
 def sgd_pass_csr(w0, row_ptr, col, val, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd,
-                 ambiguous=None):
+                 ambiguous=None, steps=None):
     """One local pass of one worker on CSR data (local row offsets); fp64.
 
     The L2 term is applied densely every step, exactly as the update states.
@@ -99,7 +117,8 @@ def sgd_pass_csr(w0, row_ptr, col, val, y, sched, *, batch, loss, lr_kind, lr0, 
     row_ptr = np.asarray(row_ptr, np.int64)
     S = len(row_ptr) - 1
     K = n_steps(S, batch)
-    for k in range(K):
+    k0, k1 = (0, K) if steps is None else steps
+    for k in range(k0, k1):
         rows = np.asarray(sched[k * batch:min((k + 1) * batch, S)], np.int64)
         lo, lens = row_ptr[rows], row_ptr[rows + 1] - row_ptr[rows]
         seg = np.repeat(np.arange(len(rows)), lens)               # pair -> position in batch

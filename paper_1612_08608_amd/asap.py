@@ -45,7 +45,7 @@ class AsapError(RuntimeError):
 
 class SgdParams(C.Structure):
     _fields_ = [("loss", C.c_int32), ("lr_kind", C.c_int32), ("lr0", C.c_float),
-                ("l2", C.c_float), ("batch", C.c_int32), ("reserved", C.c_int32),
+                ("l2", C.c_float), ("batch", C.c_int32), ("local_steps", C.c_int32),
                 ("seed", C.c_uint64)]
 
 
@@ -219,8 +219,8 @@ def asap_bind_csr(ctx, row_ptr, col, val, y, samples: int, nnz: int, stream=None
                                _stream(stream)), ctx)
 
 
-def sgd_params(loss="logistic", lr_kind="const", lr0=0.1, l2=0.0, batch=1, seed=0) -> SgdParams:
-    return SgdParams(LOSS.get(loss, loss), LR.get(lr_kind, lr_kind), lr0, l2, batch, 0, seed)
+def sgd_params(loss="logistic", lr_kind="const", lr0=0.1, l2=0.0, batch=1, seed=0, local_steps=0) -> SgdParams:
+    return SgdParams(LOSS.get(loss, loss), LR.get(lr_kind, lr_kind), lr0, l2, batch, local_steps, seed)
 
 
 def asap_local_sgd(ctx, params: SgdParams, stream=None):

@@ -88,24 +88,25 @@ struct asap_ctx {
   bool half_scaled = false;  // the half-step left per-worker L2 scales to fold
   bool tags_ready = false;
 
-  // look-ahead planning of the CSR pass: after launching round r, the plan
-  // of round r + 1 (same seed and batch) is built on a stream of the
-  // library's own into the other RoundPlan; the next call uses it when its
-  // round, seed and batch match
+  // look-ahead planning of the CSR pass: after launching the last steps of
+  // pass q, the plan of pass q + 1 (same seed and batch) is built on a
+  // stream of the library's own into the other RoundPlan; a later call uses
+  // it when its pass, seed and batch match
   hipStream_t ahead = nullptr;
   hipEvent_t ev_start = nullptr, ev_ready[2] = {nullptr, nullptr}, ev_used[2] = {nullptr, nullptr};
   bool ahead_valid = false;
   int ahead_slot = 0;
   uint64_t ahead_seed = 0;
-  int64_t ahead_round = -1;
+  int64_t ahead_pass = -1;
   int32_t ahead_batch = 0;
 
   // the half-step inputs enqueued by asap_prepare_sgd (or by asap_local_sgd
-  // itself): which RoundPlan holds them and for which round, seed and batch
+  // itself): which RoundPlan holds them and for which pass, seed and batch
+  // (they serve every round whose steps lie in that pass)
   bool prep_valid = false;
   int prep_slot = 0;
   uint64_t prep_seed = 0;
-  int64_t prep_round = -1;
+  int64_t prep_pass = -1;
   int32_t prep_batch = 0;
 
   std::string err;
@@ -279,7 +280,13 @@ asap_status check_params(asap_ctx* c, const asap_sgd_params* p) {
   if (p->batch < 1) return fail(c, ASAP_E_INVALID_ARG, "batch must be >= 1");
   if (c->kind == kCsr && p->batch > 512)
     return fail(c, ASAP_E_INVALID_ARG, "CSR minibatch is limited to 512 rows");
-  if (p->reserved != 0) return fail(c, ASAP_E_INVALID_ARG, "reserved must be 0");
+  if (p->local_steps < 0) return fail(c, ASAP_E_INVALID_ARG, "local_steps must be >= 0");
+  if (p->local_steps > 0) {
+    const int64_t K = (c->S + p->batch - 1) / p->batch;
+    if (K % p->local_steps)
+      return fail(c, ASAP_E_INVALID_ARG, "local_steps %d does not divide the %lld steps of a pass", p->local_steps,
+                  (long long)K);
+  }
   return ASAP_OK;
 }
 
@@ -707,7 +714,21 @@ SgdArgs sgd_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
   a.lr0 = p->lr0;
   a.l2 = p->l2;
   a.batch = p->batch;
-  a.round = c->round;
+  {
+    // steps of this round: the whole pass round, or local_steps steps of
+    // the sequence of passes
+    const int64_t K = (c->S + p->batch - 1) / p->batch;
+    if (p->local_steps == 0) {
+      a.round = c->round;
+      a.k0 = 0;
+      a.k1 = K;
+    } else {
+      const int64_t g = c->round * p->local_steps;
+      a.round = g / K;
+      a.k0 = g % K;
+      a.k1 = a.k0 + p->local_steps;
+    }
+  }
   a.scale = at<float>(c, c->off_scale);
   a.tag = at<int64_t>(c, c->off_tag) + size_t(c->cur) * c->n;
   a.tag_value = tag_half(c->round);
@@ -759,17 +780,19 @@ hipError_t prepare_csr_round(asap_ctx* c, const asap_sgd_params* p, int64_t roun
   return e;
 }
 
-// The current round's half-step inputs on stream s (the schedule; for CSR
-// also the row descriptors and the plan), unless already enqueued for this
-// round, seed and batch.  A CSR round planned ahead by the previous
-// asap_local_sgd is waited for instead of planned again.
+// The current round's half-step inputs on stream s (the schedule of its
+// pass; for CSR also the row descriptors and the plan), unless already
+// enqueued for this pass, seed and batch (they then serve every round of the
+// pass).  A CSR pass planned ahead by asap_local_sgd is waited for instead
+// of planned again.
 hipError_t prepare_half_step(asap_ctx* c, const asap_sgd_params* p, hipStream_t s) {
-  if (c->prep_valid && c->prep_round == c->round && c->prep_seed == p->seed && c->prep_batch == p->batch)
+  const int64_t pass = sgd_args(c, p, c->plan[0]).round;
+  if (c->prep_valid && c->prep_pass == pass && c->prep_seed == p->seed && c->prep_batch == p->batch)
     return hipSuccess;
   hipError_t e = hipSuccess;
-  int slot = 0;
+  int slot = c->prep_valid ? c->prep_slot : 0;  // a replaced plan is rewritten in place
   if (c->kind == kCsr) {
-    const bool hit = c->ahead_valid && c->ahead_round == c->round && c->ahead_seed == p->seed &&
+    const bool hit = c->ahead_valid && c->ahead_pass == pass && c->ahead_seed == p->seed &&
                      c->ahead_batch == p->batch;
     if (c->ahead_valid) {
       slot = c->ahead_slot;
@@ -777,13 +800,13 @@ hipError_t prepare_half_step(asap_ctx* c, const asap_sgd_params* p, hipStream_t 
     }
     c->ahead_valid = false;
     const bool planned = csr_plan_fits(sgd_args(c, p, c->plan[slot]));
-    if (e == hipSuccess && !hit) e = prepare_csr_round(c, p, c->round, c->plan[slot], planned, s);
+    if (e == hipSuccess && !hit) e = prepare_csr_round(c, p, pass, c->plan[slot], planned, s);
   } else {
-    e = launch_schedule(p->seed, c->round, c->n, c->S, at<int32_t>(c, c->plan[0].sched), s);
+    e = launch_schedule(p->seed, pass, c->n, c->S, at<int32_t>(c, c->plan[0].sched), s);
   }
   c->prep_valid = e == hipSuccess;
   c->prep_slot = slot;
-  c->prep_round = c->round;
+  c->prep_pass = pass;
   c->prep_seed = p->seed;
   c->prep_batch = p->batch;
   return e;
@@ -815,10 +838,10 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
   hipError_t e = prepare_half_step(c, p, s);
   if (e != hipSuccess) return hip_fail(c, e, "half-step preparation");
   const int slot = c->prep_slot;
-  c->prep_valid = false;
   if (c->kind == kCsr) {
     SgdArgs a = sgd_args(c, p, c->plan[slot]);
     const bool planned = csr_plan_fits(a);
+    const bool pass_ends = a.k1 == (c->S + p->batch - 1) / p->batch;
     if (planned) {
       // the general kernel runs only if the plan says a step does not fit;
       // it goes first, so that when it exits at once its launch does not
@@ -834,21 +857,21 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
     }
     if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_used[slot], s);
     if (e != hipSuccess) return hip_fail(c, e, "SGD kernel");
-    if (planned && c->ahead) {
-      // plan the next round into the other slot, concurrently with this
-      // pass: after this call's inputs are ready (ev_start) and after the
+    if (planned && pass_ends && c->ahead) {
+      // plan the next pass into the other slot, concurrently with this
+      // launch: after this call's inputs are ready (ev_start) and after the
       // slot's last reader (ev_used).  With fewer workers than compute
-      // units it runs beside the pass; otherwise it fills the pass's tail
-      // and overlaps the reduce.
+      // units it runs beside the launch; otherwise it fills its tail and
+      // overlaps the reduce.
       const int o = slot ^ 1;
       if ((e = hipStreamWaitEvent(c->ahead, c->ev_start, 0)) || (e = hipStreamWaitEvent(c->ahead, c->ev_used[o], 0)) ||
-          (e = prepare_csr_round(c, p, c->round + 1, c->plan[o], true, c->ahead)) ||
+          (e = prepare_csr_round(c, p, a.round + 1, c->plan[o], true, c->ahead)) ||
           (e = hipEventRecord(c->ev_ready[o], c->ahead)))
         return hip_fail(c, e, "look-ahead planning");
       c->ahead_valid = true;
       c->ahead_slot = o;
       c->ahead_seed = p->seed;
-      c->ahead_round = c->round + 1;
+      c->ahead_pass = a.round + 1;
       c->ahead_batch = p->batch;
     }
   } else {

@@ -71,7 +71,8 @@ struct SgdArgs {
   int32_t loss, lr_kind;
   float lr0, l2;
   int32_t batch;
-  int64_t round;
+  int64_t round;    // the pass the steps belong to: step k has t = round * K + k + 1
+  int64_t k0, k1;   // steps [k0, k1) of that pass run in this launch (K = ceil(S / batch))
   float* scale;     // [n] out: final L2 scale (CSR)
   int64_t* tag;     // [n] tags of the current buffer
   int64_t tag_value;

@@ -241,20 +241,23 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
   RowInfo r2, r3;
   DataReg<E> d0, d1, d2;
   float vg0[E], vg1[E];
+  // this launch runs steps [k0, kend) of the pass; loads past kend are
+  // void like those past the pass
+  const int64_t k0 = a.k0, kend = a.k1;
   if (PIPE) {
-    const RowInfo ra = load_row(a, ri, 0, K, brow), rb = load_row(a, ri, 1, K, brow);
-    r2 = load_row(a, ri, 2, K, brow);
+    const RowInfo ra = load_row(a, ri, k0, kend, brow), rb = load_row(a, ri, k0 + 1, kend, brow);
+    r2 = load_row(a, ri, k0 + 2, kend, brow);
     __syncthreads();
-    load_data<E>(w, ra, row_valid(a, 0, K, brow), sub, d0);
-    load_data<E>(w, rb, row_valid(a, 1, K, brow), sub, d1);
+    load_data<E>(w, ra, row_valid(a, k0, kend, brow), sub, d0);
+    load_data<E>(w, rb, row_valid(a, k0 + 1, kend, brow), sub, d1);
     __syncthreads();
     gather_cold<E>(w, d0, vg0);
-    count_stats<E>(sh, 0, d0, sub);
+    count_stats<E>(sh, int(k0 % 3), d0, sub);
   }
   __syncthreads();
 
-  for (int64_t k = 0; k < K; ++k) {
-    if (PIPE && k > 0) {  // rotate what the previous step loaded
+  for (int64_t k = k0; k < kend; ++k) {
+    if (PIPE && k > k0) {  // rotate what the previous step loaded
       d0 = d1;
       d1 = d2;
       r2 = r3;
@@ -273,8 +276,8 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
 
     if (fast) {
       // prefetch: row descriptors of k+3, nonzeros of k+2, cold entries of k+1
-      r3 = load_row(a, ri, k + 3, K, brow);
-      load_data<E>(w, r2, row_valid(a, k + 2, K, brow), sub, d2);
+      r3 = load_row(a, ri, k + 3, kend, brow);
+      load_data<E>(w, r2, row_valid(a, k + 2, kend, brow), sub, d2);
       gather_cold<E>(w, d1, vg1);
       count_stats<E>(sh, int((k + 1) % 3), d1, sub);
 
@@ -365,11 +368,11 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
         prev.acc[q] = 0ull;
       }
       if (PIPE) {  // re-prime the pipeline for step k+1 (this step's stores are visible)
-        const RowInfo ra = load_row(a, ri, k + 1, K, brow), rb = load_row(a, ri, k + 2, K, brow);
-        r3 = load_row(a, ri, k + 3, K, brow);
+        const RowInfo ra = load_row(a, ri, k + 1, kend, brow), rb = load_row(a, ri, k + 2, kend, brow);
+        r3 = load_row(a, ri, k + 3, kend, brow);
         __syncthreads();
-        load_data<E>(w, ra, row_valid(a, k + 1, K, brow), sub, d1);
-        load_data<E>(w, rb, row_valid(a, k + 2, K, brow), sub, d2);
+        load_data<E>(w, ra, row_valid(a, k + 1, kend, brow), sub, d1);
+        load_data<E>(w, rb, row_valid(a, k + 2, kend, brow), sub, d2);
         __syncthreads();
         gather_cold<E>(w, d1, vg1);
         count_stats<E>(sh, int((k + 1) % 3), d1, sub);

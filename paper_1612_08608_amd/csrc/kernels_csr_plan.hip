@@ -397,11 +397,11 @@ __device__ void prefetch_pass(const SgdArgs& a, const PlanArgs& p, int i) {
   const auto clist = rsrc(p.clist + seg, nnz_w * 4u);
   const auto clink = rsrc(p.clink + seg, nnz_w * 4u);
   const auto hlist = rsrc(p.hlist + seg, nnz_w * 4u);
-  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(K) * 4u);
-  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(K) * 8u);
+  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(a.k1) * 4u);
+  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(a.k1) * 8u);
   const int64_t base = a.round * K;
   float sink = 0.f;
-  for (int64_t k = 2; k < K; ++k) {
+  for (int64_t k = a.k0 + 2; k < a.k1; ++k) {
     if (tid == 0) {
       uint32_t spins = 0;
       while (__hip_atomic_load(p.progress + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < base + k - kPrefetchLead &&
@@ -450,6 +450,7 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   const RowInfo* ri = a.rowinfo + int64_t(i) * a.S;
   const int H = a.n_hot;
   const int64_t K = (a.S + a.batch - 1) / a.batch;
+  const int64_t k0 = a.k0, kend = a.k1;  // steps [k0, kend) of the pass run here
   Views w;
   w.seg = a.row_ptr[int64_t(i) * a.S];
   const uint32_t nnz_w = uint32_t(a.row_ptr[int64_t(i + 1) * a.S] - w.seg);
@@ -458,8 +459,8 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   const auto clist = rsrc(p.clist + w.seg, nnz_w * 4u);
   const auto clink = rsrc(p.clink + w.seg, nnz_w * 4u);
   const auto hlist = rsrc(p.hlist + w.seg, nnz_w * 4u);
-  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(K) * 4u);  // steps >= K read 0
-  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(K) * 8u);
+  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(a.k1) * 4u);  // steps past the launch read 0
+  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(a.k1) * 8u);
 
   for (int h = tid; h < H; h += kThreads) {
     sh.vhot[h] = vrow[a.hot_cols[h]];
@@ -520,16 +521,16 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
     }
   };
   {
-    const RowInfo ra = load_row(a, ri, 0, K, brow);
-    r1 = load_row(a, ri, 1, K, brow);
-    m0 = load_meta(so_v, cn_v, 0, lane);
-    m1 = load_meta(so_v, cn_v, 1, lane);
-    m2 = load_meta(so_v, cn_v, 2, lane);
+    const RowInfo ra = load_row(a, ri, k0, kend, brow);
+    r1 = load_row(a, ri, k0 + 1, kend, brow);
+    m0 = load_meta(so_v, cn_v, k0, lane);
+    m1 = load_meta(so_v, cn_v, k0 + 1, lane);
+    m2 = load_meta(so_v, cn_v, k0 + 2, lane);
     m0 = uniform(m0);
     m1 = uniform(m1);
     m2 = uniform(m2);
     __syncthreads();
-    load_packed<E>(pk, w.seg, ra, row_valid(a, 0, K, brow), sub, d0);
+    load_packed<E>(pk, w.seg, ra, row_valid(a, k0, kend, brow), sub, d0);
     load_cols(m0, cl0);
     load_links(m0, lk0);
     load_cols(m1, cl1);
@@ -539,10 +540,10 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   }
   __syncthreads();
 
-  for (int64_t k = 0; k < K; ++k) {
+  for (int64_t k = k0; k < kend; ++k) {
     if (p.helpers && tid == 0)
       __hip_atomic_store(p.progress + i, a.round * K + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (k > 0) {  // rotate what the previous step loaded
+    if (k > k0) {  // rotate what the previous step loaded
       d0 = d1;
       r1 = r2;
       m0 = m1;
@@ -566,20 +567,21 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
     float* cv = sh.cval[k & 1];
     const float* cvp = sh.cval[(k + 1) & 1];
 
-    // cold values of this step: changed by the previous step -> its slot,
-    // else the value gathered a step ago
+    // cold values of this step: changed by the previous step of this
+    // launch -> its slot, else the value gathered a step ago (the first step
+    // of a launch gathers them all: the launch before wrote them back)
 #pragma unroll
     for (int j = 0; j < kColdPer; ++j) {
       const int u = tid + j * kThreads;
-      if (u < m0.uc) cv[u] = (k > 0 && lk0[j] >= 0) ? cvp[lk0[j]] : g0[j];
+      if (u < m0.uc) cv[u] = (k > k0 && lk0[j] >= 0) ? cvp[lk0[j]] : g0[j];
     }
     lds_barrier();
     // prefetch, issued after the barrier so that the address work of some
     // waves overlaps the LDS work of others: nonzeros, links, hot slots and
     // values of k+1, row and columns of k+2
     load_hot(m1, hl1);
-    load_packed<E>(pk, w.seg, r1, row_valid(a, k + 1, K, brow), sub, d1);
-    r2 = load_row(a, ri, k + 2, K, brow);
+    load_packed<E>(pk, w.seg, r1, row_valid(a, k + 1, kend, brow), sub, d1);
+    r2 = load_row(a, ri, k + 2, kend, brow);
     m3 = load_meta(so_v, cn_v, k + 3, lane);
     gather(m1, cl1, g1);
     load_links(m1, lk1);
@@ -685,7 +687,7 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
     a.scale[i] = float(s);
     a.tag[i] = a.tag_value;
     if (p.helpers)
-      __hip_atomic_store(p.progress + i, a.round * K + K, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.progress + i, a.round * K + kend, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 

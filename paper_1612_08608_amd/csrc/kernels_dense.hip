@@ -171,6 +171,7 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
 
   const int B = a.batch, S = int(a.S);  // S < 2^31 (checked at bind)
   const int KS = (S + B - 1) / B;
+  const int K0 = int(a.k0), KE = int(a.k1);  // steps [K0, KE) of the pass run here
   // valid components of the thread's last float4 of each q (entries of X
   // past dim are never used)
   int nv[CPQ];
@@ -197,9 +198,9 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     hi_ = b0 + (last ? last1 : off1);
   };
   auto settle = [&](Pos p) {  // move past steps in which this member has no samples
-    while (p.t < KS && p.sb >= p.hi) {
+    while (p.t < KE && p.sb >= p.hi) {
       ++p.t;
-      if (p.t < KS) {
+      if (p.t < KE) {
         share(p.t, p.lo, p.hi);
         p.sb = p.lo;
       }
@@ -211,13 +212,13 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   // load and writing it to slot t & 1.
   int pi = 0;
   auto fetch = [&](int t) {
-    if (t >= KS) return;
+    if (t >= KE) return;
     int lo_, hi_;
     share(t, lo_, hi_);
     if (tid < hi_ - lo_) pi = si[lo_ + tid];
   };
   auto stage = [&](int t) {
-    if (t >= KS) return;
+    if (t >= KE) return;
     int lo_, hi_;
     share(t, lo_, hi_);
     if (tid < hi_ - lo_) ridx[t & 1][tid] = pi;
@@ -369,7 +370,7 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     }
     during();
     if (K > 1) {
-      if (!gather(uint32_t(K) * uint32_t(t + 2))) return false;
+      if (!gather(uint32_t(K) * uint32_t(t - K0 + 2))) return false;
       // ... and every member sums all K partials in fp64 in member order,
       // so all members get the same gradient bit for bit.  Members on one
       // XCD meet in its L2 (loads that bypass only the CU's L1); otherwise
@@ -423,10 +424,10 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
   float4 xa[SR][CPQ], xb[SR][CPQ];
   float ya = 0.f, yb = 0.f;
   bool ok = true;
-  int done = 0;  // steps finished
+  int done = K0;  // steps finished
   // Whether all members of the worker run on this XCD: they publish their
   // XCD and meet once before the first step (count K; step t meets at
-  // K (t + 2)).
+  // K (t - K0 + 2)).
   if (K > 1) {
     const int me = xcd_id();
     if (tid == 0) __hip_atomic_store(ds.xcd + i * K + k, me, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -436,19 +437,19 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     for (int m = 0; m < K; ++m)
       local = local && __hip_atomic_load(ds.xcd + i * K + m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == me;
   }
-  fetch(0);
-  stage(0);
-  fetch(1);
-  stage(1);
-  fetch(2);
+  fetch(K0);
+  stage(K0);
+  fetch(K0 + 1);
+  stage(K0 + 1);
+  fetch(K0 + 2);
   __syncthreads();
-  Pos cur{0, 0, 0, 0};
-  share(0, cur.lo, cur.hi);
+  Pos cur{K0, 0, 0, 0};
+  share(K0, cur.lo, cur.hi);
   cur.sb = cur.lo;
   cur = settle(cur);
-  if (cur.t < KS) load(xa, ya, cur);
-  while (ok && done < min(cur.t, KS)) ok = finish_step(done++, [] {});  // steps without samples
-  while (ok && cur.t < KS) {
+  if (cur.t < KE) load(xa, ya, cur);
+  while (ok && done < min(cur.t, KE)) ok = finish_step(done++, [] {});  // steps without samples
+  while (ok && cur.t < KE) {
     const Pos nx = settle(Pos{cur.t, cur.sb + SR, cur.lo, cur.hi});
     const bool same = nx.t == cur.t;
     if (same) load(xb, yb, nx);
@@ -460,10 +461,10 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
         for (int q = 0; q < CPQ; ++q) xa[s2][q] = xb[s2][q];
       ya = yb;
     } else {
-      while (ok && done < min(nx.t, KS)) {
+      while (ok && done < min(nx.t, KE)) {
         const int t = done++;
         ok = finish_step(t, [&]() {
-          if (t + 1 == nx.t && nx.t < KS) load(xa, ya, nx);
+          if (t + 1 == nx.t && nx.t < KE) load(xa, ya, nx);
         });
       }
     }

@@ -81,7 +81,7 @@ __global__ __launch_bounds__(1024) void sgd_dense_kernel(SgdArgs a) {
     wr[q] = c < a.dim ? wrow[c] : 0.f;
   }
   const int64_t K = (a.S + a.batch - 1) / a.batch;
-  for (int64_t k = 0; k < K; ++k) {
+  for (int64_t k = a.k0; k < a.k1; ++k) {
     const int64_t b0 = k * a.batch;
     const int Bp = int(min(int64_t(a.batch), a.S - b0));
     const double eta = step_size(a.lr_kind, a.lr0, a.round * K + k + 1);

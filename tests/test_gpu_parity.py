@@ -58,8 +58,8 @@ def f32(x):
     return float(np.float32(x))
 
 
-def params(wl):
-    return asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, wl.batch, wl.seed)
+def params(wl, local_steps=0):
+    return asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, wl.batch, wl.seed, local_steps)
 
 
 def oracle_kw(wl):
@@ -111,7 +111,7 @@ def test_schedule_device_matches_oracle(torch, n, S, rnd):
 # free-running rounds: both sides start from the same seeded models and run
 # independently; models are compared after every round
 # ----------------------------------------------------------------------------
-def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False):
+def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False, local_steps=0):
     p, i, w = graph(kind, wl.n_workers, d)
     if wl.features == "dense":
         X, y = synth.dense_data(wl)
@@ -127,7 +127,8 @@ def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False):
         sess.bind_dense(X, y)
     else:
         sess.bind_csr(rp, col, val, yy, wl.samples)
-    prm = params(wl)
+    prm = params(wl, local_steps)
+    K = oracle.sgd.n_steps(wl.samples, wl.batch)
     for r in range(rounds):
         if r % 2:
             sess.prepare_sgd(prm)  # optional; asap_local_sgd prepares by itself on even rounds
@@ -135,17 +136,18 @@ def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False):
         got = sess.models().cpu().numpy()
         amb = []
         halves = []
+        q, k0, k1 = oracle.sgd.round_steps(r, local_steps, K)
         for k in range(wl.n_workers):
-            sched = oracle.prng.schedule(wl.samples, wl.seed, k, r)
+            sched = oracle.prng.schedule(wl.samples, wl.seed, k, q)
             if shards[k][0] == "dense":
-                halves.append(oracle.sgd.sgd_pass_dense(W[k], shards[k][1], shards[k][2], sched, rnd=r,
-                                                        **oracle_kw(wl)))
+                halves.append(oracle.sgd.sgd_pass_dense(W[k], shards[k][1], shards[k][2], sched, rnd=q,
+                                                        steps=(k0, k1), **oracle_kw(wl)))
             else:
                 a = []
                 _, rpk, ck, vk, yk = shards[k]
-                halves.append(oracle.sgd.sgd_pass_csr(W[k], rpk, ck, vk, yk, sched, rnd=r, ambiguous=a,
-                                                      **oracle_kw(wl)))
-                amb += [(k, q) for q in a]
+                halves.append(oracle.sgd.sgd_pass_csr(W[k], rpk, ck, vk, yk, sched, rnd=q, ambiguous=a,
+                                                      steps=(k0, k1), **oracle_kw(wl)))
+                amb += [(k, qq) for qq in a]
         W = oracle.mix.stochastic_reduce(np.stack(halves), p, i, w)
         if amb:
             # an fp32 hinge decision may differ from the fp64 one: compare the
@@ -257,6 +259,44 @@ def test_csr_long_rows_and_large_batch_general_path(torch):
 def test_csr_logistic_on_directed_graphs(torch, kind):
     wl = synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 13, samples=200)
     _free_run(torch, wl, kind, 0, 4)
+
+
+# (A.2) as printed is one gradient step per mix (local_steps = 1); blocks of
+# L steps walk through the passes one after the other
+@pytest.mark.parametrize("case,L", [("dense", 1), ("dense", 4), ("wide", 1), ("wide", 3), ("csr", 1), ("csr", 4),
+                                    ("csr_general", 2), ("svm", 2)])
+def test_local_steps(torch, case, L):
+    if case == "dense":
+        wl = synth.RING8_DENSE_LR.with_(samples=128, batch=16)          # K = 8
+        kind, d = "ring", 2
+    elif case == "wide":
+        wl = synth.DENSE_LR_32W.with_(n_workers=3, dim=2048, samples=72, batch=8, lr_kind="inv_sqrt", lr0=0.2)  # K = 9
+        kind, d = "complete", 0
+    elif case == "csr":
+        wl = synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=256, batch=32)  # K = 8, planned pass
+        kind, d = "random", 4
+    elif case == "csr_general":
+        wl = synth.SPARSE_LR_64W.with_(n_workers=4, dim=1 << 12, samples=96, batch=96 // 4, nnz_mean=200.0)  # long rows
+        kind, d = "ring", 2
+    else:
+        wl = synth.SPARSE_SVM_256W.with_(n_workers=8, dim=1 << 12, samples=128, batch=16)  # K = 8, hinge + L2
+        kind, d = "random", 4
+    K = -(-wl.samples // wl.batch)
+    _free_run(torch, wl, kind, d, 2 * K // L + 1, local_steps=L)
+
+
+def test_local_steps_must_divide_the_pass(torch):
+    wl = synth.RING8_DENSE_LR.with_(samples=128, batch=16)  # K = 8
+    p, i, w = graph("ring", wl.n_workers, 2)
+    X, y = synth.dense_data(wl)
+    sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
+    sess.bind_dense(X, y)
+    for L in (3, -1, 16):
+        with pytest.raises(asap.AsapError) as e:
+            sess.local_sgd(params(wl, L))
+        assert e.value.status == asap.E_INVALID_ARG
+    sess.local_sgd(params(wl, 8))  # a whole pass in one round is allowed
+    sess.close()
 
 
 def test_csr_single_sample_and_full_batch(torch):

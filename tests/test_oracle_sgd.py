@@ -88,6 +88,37 @@ def test_step_counter_spans_rounds():
     assert sgd.n_steps(5, 2) == 3 and sgd.n_steps(4, 2) == 2 and sgd.n_steps(0, 2) == 0
 
 
+def test_round_steps_rule():
+    # local_steps = 0: round r is pass r; L dividing K: consecutive blocks of
+    # L steps of the sequence of passes
+    assert sgd.round_steps(7, 0, 5) == (7, 0, 5)
+    assert [sgd.round_steps(r, 2, 6) for r in range(4)] == [(0, 0, 2), (0, 2, 4), (0, 4, 6), (1, 0, 2)]
+    assert [sgd.round_steps(r, 1, 3)[:2] for r in range(7)] == [(0, 0), (0, 1), (0, 2), (1, 0), (1, 1), (1, 2), (2, 0)]
+    with pytest.raises(ValueError):
+        sgd.round_steps(0, 4, 6)
+
+
+def test_step_ranges_compose_to_the_pass():
+    # running steps [0, a) then [a, K) of a pass is the pass; the step
+    # counter t of the second block continues (pass q: t = q K + k + 1)
+    rng = np.random.default_rng(5)
+    S, D, B = 11, 4, 2
+    X, y = rng.standard_normal((S, D)), np.where(rng.random(S) < 0.5, -1.0, 1.0)
+    sched = rng.permutation(S)
+    kw = dict(batch=B, loss="logistic", lr_kind="inv_sqrt", lr0=0.3, l2=0.01, rnd=3)
+    w0 = rng.standard_normal(D)
+    full = sgd.sgd_pass_dense(w0, X, y, sched, **kw)
+    K = sgd.n_steps(S, B)
+    for a in range(K + 1):
+        part = sgd.sgd_pass_dense(w0, X, y, sched, steps=(0, a), **kw)
+        part = sgd.sgd_pass_dense(part, X, y, sched, steps=(a, K), **kw)
+        assert np.array_equal(part, full)
+    # one step from w = 0 on a one-sample pass is eta_t y x with t = q K + k + 1
+    w = sgd.sgd_pass_dense(np.zeros(D), X[:1], np.array([-1.0]), np.array([0]), batch=1, loss="hinge",
+                           lr_kind="inv_sqrt", lr0=0.5, l2=0.0, rnd=4, steps=(0, 1))
+    assert np.allclose(w, 0.5 / math.sqrt(4 * 1 + 0 + 1) * -1.0 * X[0])
+
+
 def test_ragged_last_batch_uses_its_own_size():
     # S = 3, B = 2: second batch holds one sample and averages over one.
     X = np.array([[1.0], [1.0], [4.0]])
