@@ -370,6 +370,30 @@ class Session:
     def current(self):
         return asap_current(self.ctx)
 
+    # checkpoints ----------------------------------------------------------
+    def save(self, path):
+        """Write the models and the round counter between two rounds (npz).
+
+        The models are those every worker holds at the start of the next
+        round, so a session that loads the file continues bit for bit as this
+        one would (same data, graph and parameters)."""
+        b, rnd, half = self.current()
+        if half:
+            raise RuntimeError("a checkpoint is taken between rounds, not after a half-step")
+        W = self.bufs[b][:, :self.dim].cpu().numpy()
+        with open(path, "wb") as f:
+            np.savez(f, models=W, round=np.int64(rnd), n=np.int64(self.n), dim=np.int64(self.dim))
+
+    def load(self, path, stream=None):
+        """Resume from a file written by save(): models into buffer 0, round
+        counter and epoch tags as at that round's start (asap_set_round)."""
+        with np.load(path, allow_pickle=False) as z:
+            W, rnd = z["models"], int(z["round"])
+            if int(z["n"]) != self.n or int(z["dim"]) != self.dim:
+                raise ValueError(f"checkpoint is {int(z['n'])} x {int(z['dim'])}, session is {self.n} x {self.dim}")
+        self.set_models(W, stream)
+        asap_set_round(self.ready(stream).ctx, rnd, 0, stream)
+
     def models(self):
         """Current models [n, dim] as a device view (no copy)."""
         b, _, _ = self.current()

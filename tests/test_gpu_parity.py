@@ -305,6 +305,46 @@ def test_csr_single_sample_and_full_batch(torch):
         _free_run(torch, wl, "ring", 2, 2)
 
 
+@pytest.mark.parametrize("features", ["csr", "dense"])
+def test_checkpoint_resume_is_bitwise_identical(torch, tmp_path, features):
+    if features == "csr":
+        wl = synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=256)
+        data = synth.csr_data(wl)
+    else:
+        wl = synth.DENSE_LR_32W.with_(n_workers=4, dim=2048, samples=64, batch=16)
+        data = synth.dense_data(wl)
+    p, i, w = graph("random", wl.n_workers, 2 if wl.n_workers == 4 else 4)
+
+    def session():
+        sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
+        if features == "csr":
+            sess.bind_csr(*data, wl.samples)
+        else:
+            sess.bind_dense(*data)
+        return sess
+
+    prm = params(wl)
+    a = session()
+    for _ in range(3):
+        a.round(prm)
+    ck = tmp_path / "ck.npz"
+    a.save(ck)
+    for _ in range(2):
+        a.round(prm)
+    want = a.models().cpu().numpy().copy()
+    assert a.current()[1] == 5
+    a.close()
+    b = session()
+    b.load(ck)
+    assert b.current() == (0, 3, 0)
+    for _ in range(2):
+        b.round(prm)
+    assert b.current()[1] == 5
+    assert np.array_equal(b.models().cpu().numpy().view(np.uint32), want.view(np.uint32))
+    assert b.check()[0] == asap.OK
+    b.close()
+
+
 def test_csr_run_twice_is_bitwise_identical(torch):
     wl = synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 14, samples=640)
     outs = []
