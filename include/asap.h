@@ -243,6 +243,36 @@ asap_status asap_stochastic_reduce(asap_ctx* ctx, void* stream);
 /* asap_local_sgd followed by asap_stochastic_reduce. */
 asap_status asap_round(asap_ctx* ctx, const asap_sgd_params* p, void* stream);
 
+/* `rounds` consecutive rounds (half-step, then reduce) in ONE persistent
+ * launch on `stream`, synchronised per worker by the fine-grained NOTIFY-ACK
+ * protocol of Section 4 rather than by kernel boundaries: worker i reduces
+ * as soon as its in-neighbours have published this round's half-step, and
+ * starts its next half-step right after its own reduce, while slower
+ * workers are still reducing.  Before overwriting its row in the other
+ * buffer it waits until every worker that reads that row (its out-neighbours
+ * in the graph) has acknowledged the previous round.
+ *
+ * Result: bit for bit the models, buffer index, round counter and epoch
+ * tags that `rounds` calls of asap_round with the same parameters leave,
+ * provided asap_round runs the same half-step code: dense shards always;
+ * CSR shards when the stream-ordered path takes its general kernel (the
+ * planned CSR pass is not used here, so with minibatches of at most 64 rows
+ * of at most 128 nonzeros the two paths agree to the oracle's tolerance but
+ * not bitwise).
+ *
+ * Requirements: state as after a reduce or asap_set_round (no half-step
+ * pending); every worker has at most 64 in-neighbours and at most 64
+ * out-neighbours (self included); all workgroups of the launch fit on the
+ * device at once (one per worker; K per worker for dense D in (1024, 8192]),
+ * else ASAP_E_STATE.  `wait_ms` bounds each wait for a neighbour (0: 10 s).
+ * A wait that runs out stops that worker and, in turn, its neighbours; the
+ * launch ends and asap_check reports ASAP_E_EPOCH.  The models are then
+ * undefined (restore a checkpoint).  A worker whose starting tag is not the
+ * round's start tag stops the same way.  Uses the schedule area of the
+ * workspace; forgets any CSR plan prepared ahead.  Asynchronous. */
+asap_status asap_run_rounds(asap_ctx* ctx, const asap_sgd_params* p, int64_t rounds, int32_t wait_ms,
+                            void* stream);
+
 /* Where the live models are: index (0 or 1) of the buffer holding the
  * current round's models, the round number, and whether this round's
  * half-step already ran (1) or not (0).  Any out pointer may be NULL. */

@@ -31,7 +31,8 @@ EXPORTS = (
     "asap_graph_random_regular",
     "asap_metropolis_weights", "asap_schedule", "asap_create", "asap_workspace_size",
     "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr",
-    "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_current",
+    "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_run_rounds",
+    "asap_current",
     "asap_set_round", "asap_schedule_device", "asap_metrics", "asap_check",
     "asap_debug_set_tag", "asap_last_error", "asap_destroy",
 )
@@ -79,6 +80,7 @@ def lib():
         "asap_prepare_sgd": [p, C.POINTER(SgdParams), p],
         "asap_stochastic_reduce": [p, p],
         "asap_round": [p, C.POINTER(SgdParams), p],
+        "asap_run_rounds": [p, C.POINTER(SgdParams), i64, i32, p],
         "asap_current": [p, C.POINTER(i32), C.POINTER(i64), C.POINTER(i32)],
         "asap_set_round": [p, i64, i32, p],
         "asap_schedule_device": [p, u64, i64, p, p],
@@ -239,6 +241,10 @@ def asap_round(ctx, params: SgdParams, stream=None):
     _check(lib().asap_round(ctx, C.byref(params), _stream(stream)), ctx)
 
 
+def asap_run_rounds(ctx, params: SgdParams, rounds: int, wait_ms: int = 0, stream=None):
+    _check(lib().asap_run_rounds(ctx, C.byref(params), int(rounds), int(wait_ms), _stream(stream)), ctx)
+
+
 def asap_current(ctx):
     b, r, h = C.c_int32(), C.c_int64(), C.c_int32()
     _check(lib().asap_current(ctx, C.byref(b), C.byref(r), C.byref(h)), ctx)
@@ -365,6 +371,10 @@ class Session:
 
     def round(self, params, stream=None):
         asap_round(self.ready().ctx, params, stream)
+
+    def run_rounds(self, params, rounds, wait_ms=0, stream=None):
+        """`rounds` rounds in one launch with per-worker NOTIFY-ACK."""
+        asap_run_rounds(self.ready().ctx, params, rounds, wait_ms, stream)
 
     # inspection ---------------------------------------------------------
     def current(self):

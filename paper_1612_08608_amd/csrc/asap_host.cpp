@@ -33,6 +33,7 @@ enum DataKind { kNoData = 0, kDense = 1, kCsr = 2 };
 constexpr int kDenseMaxMembers = 8;
 constexpr int kDenseCus = 256;
 constexpr uint32_t kDenseSpinLimit = 1u << 20;
+constexpr int32_t kRoundsWaitMs = 10000;  // default bound on one neighbour wait of the multi-round launch
 
 // Per-round buffers of the CSR pass: the sample schedule, row descriptors
 // and the column plan.  CSR workspaces hold two, so that the next round can
@@ -48,8 +49,10 @@ struct asap_ctx {
   int64_t dim = 0;
   std::vector<int32_t> ptr, idx;
   std::vector<float> w;
+  std::vector<int32_t> optr, oidx;  // the transpose: the workers that read row i
   bool complete_uniform = false;
   int32_t max_deg = 0;  // longest row of the graph (entries, self included)
+  int32_t max_out = 0;  // most workers that read one row
   int32_t n_cu = 256;   // compute units of the device the workspace is on
 
   // caller-owned device memory
@@ -74,7 +77,7 @@ struct asap_ctx {
   int32_t max_row = 0;
 
   // workspace layout (byte offsets)
-  size_t off_ptr = 0, off_idx = 0, off_w = 0, off_tag = 0, off_scale = 0, off_err = 0,
+  size_t off_ptr = 0, off_idx = 0, off_w = 0, off_optr = 0, off_oidx = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
          off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dxcd = 0, off_dcount = 0, off_progress = 0,
          total = 0;
@@ -142,8 +145,10 @@ void layout(asap_ctx* c) {
   c->off_ptr = o;   o = align_up(o + (n + 1) * 4);
   c->off_idx = o;   o = align_up(o + nnz * 4);
   c->off_w = o;     o = align_up(o + nnz * 4);
+  c->off_optr = o;  o = align_up(o + (n + 1) * 4);
+  c->off_oidx = o;  o = align_up(o + nnz * 4);
   c->off_tag = o;   o = align_up(o + 2 * n * 8);
-  c->off_scale = o; o = align_up(o + n * 4);
+  c->off_scale = o; o = align_up(o + 2 * n * 4);  // [2][n]: the multi-round launch keeps one per buffer
   c->off_err = o;   o = align_up(o + kErrWords * 4);
   c->off_vmax = o;  o = align_up(o + n * 4);
   c->off_scan = o;  o = align_up(o + 8 * 8);
@@ -533,6 +538,19 @@ extern "C" asap_status asap_create(int32_t n, int64_t dim, const int32_t* nbr_pt
   c->w.assign(nbr_w, nbr_w + nbr_ptr[n]);
   c->complete_uniform = is_complete_uniform(n, nbr_ptr, nbr_w);
   for (int32_t i = 0; i < n; ++i) c->max_deg = std::max(c->max_deg, nbr_ptr[i + 1] - nbr_ptr[i]);
+  {
+    // transpose of the graph rows: out-neighbours in ascending order
+    c->optr.assign(size_t(n) + 1, 0);
+    for (int32_t p = 0; p < nbr_ptr[n]; ++p) ++c->optr[size_t(nbr_idx[p]) + 1];
+    for (int32_t j = 0; j < n; ++j) {
+      c->max_out = std::max(c->max_out, c->optr[size_t(j) + 1]);
+      c->optr[size_t(j) + 1] += c->optr[size_t(j)];
+    }
+    c->oidx.resize(size_t(nbr_ptr[n]));
+    std::vector<int32_t> fill(c->optr.begin(), c->optr.end() - 1);
+    for (int32_t i = 0; i < n; ++i)
+      for (int32_t p = nbr_ptr[i]; p < nbr_ptr[i + 1]; ++p) c->oidx[size_t(fill[size_t(nbr_idx[p])]++)] = i;
+  }
   layout(c);
   *out = c;
   return ASAP_OK;
@@ -626,11 +644,13 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
   const size_t n = size_t(c->n), nnz = c->idx.size();
   if ((e = hipMemcpyAsync(at<int32_t>(c, c->off_ptr), c->ptr.data(), (n + 1) * 4, hipMemcpyHostToDevice, s)) ||
       (e = hipMemcpyAsync(at<int32_t>(c, c->off_idx), c->idx.data(), nnz * 4, hipMemcpyHostToDevice, s)) ||
-      (e = hipMemcpyAsync(at<float>(c, c->off_w), c->w.data(), nnz * 4, hipMemcpyHostToDevice, s)))
+      (e = hipMemcpyAsync(at<float>(c, c->off_w), c->w.data(), nnz * 4, hipMemcpyHostToDevice, s)) ||
+      (e = hipMemcpyAsync(at<int32_t>(c, c->off_optr), c->optr.data(), (n + 1) * 4, hipMemcpyHostToDevice, s)) ||
+      (e = hipMemcpyAsync(at<int32_t>(c, c->off_oidx), c->oidx.data(), nnz * 4, hipMemcpyHostToDevice, s)))
     return hip_fail(c, e, "graph upload");
   if ((e = launch_fill_i64(at<int64_t>(c, c->off_tag), 2 * int64_t(n), -1, s)) ||
       (e = launch_fill_i64(at<int64_t>(c, c->off_tag) + c->cur * n, int64_t(n), tag_start(c->round), s)) ||
-      (e = launch_fill_f32(at<float>(c, c->off_scale), int64_t(n), 1.0f, s)) ||
+      (e = launch_fill_f32(at<float>(c, c->off_scale), 2 * int64_t(n), 1.0f, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err), 1, 0, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)) ||
@@ -940,6 +960,82 @@ extern "C" asap_status asap_round(asap_ctx* c, const asap_sgd_params* p, void* s
   asap_status s = asap_local_sgd(c, p, stream);
   if (s != ASAP_OK) return s;
   return asap_stochastic_reduce(c, stream);
+}
+
+extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, int64_t rounds, int32_t wait_ms,
+                                       void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  asap_status st = check_half_step(c, p);
+  if (st != ASAP_OK) return st;
+  if (rounds < 1 || rounds > (int64_t(1) << 40)) return fail(c, ASAP_E_INVALID_ARG, "rounds must be in [1, 2^40]");
+  if (wait_ms < 0) return fail(c, ASAP_E_INVALID_ARG, "wait_ms must be >= 0");
+  if (c->max_deg > kRoundsMaxDeg || c->max_out > kRoundsMaxDeg)
+    return fail(c, ASAP_E_STATE, "a worker has %d in- and %d out-neighbours; the multi-round launch takes at most %d",
+                c->max_deg, c->max_out, kRoundsMaxDeg);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the launch rewrites the schedule and row-descriptor area of plan slot 0
+  drain_ahead(c);
+  hipError_t e;
+  int dev_id = 0, khz = 0;
+  if ((e = hipGetDevice(&dev_id)) || (e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev_id)))
+    return hip_fail(c, e, "wall clock rate");
+  const int64_t n = c->n;
+  SgdArgs a = sgd_args(c, p, c->plan[0]);
+  RoundsArgs ra{};
+  ra.buf[0] = c->buf[0];
+  ra.buf[1] = c->buf[1];
+  ra.cur = c->cur;
+  ra.n = c->n;
+  ra.r0 = c->round;
+  ra.R = rounds;
+  ra.local_steps = p->local_steps;
+  ra.seed = p->seed;
+  ra.in_ptr = at<int32_t>(c, c->off_ptr);
+  ra.in_idx = at<int32_t>(c, c->off_idx);
+  ra.in_w = at<float>(c, c->off_w);
+  ra.out_ptr = at<int32_t>(c, c->off_optr);
+  ra.out_idx = at<int32_t>(c, c->off_oidx);
+  ra.tag = at<int64_t>(c, c->off_tag);
+  ra.scale2 = at<float>(c, c->off_scale);
+  ra.scaled = (c->kind == kCsr && p->l2 > 0.0f) ? 1 : 0;
+  {
+    // the reduce arithmetic of the kernel asap_stochastic_reduce launches
+    MixArgs m{};
+    m.n = c->n;
+    m.ld = c->ld;
+    m.dim = c->dim;
+    ra.fp64_mix = (c->complete_uniform || !mix_slab_applies(m, c->max_deg)) ? 1 : 0;
+  }
+  ra.wait_ticks = (long long)(wait_ms ? wait_ms : kRoundsWaitMs) * (long long)std::max(khz, 1);
+  ra.err = at<int32_t>(c, c->off_err);
+  ra.sched = at<int32_t>(c, c->plan[0].sched);
+  ra.rowinfo = at<RowInfo>(c, c->plan[0].rowinfo);
+  if (c->kind == kCsr) {
+    e = launch_rounds_csr(a, ra, c->n_cu, s);
+  } else if (dense_wide_cpq(c->dim)) {
+    DenseSync ds{};
+    ds.part = at<float>(c, c->off_dacc);
+    ds.count = at<uint32_t>(c, c->off_dcount);
+    ds.xcd = at<int32_t>(c, c->off_dxcd);
+    ds.ldp = int64_t(dense_wide_cpq(c->dim)) * 2048;
+    ds.K = std::max(1, std::min(c->dense_k, dense_wide_max_members(a, c->n_cu) / c->n));
+    ds.spin_limit = kDenseSpinLimit;
+    ds.err = at<int32_t>(c, c->off_err) + kErrRendezvous;
+    ds.base = 0;
+    e = launch_fill_i32(reinterpret_cast<int32_t*>(ds.count), n, 0, s);
+    if (e == hipSuccess) e = launch_rounds_dense_wide(a, ds, ra, s);
+  } else {
+    e = launch_rounds_dense(a, ra, c->n_cu, s);
+  }
+  if (e == hipErrorCooperativeLaunchTooLarge)
+    return fail(c, ASAP_E_STATE, "the %d workers' workgroups do not fit on the device at once", c->n);
+  if (e != hipSuccess) return hip_fail(c, e, "multi-round kernel");
+  c->cur ^= int32_t(rounds & 1);
+  c->round += rounds;
+  c->half_done = false;
+  c->half_scaled = false;
+  c->prep_valid = false;
+  return ASAP_OK;
 }
 
 extern "C" asap_status asap_current(const asap_ctx* c, int32_t* buffer, int64_t* round,

@@ -9,8 +9,8 @@ namespace asap {
 
 // Epoch tags: 2r = "models of round r at the start of the round",
 // 2r + 1 = "round r half-step published" (the NOTIFY of Section 4).
-inline int64_t tag_start(int64_t r) { return 2 * r; }
-inline int64_t tag_half(int64_t r) { return 2 * r + 1; }
+__host__ __device__ inline int64_t tag_start(int64_t r) { return 2 * r; }
+__host__ __device__ inline int64_t tag_half(int64_t r) { return 2 * r + 1; }
 
 // Device error words (int32 each).
 enum { kErrEpochCount = 0, kErrEpochWorker = 1, kErrRendezvous = 2, kErrWords = 16 };
@@ -123,7 +123,40 @@ struct DenseSync {
   int32_t K;
   uint32_t spin_limit;
   int32_t* err;
+  uint32_t base;  // arrivals already counted when the pass starts
 };
+// Several rounds in one persistent launch with per-worker NOTIFY-ACK
+// (Section 4; device side in rounds_device.h).  Workgroups of worker i run
+// the same half-step code as the stream-ordered kernels, then reduce row i
+// themselves.
+struct RoundsArgs {
+  float* buf[2];       // the two model buffers [n][ld]
+  int32_t cur;         // buffer of round r0
+  int32_t n;
+  int64_t r0, R;       // rounds r0 .. r0 + R - 1
+  int32_t local_steps; // as asap_sgd_params.local_steps
+  uint64_t seed;       // schedule seed
+  const int32_t* in_ptr;   // [n+1] graph rows: in-neighbours (self included)
+  const int32_t* in_idx;
+  const float* in_w;
+  const int32_t* out_ptr;  // [n+1] the transpose: workers that read row i
+  const int32_t* out_idx;
+  int64_t* tag;        // [2][n] epoch tags, as the stream-ordered path keeps them
+  float* scale2;       // [2][n] L2 scale of each worker's half-step, per buffer
+  int32_t scaled;      // fold the scales into the weights (CSR with l2 > 0)
+  int32_t fp64_mix;    // 1: reduce in fp64 (tile / mean kernels); 0: fp32 (slab kernel)
+  long long wait_ticks;  // wall-clock ticks a worker waits for its neighbours
+  int32_t* err;        // device error words
+  int32_t* sched;      // [n][S] dense: this pass's schedule rows
+  RowInfo* rowinfo;    // [n][S] CSR: this pass's row descriptors
+};
+constexpr int kRoundsMaxDeg = 64;  // in- and out-neighbours of a worker in a multi-round launch
+hipError_t launch_rounds_dense(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s);
+hipError_t launch_rounds_dense_wide(const SgdArgs& a, const DenseSync& ds, const RoundsArgs& ra, hipStream_t s);
+hipError_t launch_rounds_csr(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s);
+// whether the stream-ordered reduce of this graph runs the slab kernel
+bool mix_slab_applies(const MixArgs& a, int max_deg);
+
 hipError_t launch_dense_scan(const float* X, const float* y, int32_t n, int64_t S, int64_t dim, int64_t ldx,
                              float* xmax, unsigned long long* out, hipStream_t s);
 int dense_wide_cpq(int64_t dim);                               // 0: not handled

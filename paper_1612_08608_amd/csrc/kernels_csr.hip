@@ -32,6 +32,7 @@
 #include <cmath>
 
 #include "asap_launch.h"
+#include "rounds_device.h"
 #include "csr_device.h"
 
 namespace asap {
@@ -196,10 +197,9 @@ __device__ __forceinline__ void count_stats(Shared& sh, int slot, const DataReg<
 }
 
 template <int E, bool PIPE>
-__global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
-  if (a.run_if && *a.run_if == 0) return;  // the planned kernel took this round
+__device__ __forceinline__ void csr_pass(const SgdArgs& a, int i) {
   __shared__ Shared sh;
-  const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane & (kRowLanes - 1);
   const int brow = wave * (64 / kRowLanes) + (lane / kRowLanes);  // fast-path row of this lane
   float* vrow = a.models + int64_t(i) * a.ld;
@@ -396,8 +396,49 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
   for (int h = tid; h < H; h += kThreads) vrow[a.hot_cols[h]] = sh.vhot[h];
   if (tid == 0) {
     a.scale[i] = float(s);
-    a.tag[i] = a.tag_value;
+    if (a.tag) a.tag[i] = a.tag_value;
   }
+}
+
+template <int E, bool PIPE>
+__global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
+  if (a.run_if && *a.run_if == 0) return;  // the planned kernel took this round
+  csr_pass<E, PIPE>(a, int(blockIdx.x));
+}
+
+// Several rounds in one launch (rounds_device.h): one workgroup per worker
+// runs its passes on this kernel's code and reduces its own row.
+template <int E, bool PIPE>
+__global__ __launch_bounds__(kThreads) void rounds_csr_kernel(SgdArgs a, RoundsArgs ra) {
+  const int i = int(blockIdx.x);
+  rounds::drive(
+      a, ra, i, 0,
+      [&](int64_t pass) {
+        rounds::fill_rowinfo(ra.seed, i, pass, a.S, a.row_ptr, a.y, ra.rowinfo + int64_t(i) * a.S);
+      },
+      [&](const SgdArgs& ar) {
+        csr_pass<E, PIPE>(ar, i);
+        return true;
+      });
+}
+
+template <int E, bool PIPE>
+hipError_t launch_rounds_e(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s) {
+  int per = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_csr_kernel<E, PIPE>, kThreads, 0);
+  if (e != hipSuccess) return e;
+  if (int64_t(per) * n_cu < a.n) return hipErrorCooperativeLaunchTooLarge;
+  SgdArgs aa = a;
+  RoundsArgs rr = ra;
+  aa.rowinfo = ra.rowinfo;
+  void* args[] = {&aa, &rr};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&rounds_csr_kernel<E, PIPE>), dim3(uint32_t(a.n)),
+                                    dim3(kThreads), args, 0, s);
+}
+
+template <int E>
+hipError_t launch_rounds_pipe(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s, bool pipe) {
+  return pipe ? launch_rounds_e<E, true>(a, ra, n_cu, s) : launch_rounds_e<E, false>(a, ra, n_cu, s);
 }
 
 // ----------------------------------------------------------------------------
@@ -466,6 +507,17 @@ hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s) {
   if (a.max_row <= kRowLanes * 4) return launch_e<4>(a, s, pipe);
   if (a.max_row <= kRowLanes * 6) return launch_e<6>(a, s, pipe);
   return launch_e<8>(a, s, pipe);
+}
+
+// the same kernel choice as launch_sgd_csr, so that both paths run the same code
+hipError_t launch_rounds_csr(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s) {
+  if (a.batch > kBMax || a.n_hot > kHotMax) return hipErrorInvalidValue;
+  const bool pipe = a.batch <= kFastRows;
+  if (a.max_row <= kRowLanes * 2) return launch_rounds_pipe<2>(a, ra, n_cu, s, pipe);
+  if (a.max_row <= kRowLanes * 3) return launch_rounds_pipe<3>(a, ra, n_cu, s, pipe);
+  if (a.max_row <= kRowLanes * 4) return launch_rounds_pipe<4>(a, ra, n_cu, s, pipe);
+  if (a.max_row <= kRowLanes * 6) return launch_rounds_pipe<6>(a, ra, n_cu, s, pipe);
+  return launch_rounds_pipe<8>(a, ra, n_cu, s, pipe);
 }
 
 hipError_t launch_col_hist(const int32_t* col, int64_t nnz, int64_t stride, int32_t* counts, hipStream_t s) {

@@ -33,6 +33,7 @@
 #include <cmath>
 
 #include "asap_launch.h"
+#include "rounds_device.h"
 
 namespace asap {
 namespace {
@@ -118,26 +119,28 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Worker i and member k of this workgroup: the members of one worker on one
+// XCD when the grid allows it (blocks are dealt to the 8 XCDs round-robin),
+// so the exchange stays in one L2.
+__device__ __forceinline__ void wide_member(int n, int K, int& i, int& k) {
+  const int bid = int(blockIdx.x), nb = int(gridDim.x);
+  if (nb % 8 == 0 && n % 8 == 0) {
+    const int j = bid / 8;
+    i = (bid % 8) * (n / 8) + j / K;
+    k = j % K;
+  } else {
+    i = bid / K;
+    k = bid % K;
+  }
+}
+
+// Member k's part of worker i's pass; false when a rendezvous timed out.
 template <int CPQ, int SR>
-__global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, DenseSync ds) {
+__device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSync& ds, int i, int k) {
   __shared__ double red[2][kWaves][4][SR];  // per-row partial margins
   __shared__ int ridx[2][kMaxBatch];  // this member's row indices of steps t, t+1 (slot t & 1)
   __shared__ int abort_flag;
   const int K = ds.K;
-  // members of one worker on one XCD when the grid allows it (blocks are
-  // dealt to the 8 XCDs round-robin), so the exchange stays in one L2
-  int i, k;
-  {
-    const int bid = int(blockIdx.x), nb = int(gridDim.x);
-    if (nb % 8 == 0 && a.n % 8 == 0) {
-      const int j = bid / 8;
-      i = (bid % 8) * (a.n / 8) + j / K;
-      k = j % K;
-    } else {
-      i = bid / K;
-      k = bid % K;
-    }
-  }
   const int tid = int(threadIdx.x), lane = tid & 63, wave = tid >> 6;
   if (tid == 0) abort_flag = 0;
   float* wrow = a.models + int64_t(i) * a.ld;
@@ -370,7 +373,7 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     }
     during();
     if (K > 1) {
-      if (!gather(uint32_t(K) * uint32_t(t - K0 + 2))) return false;
+      if (!gather(ds.base + uint32_t(K) * uint32_t(t - K0 + 2))) return false;
       // ... and every member sums all K partials in fp64 in member order,
       // so all members get the same gradient bit for bit.  Members on one
       // XCD meet in its L2 (loads that bypass only the CU's L1); otherwise
@@ -432,7 +435,7 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     const int me = xcd_id();
     if (tid == 0) __hip_atomic_store(ds.xcd + i * K + k, me, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     arrive();
-    ok = gather(uint32_t(K));
+    ok = gather(ds.base + uint32_t(K));
     local = ok;
     for (int m = 0; m < K; ++m)
       local = local && __hip_atomic_load(ds.xcd + i * K + m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == me;
@@ -485,9 +488,35 @@ __global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, Den
     }
     if (tid == 0) {
       a.scale[i] = 1.0f;
-      a.tag[i] = a.tag_value;
+      if (a.tag) a.tag[i] = a.tag_value;
     }
   }
+  return ok;
+}
+
+template <int CPQ, int SR>
+__global__ __launch_bounds__(kThreads) void sgd_dense_wide_kernel(SgdArgs a, DenseSync ds) {
+  int i, k;
+  wide_member(a.n, ds.K, i, k);
+  (void)dense_wide_pass<CPQ, SR>(a, ds, i, k);
+}
+
+// Several rounds in one launch (rounds_device.h): the K members of a worker
+// run each pass together; member 0 publishes the row, waits for the
+// neighbours and reduces it, and the others wait for the reduced row.  The
+// members' arrival counter keeps counting across rounds (ds.base).
+template <int CPQ, int SR>
+__global__ __launch_bounds__(kThreads) void rounds_dense_wide_kernel(SgdArgs a, DenseSync ds, RoundsArgs ra) {
+  int i, k;
+  wide_member(a.n, ds.K, i, k);
+  rounds::drive(
+      a, ra, i, k, [&](int64_t pass) { rounds::fill_schedule(ra.seed, i, pass, a.S, ra.sched + int64_t(i) * a.S); },
+      [&](const SgdArgs& ar) {
+        const bool ok = dense_wide_pass<CPQ, SR>(ar, ds, i, k);
+        // arrivals of this pass: the opening meeting and one per step
+        if (ds.K > 1) ds.base += uint32_t(ds.K) * uint32_t(ar.k1 - ar.k0 + 1);
+        return ok;
+      });
 }
 
 template <int CPQ, int SR>
@@ -502,6 +531,16 @@ hipError_t launch_wide(const SgdArgs& a, const DenseSync& ds, hipStream_t s) {
   void* args[] = {&aa, &dd};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&sgd_dense_wide_kernel<CPQ, SR>), grid, block,
                                     args, 0, s);
+}
+
+template <int CPQ, int SR>
+hipError_t launch_rounds_wide(const SgdArgs& a, const DenseSync& ds, const RoundsArgs& ra, hipStream_t s) {
+  SgdArgs aa = a;
+  DenseSync dd = ds;
+  RoundsArgs rr = ra;
+  void* args[] = {&aa, &dd, &rr};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&rounds_dense_wide_kernel<CPQ, SR>),
+                                    dim3(uint32_t(a.n * ds.K)), dim3(kThreads), args, 0, s);
 }
 
 // Bind-time scan of dense shards: xmax[i] = max |x| over worker i's shard
@@ -563,6 +602,15 @@ int dense_wide_max_members(const SgdArgs& a, int n_cu) {
     default: return 1;
   }
   return std::max(1, per) * n_cu;
+}
+
+hipError_t launch_rounds_dense_wide(const SgdArgs& a, const DenseSync& ds, const RoundsArgs& ra, hipStream_t s) {
+  switch (dense_wide_cpq(a.dim)) {
+    case 1: return launch_rounds_wide<1, 8>(a, ds, ra, s);
+    case 2: return launch_rounds_wide<2, 8>(a, ds, ra, s);
+    case 4: return launch_rounds_wide<4, 1>(a, ds, ra, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_sgd_dense_wide(const SgdArgs& a, const DenseSync& ds, hipStream_t s) {

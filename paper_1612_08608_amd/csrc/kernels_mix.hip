@@ -368,31 +368,47 @@ hipError_t launch_epoch_check(const MixArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+namespace {
+// float4 per thread per chunk of the slab kernel for this graph (0: the slab
+// kernel does not apply).  With more than 512 rows a 64 KiB chunk holds under
+// 128 bytes of each row, half a cache line, and the other half is fetched
+// again for the next chunk; a 128 KiB chunk (8 float4 per thread) reads whole
+// lines.  Rows of 17 entries keep 4 (8 would not fit the registers).
+int slab_pf(int n, int max_deg) {
+  if (n < 8 || n > kSlabThreads || (n & (n - 1)) || max_deg > 17) return 0;
+  return (n > 512 && max_deg <= 9) ? 8 : 4;
+}
+
+// per-thread staging offset (rows below 1024/(C/4), float4 slots below C/4)
+// and chunk count within 31 bits
+bool slab_fits(const MixArgs& a, int PF) {
+  const int C = 4 * PF * kSlabThreads / a.n;
+  if ((int64_t(kSlabThreads / (C / 4) - 1) * a.ld + C) * 4 >= (int64_t(1) << 31)) return false;
+  return (a.dim + C - 1) / C < (int64_t(1) << 31);
+}
+}  // namespace
+
+bool mix_slab_applies(const MixArgs& a, int max_deg) {
+  const int pf = slab_pf(a.n, max_deg);
+  return pf != 0 && slab_fits(a, pf);
+}
+
 // Slab kernel when n is a power of two in [8, 1024] and every row has at most
 // 17 entries (returns hipErrorNotSupported otherwise).
 template <int DEG, int PF>
 hipError_t launch_slab(const MixArgs& a, int n_cu, hipStream_t s) {
-  const int n = a.n;
-  const int C = 4 * PF * kSlabThreads / n;
-  // per-thread staging offset: rows below 1024/(C/4), float4 slots below C/4
-  if ((int64_t(kSlabThreads / (C / 4) - 1) * a.ld + C) * 4 >= (int64_t(1) << 31))
-    return hipErrorNotSupported;
-  const int64_t nchunks64 = (a.dim + C - 1) / C;
-  if (nchunks64 >= (int64_t(1) << 31)) return hipErrorNotSupported;
-  const int nchunks = int(nchunks64);
+  if (!slab_fits(a, PF)) return hipErrorNotSupported;
+  const int C = 4 * PF * kSlabThreads / a.n;
+  const int nchunks = int((a.dim + C - 1) / C);
   const int grid = std::max(1, std::min(nchunks, n_cu));
   hipLaunchKernelGGL((mix_slab_kernel<DEG, PF>), dim3(grid), dim3(kSlabThreads), 0, s, a, nchunks);
   return hipGetLastError();
 }
 
 hipError_t launch_mix_slab(const MixArgs& a, int max_deg, int n_cu, hipStream_t s) {
-  const int n = a.n;
-  if (n < 8 || n > kSlabThreads || (n & (n - 1)) || max_deg > 17) return hipErrorNotSupported;
-  // With more than 512 rows a 64 KiB chunk holds under 128 bytes of each
-  // row, half a cache line, and the other half is fetched again for the
-  // next chunk; a 128 KiB chunk (8 float4 per thread) reads whole lines.
-  // Rows of 17 entries keep 4 (8 would not fit the registers).
-  const bool wide = n > 512;
+  const int pf = slab_pf(a.n, max_deg);
+  if (pf == 0) return hipErrorNotSupported;
+  const bool wide = pf == 8;
   if (max_deg <= 3) return wide ? launch_slab<3, 8>(a, n_cu, s) : launch_slab<3, 4>(a, n_cu, s);
   if (max_deg <= 5) return wide ? launch_slab<5, 8>(a, n_cu, s) : launch_slab<5, 4>(a, n_cu, s);
   if (max_deg <= 9) return wide ? launch_slab<9, 8>(a, n_cu, s) : launch_slab<9, 4>(a, n_cu, s);

@@ -15,6 +15,7 @@
 
 #include "asap_common.h"
 #include "asap_launch.h"
+#include "rounds_device.h"
 
 namespace asap {
 namespace {
@@ -65,10 +66,9 @@ template <int CPT>
 constexpr int dense_sb() { return CPT >= 16 ? 2 : CPT >= 8 ? 4 : 8; }
 
 template <int CPT>
-__global__ __launch_bounds__(1024) void sgd_dense_kernel(SgdArgs a) {
+__device__ __forceinline__ void dense_pass(const SgdArgs& a, int i) {
   constexpr int SB = dense_sb<CPT>();
   __shared__ double part[16 * SB];
-  const int i = blockIdx.x;
   const int T = blockDim.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = T >> 6;
   float* wrow = a.models + int64_t(i) * a.ld;
   const float* Xi = a.X + int64_t(i) * a.S * a.ldx;
@@ -141,8 +141,26 @@ __global__ __launch_bounds__(1024) void sgd_dense_kernel(SgdArgs a) {
   }
   if (tid == 0) {
     a.scale[i] = 1.0f;
-    a.tag[i] = a.tag_value;
+    if (a.tag) a.tag[i] = a.tag_value;
   }
+}
+
+template <int CPT>
+__global__ __launch_bounds__(1024) void sgd_dense_kernel(SgdArgs a) {
+  dense_pass<CPT>(a, int(blockIdx.x));
+}
+
+// Several rounds in one launch (rounds_device.h): one workgroup per worker
+// runs its passes and reduces its own row.
+template <int CPT>
+__global__ __launch_bounds__(1024) void rounds_dense_kernel(SgdArgs a, RoundsArgs ra) {
+  const int i = int(blockIdx.x);
+  rounds::drive(
+      a, ra, i, 0, [&](int64_t pass) { rounds::fill_schedule(ra.seed, i, pass, a.S, ra.sched + int64_t(i) * a.S); },
+      [&](const SgdArgs& ar) {
+        dense_pass<CPT>(ar, i);
+        return true;
+      });
 }
 
 // ----------------------------------------------------------------------------
@@ -228,6 +246,32 @@ hipError_t launch_sgd_dense(const SgdArgs& a, hipStream_t s) {
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+namespace {
+template <int CPT>
+hipError_t launch_rounds_dense_t(const SgdArgs& a, const RoundsArgs& ra, int T, int n_cu, hipStream_t s) {
+  const void* fn = reinterpret_cast<const void*>(&rounds_dense_kernel<CPT>);
+  int per = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_dense_kernel<CPT>, T, 0);
+  if (e != hipSuccess) return e;
+  if (int64_t(per) * n_cu < a.n) return hipErrorCooperativeLaunchTooLarge;
+  SgdArgs aa = a;
+  RoundsArgs rr = ra;
+  void* args[] = {&aa, &rr};
+  return hipLaunchCooperativeKernel(fn, dim3(uint32_t(a.n)), dim3(uint32_t(T)), args, 0, s);
+}
+}  // namespace
+
+hipError_t launch_rounds_dense(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s) {
+  const int T = int(std::min<int64_t>(1024, (a.dim + 63) / 64 * 64));
+  const int64_t need = (a.dim + T - 1) / T;
+  if (need <= 1) return launch_rounds_dense_t<1>(a, ra, T, n_cu, s);
+  if (need <= 2) return launch_rounds_dense_t<2>(a, ra, T, n_cu, s);
+  if (need <= 4) return launch_rounds_dense_t<4>(a, ra, T, n_cu, s);
+  if (need <= 8) return launch_rounds_dense_t<8>(a, ra, T, n_cu, s);
+  if (need <= 16) return launch_rounds_dense_t<16>(a, ra, T, n_cu, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_csr_scan(const int64_t* row_ptr, const int32_t* col, const float* val,

@@ -1,0 +1,176 @@
+"""Multi-round launch with per-worker NOTIFY-ACK (Section 4), through the C ABI.
+
+asap_run_rounds runs R rounds in one persistent launch, each worker waiting
+only for its own neighbours.  The data dependencies are those of R calls of
+asap_round, so the result must be the same bits (same half-step code, same
+reduce arithmetic); both paths are also checked against the oracle, and the
+stream-ordered path continues from the state the launch leaves.
+"""
+import numpy as np
+import pytest
+
+from conftest import assert_models_close
+from paper_1612_08608_amd import asap, synth
+import oracle
+from test_gpu_parity import graph, params, oracle_kw, csr_shards
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+    assert _t.cuda.is_available(), "GPU tests need a GPU"
+    asap.lib()
+    return _t
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    print(f"\n[gpu] {request.node.nodeid}", flush=True)
+    yield
+
+
+def _session(wl, kind, d, W0=None):
+    p, i, w = graph(kind, wl.n_workers, d)
+    sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
+    if W0 is not None:
+        sess.set_models(W0)
+    if wl.features == "dense":
+        X, y = synth.dense_data(wl)
+        sess.bind_dense(X, y)
+    else:
+        rp, col, val, yy = synth.csr_data(wl)
+        sess.bind_csr(rp, col, val, yy, wl.samples)
+    return sess, (p, i, w)
+
+
+def _bits(sess):
+    return sess.models().cpu().numpy().view(np.uint32).copy()
+
+
+# (workload, graph kind, degree, rounds, local steps); the reduce runs the
+# slab kernel's arithmetic (n a power of two, short rows), the tile kernel's
+# (other n) or the mean kernel's (complete uniform graph)
+CASES = {
+    "dense_ring8": (synth.RING8_DENSE_LR.with_(samples=256), "ring", 2, 5, 0),
+    "dense_random12_ragged": (synth.RING8_DENSE_LR.with_(n_workers=12, dim=101, samples=203, batch=16),
+                              "random", 4, 4, 0),
+    "dense_complete6": (synth.RING8_DENSE_LR.with_(n_workers=6, samples=160), "complete", 0, 4, 0),
+    "dense_chain16": (synth.RING8_DENSE_LR.with_(n_workers=16, samples=128), "chain", 0, 4, 0),
+    "dense_root10": (synth.RING8_DENSE_LR.with_(n_workers=10, samples=128), "root", 0, 4, 0),
+    "dense_one_step_per_mix": (synth.RING8_DENSE_LR.with_(samples=128, batch=16), "ring", 2, 19, 1),
+    "wide_8w": (synth.DENSE_LR_32W.with_(n_workers=8, dim=2048, samples=192, batch=32), "random", 4, 3, 0),
+    "wide_32w_4096": (synth.DENSE_LR_32W.with_(samples=1024, batch=256), "random", 6, 3, 0),
+    "wide_3w_L3": (synth.DENSE_LR_32W.with_(n_workers=3, dim=2048, samples=72, batch=8, lr_kind="inv_sqrt",
+                                            lr0=0.2), "complete", 0, 7, 3),
+    "csr_general": (synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=600, batch=100), "random", 4, 3, 0),
+    "csr_hinge_l2": (synth.SPARSE_SVM_256W.with_(n_workers=32, dim=1 << 12, samples=560, batch=80, l2=1e-3),
+                     "random", 8, 3, 0),
+    "csr_long_rows_ring": (synth.SPARSE_LR_64W.with_(n_workers=4, dim=1 << 13, samples=240, batch=40,
+                                                     nnz_mean=200.0, zipf_s=0.9), "ring", 2, 3, 0),
+    "csr_local_steps": (synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=400, batch=100), "chain", 0,
+                        9, 2),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_run_rounds_is_bitwise_the_stream_path(torch, case):
+    wl, kind, d, R, L = CASES[case]
+    prm = params(wl, L)
+    a, _ = _session(wl, kind, d)
+    b, _ = _session(wl, kind, d)
+    for _ in range(R):
+        a.round(prm)
+    b.run_rounds(prm, R, wait_ms=3000)
+    assert b.check()[0] == asap.OK
+    assert b.current() == a.current()
+    assert np.array_equal(_bits(b), _bits(a)), case
+    # the stream-ordered path continues from the launch's state (tags included)
+    for s in (a, b):
+        s.round(prm)
+    assert a.check()[0] == asap.OK and b.check()[0] == asap.OK
+    assert np.array_equal(_bits(b), _bits(a)), case
+    # and a launch continues from a stream-ordered round
+    a.round(prm)
+    a.round(prm)
+    b.run_rounds(prm, 2, wait_ms=3000)
+    assert b.check()[0] == asap.OK
+    assert b.current() == a.current()
+    assert np.array_equal(_bits(b), _bits(a)), case
+    a.close()
+    b.close()
+
+
+@pytest.mark.parametrize("case", ["c2_shape", "c3_shape"])
+def test_run_rounds_against_the_oracle(torch, case):
+    # minibatches of at most 64 rows: the stream-ordered path would plan the
+    # pass; the launch runs the general CSR code, checked against the oracle
+    if case == "c2_shape":
+        wl, kind, d = synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=512), "random", 4
+    else:
+        wl, kind, d = synth.SPARSE_SVM_256W.with_(n_workers=16, dim=1 << 12, samples=256), "random", 8
+    R = 3
+    sess, (p, i, w) = _session(wl, kind, d)
+    sess.run_rounds(params(wl), R, wait_ms=3000)
+    assert sess.check()[0] == asap.OK
+    got = sess.models().cpu().numpy()
+    rp, col, val, yy = synth.csr_data(wl)
+    shards = csr_shards(wl, rp, col, val, yy)
+    W = np.zeros((wl.n_workers, wl.dim))
+    amb = []
+    for r in range(R):
+        halves = []
+        for k in range(wl.n_workers):
+            sched = oracle.prng.schedule(wl.samples, wl.seed, k, r)
+            _, rpk, ck, vk, yk = shards[k]
+            a = []
+            halves.append(oracle.sgd.sgd_pass_csr(W[k], rpk, ck, vk, yk, sched, rnd=r, ambiguous=a, **oracle_kw(wl)))
+            amb += a
+        W = oracle.mix.stochastic_reduce(np.stack(halves), p, i, w)
+    if amb:
+        pytest.skip(f"{len(amb)} hinge decisions within rounding of the kink; covered by the stream-path tests")
+    assert_models_close(got, W, what=case)
+    sess.close()
+
+
+def test_run_rounds_stale_start_tag_stops_and_reports(torch):
+    wl = synth.RING8_DENSE_LR.with_(samples=128)
+    prm = params(wl)
+    sess, _ = _session(wl, "ring", 2)
+    sess.round(prm)
+    buf, rnd, _ = sess.current()
+    asap.asap_debug_set_tag(sess.ctx, buf, 3, 2 * rnd - 2)  # worker 3 looks a round behind
+    sess.run_rounds(prm, 3, wait_ms=50)  # neighbours give up after 50 ms
+    st, bad = sess.check()
+    assert st == asap.E_EPOCH and 0 <= bad < wl.n_workers
+    # a restart from a known state runs again
+    sess.set_models(np.zeros((wl.n_workers, wl.dim), np.float32))
+    ref, _ = _session(wl, "ring", 2)
+    sess.run_rounds(prm, 2, wait_ms=3000)
+    ref.round(prm)
+    ref.round(prm)
+    assert sess.check()[0] == asap.OK
+    assert np.array_equal(_bits(sess), _bits(ref))
+    sess.close()
+    ref.close()
+
+
+def test_run_rounds_rejects_hubs_and_bad_arguments(torch):
+    wl = synth.RING8_DENSE_LR.with_(n_workers=70, samples=16)
+    sess, _ = _session(wl, "complete", 0)  # 70 in- and out-neighbours per worker
+    with pytest.raises(asap.AsapError) as e:
+        sess.run_rounds(params(wl), 2)
+    assert e.value.status == asap.E_STATE
+    sess.close()
+    wl = synth.RING8_DENSE_LR.with_(samples=16)
+    sess, _ = _session(wl, "ring", 2)
+    for R, ms in ((0, 0), (2, -1)):
+        with pytest.raises(asap.AsapError) as e:
+            sess.run_rounds(params(wl), R, wait_ms=ms)
+        assert e.value.status == asap.E_INVALID_ARG
+    sess.local_sgd(params(wl))
+    with pytest.raises(asap.AsapError) as e:  # a half-step is pending
+        sess.run_rounds(params(wl), 1)
+    assert e.value.status == asap.E_STATE
+    sess.close()
