@@ -219,6 +219,44 @@ def converge(wl, rounds):
     print(json.dumps(out), flush=True)
 
 
+def run_rounds_bench(sess, prm, step, args, wl, name, torch):
+    """K rounds stream-ordered (asap_prepare_sgd / asap_local_sgd /
+    asap_stochastic_reduce per round), then K rounds as one multi-round
+    launch from the state they left; both timed by the host clock between
+    device synchronisations.  The same models at the end are not expected:
+    the two runs cover different rounds (the launch continues the first)."""
+    from paper_1612_08608_amd import asap
+    K = args.steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        step()
+    torch.cuda.synchronize()
+    stream_s = time.perf_counter() - t0
+    sess.run_rounds(prm, 1)  # first launch of the kernel (code object load) outside the timing
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    sess.run_rounds(prm, K)
+    torch.cuda.synchronize()
+    launch_s = time.perf_counter() - t0
+    st, bad = sess.check()
+    if st != asap.OK:
+        raise RuntimeError(f"multi-round launch reported a stale neighbour (worker {bad})")
+    samples = wl.n_workers * wl.samples
+    planned = wl.features == "csr" and wl.batch <= 64
+    out = {"metric": "rounds/s, one multi-round launch vs stream-ordered rounds", "mode": "notify_ack",
+           "n_gpus": 1, "steps": K, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
+           "higher_is_better": True,
+           "config": {"workload": name, "workers": wl.n_workers, "dim": wl.dim, "samples_per_worker": wl.samples,
+                      "batch": wl.batch, "graph": wl.graph, "degree": wl.degree},
+           "stream_ms_per_round": stream_s / K * 1e3, "launch_ms_per_round": launch_s / K * 1e3,
+           "stream_samples_per_s": samples * K / stream_s, "launch_samples_per_s": samples * K / launch_s,
+           "speedup": stream_s / launch_s,
+           "stream_sgd_kernel": "planned CSR pass" if planned else "the launch's half-step code",
+           "launch_sgd_kernel": "general CSR pass" if wl.features == "csr" else "dense pass"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -233,6 +271,9 @@ def main():
     ap.add_argument("--converge", type=int, default=0, metavar="ROUNDS",
                     help="instead of timing: loss per round on the complete, root-expander and chain graphs "
                          "(the workload at 1/16 of its samples and dimension), and the bytes each worker sends")
+    ap.add_argument("--run-rounds", action="store_true",
+                    help="instead of the headline line: time the rounds as one multi-round launch "
+                         "(asap_run_rounds, per-worker NOTIFY-ACK) beside the same rounds stream-ordered")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="GIB")
     args = ap.parse_args()
@@ -299,6 +340,12 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.run_rounds:
+        if prm is None:
+            raise SystemExit("--run-rounds needs a workload with SGD")
+        run_rounds_bench(sess, prm, step, args, wl, name, torch)
+        sess.close()
+        return
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()

@@ -262,9 +262,9 @@ asap_status asap_round(asap_ctx* ctx, const asap_sgd_params* p, void* stream);
  *
  * Requirements: state as after a reduce or asap_set_round (no half-step
  * pending); every worker has at most 64 in-neighbours and at most 64
- * out-neighbours (self included); all workgroups of the launch fit on the
- * device at once (one per worker; K per worker for dense D in (1024, 8192]),
- * else ASAP_E_STATE.  `wait_ms` bounds each wait for a neighbour (0: 10 s).
+ * out-neighbours (self included); rows of under 2^31 bytes; all workgroups
+ * of the launch fit on the device at once (one per worker; K per worker for
+ * dense D in (1024, 8192]); else ASAP_E_STATE.  `wait_ms` bounds each wait for a neighbour (0: 10 s).
  * A wait that runs out stops that worker and, in turn, its neighbours; the
  * launch ends and asap_check reports ASAP_E_EPOCH.  The models are then
  * undefined (restore a checkpoint).  A worker whose starting tag is not the

@@ -729,6 +729,7 @@ SgdArgs sgd_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
   a.val = c->val;
   a.vmax = at<float>(c, c->off_vmax);
   a.sched = at<int32_t>(c, rp.sched);
+  a.seed = p->seed;
   a.loss = p->loss;
   a.lr_kind = p->lr_kind;
   a.lr0 = p->lr0;
@@ -821,7 +822,9 @@ hipError_t prepare_half_step(asap_ctx* c, const asap_sgd_params* p, hipStream_t 
     c->ahead_valid = false;
     const bool planned = csr_plan_fits(sgd_args(c, p, c->plan[slot]));
     if (e == hipSuccess && !hit) e = prepare_csr_round(c, p, pass, c->plan[slot], planned, s);
-  } else {
+  } else if (dense_wide_cpq(c->dim)) {
+    // the wide dense pass reads its rows' order from the schedule; the
+    // narrow one evaluates the permutation itself
     e = launch_schedule(p->seed, pass, c->n, c->S, at<int32_t>(c, c->plan[0].sched), s);
   }
   c->prep_valid = e == hipSuccess;
@@ -972,6 +975,8 @@ extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, in
   if (c->max_deg > kRoundsMaxDeg || c->max_out > kRoundsMaxDeg)
     return fail(c, ASAP_E_STATE, "a worker has %d in- and %d out-neighbours; the multi-round launch takes at most %d",
                 c->max_deg, c->max_out, kRoundsMaxDeg);
+  if (c->ld * 4 >= (int64_t(1) << 31))
+    return fail(c, ASAP_E_STATE, "the multi-round launch takes rows of under 2^31 bytes (ld = %lld)", (long long)c->ld);
   hipStream_t s = static_cast<hipStream_t>(stream);
   // the launch rewrites the schedule and row-descriptor area of plan slot 0
   drain_ahead(c);

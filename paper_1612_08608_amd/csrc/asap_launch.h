@@ -68,6 +68,7 @@ struct SgdArgs {
   int32_t max_row;         // longest row (nonzeros)
   // schedule of this round, [n][S]
   const int32_t* sched;
+  uint64_t seed;    // schedule seed (the dense pass evaluates the order itself)
   int32_t loss, lr_kind;
   float lr0, l2;
   int32_t batch;

@@ -37,10 +37,21 @@ __device__ __forceinline__ double step_size(int lr_kind, float lr0, int64_t t) {
   return lr_kind == 0 ? double(lr0) : double(lr0) / sqrt(double(t));
 }
 
-__device__ __forceinline__ double wave_sum(double v) {
+// N independent butterfly sums over the wave, level by level, so that the N
+// shuffles of a level are in flight together; every lane ends with lane 0's
+// association order.
+template <int N>
+__device__ __forceinline__ void wave_sums(double (&v)[N]) {
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-  return __shfl(v, 0, 64);  // every lane takes lane 0's association order
+  for (int off = 32; off >= 1; off >>= 1) {
+    double o[N];
+#pragma unroll
+    for (int s = 0; s < N; ++s) o[s] = __shfl_xor(v[s], off, 64);
+#pragma unroll
+    for (int s = 0; s < N; ++s) v[s] += o[s];
+  }
+#pragma unroll
+  for (int s = 0; s < N; ++s) v[s] = __shfl(v[s], 0, 64);
 }
 
 // ----------------------------------------------------------------------------
@@ -73,7 +84,10 @@ __device__ __forceinline__ void dense_pass(const SgdArgs& a, int i) {
   float* wrow = a.models + int64_t(i) * a.ld;
   const float* Xi = a.X + int64_t(i) * a.S * a.ldx;
   const float* yi = a.y + int64_t(i) * a.S;
-  const int32_t* si = a.sched + int64_t(i) * a.S;
+  // sample order of the pass: every lane evaluates the keyed permutation at
+  // one position of the step (64 at a time) and each sub-batch takes its row
+  // indices from those lanes, so no index is read from memory on the chain
+  const Perm P = perm_make(a.seed, i, a.round, uint32_t(a.S));
   float wr[CPT];
 #pragma unroll
   for (int q = 0; q < CPT; ++q) {
@@ -88,24 +102,41 @@ __device__ __forceinline__ void dense_pass(const SgdArgs& a, int i) {
     double gr[CPT];
 #pragma unroll
     for (int q = 0; q < CPT; ++q) gr[q] = 0.0;
+    int rows = 0;      // lane l: the sample at position b0 + (sb & ~63) + l ...
+    float labels = 0.f;  // ... and its label, loaded with the rows' first loads
     for (int sb = 0; sb < Bp; sb += SB) {
+      if ((sb & 63) == 0) {
+        const int u = sb + lane;
+        rows = u < Bp ? int(perm_at(P, uint32_t(b0 + u))) : 0;
+        labels = u < Bp ? yi[rows] : 0.f;
+      }
       float xr[SB][CPT];
       double d[SB];
+      int rix[SB];
+#pragma unroll
+      for (int s = 0; s < SB; ++s) rix[s] = __builtin_amdgcn_readlane(rows, (sb & 63) + s);  // SB divides 64
+      // every load is issued (out-of-range ones read row 0 / column 0 and
+      // are replaced by 0), so the sub-batch's loads are in flight together
 #pragma unroll
       for (int s = 0; s < SB; ++s) {
         const bool ok = sb + s < Bp;
-        const float* row = Xi + int64_t(ok ? si[b0 + sb + s] : 0) * a.ldx;
-        d[s] = 0.0;
+        const float* row = Xi + int64_t(ok ? rix[s] : 0) * a.ldx;
 #pragma unroll
         for (int q = 0; q < CPT; ++q) {
           const int64_t c = tid + int64_t(q) * T;
-          xr[s][q] = (ok && c < a.dim) ? row[c] : 0.f;
-          d[s] = fma(double(wr[q]), double(xr[s][q]), d[s]);
+          const bool in = ok && c < a.dim;
+          const float v = row[in ? c : 0];
+          xr[s][q] = in ? v : 0.f;
         }
       }
-      // margins: butterfly within the wave, then waves in order
 #pragma unroll
-      for (int s = 0; s < SB; ++s) d[s] = wave_sum(d[s]);
+      for (int s = 0; s < SB; ++s) {
+        d[s] = 0.0;
+#pragma unroll
+        for (int q = 0; q < CPT; ++q) d[s] = fma(double(wr[q]), double(xr[s][q]), d[s]);
+      }
+      // margins: butterfly within the wave, then waves in order
+      wave_sums<SB>(d);
       if (lane == 0) {
 #pragma unroll
         for (int s = 0; s < SB; ++s) part[wave * SB + s] = d[s];
@@ -121,7 +152,9 @@ __device__ __forceinline__ void dense_pass(const SgdArgs& a, int i) {
 #pragma unroll
       for (int s = 0; s < SB; ++s) {
         if (sb + s < Bp) {
-          const double cf = loss_coef(d[s], double(yi[si[b0 + sb + s]]), a.loss);
+          const float ys = __builtin_bit_cast(
+              float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, labels), (sb & 63) + s));
+          const double cf = loss_coef(d[s], double(ys), a.loss);
 #pragma unroll
           for (int q = 0; q < CPT; ++q) gr[q] = fma(cf, double(xr[s][q]), gr[q]);
         }
@@ -156,7 +189,7 @@ template <int CPT>
 __global__ __launch_bounds__(1024) void rounds_dense_kernel(SgdArgs a, RoundsArgs ra) {
   const int i = int(blockIdx.x);
   rounds::drive(
-      a, ra, i, 0, [&](int64_t pass) { rounds::fill_schedule(ra.seed, i, pass, a.S, ra.sched + int64_t(i) * a.S); },
+      a, ra, i, 0, [](int64_t) {},  // the pass evaluates its sample order itself
       [&](const SgdArgs& ar) {
         dense_pass<CPT>(ar, i);
         return true;

@@ -42,6 +42,17 @@ __device__ __forceinline__ void tag_release(int64_t* p, int64_t v) {
 
 __device__ __forceinline__ void acquire_fence() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
 
+// Device-coherent 16-byte load (cache policy sc1): served from memory or a
+// coherent level, never from a stale line of this XCD's L2.  The reduce
+// reads neighbours' rows this way instead of invalidating the whole L2 after
+// each wait, which would also evict the worker's shard.
+__device__ __forceinline__ float4 load_coherent(const float* row, uint32_t bytes, uint32_t off) {
+  const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(row), 0, int(bytes), 0x00020000);
+  const auto u = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16);
+  const unsigned u0 = u[0], u1 = u[1], u2 = u[2], u3 = u[3];
+  return make_float4(__uint_as_float(u0), __uint_as_float(u1), __uint_as_float(u2), __uint_as_float(u3));
+}
+
 // One thread: wait until *tag >= want or until the wall clock passes
 // `deadline`; false when the deadline passed first.
 __device__ inline bool wait_tag(const int64_t* tag, int64_t want, long long deadline) {
@@ -110,7 +121,9 @@ __device__ inline void fill_rowinfo(uint64_t seed, int i, int64_t pass, int64_t 
 // rounded once (the tile and mean kernels); else fp32 weights w_ij * s_j and
 // fp32 fused multiply-adds from +0 (the slab kernel).  Columns go in blocks
 // of kMixVec float4 per thread so that each neighbour's index and weight are
-// read once per block; no LDS (the CSR pass leaves almost none).
+// read once per block; no LDS (the CSR pass leaves almost none).  Rows and
+// scales written by other workgroups are read device-coherently (their
+// writers released them before the tags this workgroup waited for).
 constexpr int kMixVec = 4;
 
 template <bool F64>
@@ -133,16 +146,16 @@ __device__ void mix_row(const RoundsArgs& ra, int i, int e, int64_t ld, int64_t 
       float wf = ra.in_w[p0 + u];
       double wd = ra.in_w[p0 + u];
       if (scale) {
-        const float sj = scale[j];
+        const float sj = __hip_atomic_load(scale + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         wf *= sj;
         wd *= double(sj);
       }
-      const float4* row = reinterpret_cast<const float4*>(src + int64_t(j) * ld);
+      const float* row = src + int64_t(j) * ld;
 #pragma unroll
       for (int v = 0; v < kMixVec; ++v) {
         const int64_t q = q0 + v * T;
         if (q < nq) {
-          const float4 x = row[q];
+          const float4 x = load_coherent(row, uint32_t(ld) * 4u, uint32_t(q) * 16u);
           if constexpr (F64) {
             ad[v][0] = fma(wd, double(x.x), ad[v][0]);
             ad[v][1] = fma(wd, double(x.y), ad[v][1]);
@@ -222,7 +235,9 @@ __device__ void drive(SgdArgs a, const RoundsArgs& ra, int i, int member, Prepar
         const int pi = ra.in_ptr[i], po = ra.out_ptr[i];
         int miss = wait_tags(te, ra.in_idx + pi, ra.in_ptr[i + 1] - pi, tag_half(r), deadline);
         if (miss < 0) miss = wait_tags(te, ra.out_idx + po, ra.out_ptr[i + 1] - po, tag_start(r), deadline);
-        acquire_fence();
+        // no acquire fence: the reduce reads what the neighbours released
+        // with device-coherent loads (the workgroup barrier below keeps
+        // them after this wait)
         stop = miss >= 0;
         if (stop) report_stale(ra.err, i);
       }
