@@ -284,6 +284,26 @@ asap_status asap_current(const asap_ctx* ctx, int32_t* buffer, int64_t* round,
  * The schedule and step counter continue exactly from `round`. */
 asap_status asap_set_round(asap_ctx* ctx, int64_t round, int32_t buffer, void* stream);
 
+/* Reconfiguration after a failure: the graph should be easy to generate
+ * for a variable number of machines (the properties listed before
+ * Section 4), so the survivors go on with a graph built for their number.
+ * Workers dropped[0..n_drop) (ascending, distinct, 1 <= n_drop < n) leave;
+ * the others keep their current models, renumbered 0..n-n_drop-1 in their
+ * old order (the sample schedule is then keyed by the new number), and use
+ * the in-neighbour CSR (nbr_ptr, nbr_idx, nbr_w) over n - n_drop workers
+ * from the current round on (validated as in asap_create, `flags` alike).
+ * On `stream`, the surviving rows of the current buffer are copied, in
+ * order, into the other buffer, which becomes current; the round counter is
+ * kept.  The data shards were laid out per old worker, so they are
+ * unbound: bind the survivors' shards (asap_bind_dense / asap_bind_csr with
+ * n - n_drop workers) and a workspace of the new size before the next
+ * half-step.  Needs bound models and no half-step pending (ASAP_E_STATE);
+ * argument errors (ASAP_E_INVALID_ARG, ASAP_E_GRAPH) leave the context as it
+ * was.  The model buffers keep their size (the first n - n_drop rows are
+ * used). */
+asap_status asap_drop_workers(asap_ctx* ctx, int32_t n_drop, const int32_t* dropped, const int32_t* nbr_ptr,
+                              const int32_t* nbr_idx, const float* nbr_w, uint32_t flags, void* stream);
+
 /* The schedules of all workers for `round`, computed by the same device
  * code the SGD kernels use: dev_out [n][S] int32 (device).  Parity hook. */
 asap_status asap_schedule_device(asap_ctx* ctx, uint64_t seed, int64_t round,

@@ -33,7 +33,7 @@ EXPORTS = (
     "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr",
     "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_run_rounds",
     "asap_current",
-    "asap_set_round", "asap_schedule_device", "asap_metrics", "asap_check",
+    "asap_set_round", "asap_drop_workers", "asap_schedule_device", "asap_metrics", "asap_check",
     "asap_debug_set_tag", "asap_last_error", "asap_destroy",
 )
 
@@ -83,6 +83,7 @@ def lib():
         "asap_run_rounds": [p, C.POINTER(SgdParams), i64, i32, p],
         "asap_current": [p, C.POINTER(i32), C.POINTER(i64), C.POINTER(i32)],
         "asap_set_round": [p, i64, i32, p],
+        "asap_drop_workers": [p, i32, p, p, p, p, u32, p],
         "asap_schedule_device": [p, u64, i64, p, p],
         "asap_metrics": [p, i32, C.c_float, p, p],
         "asap_check": [p, p, C.POINTER(i32)],
@@ -255,6 +256,14 @@ def asap_set_round(ctx, round_: int, buffer: int, stream=None):
     _check(lib().asap_set_round(ctx, round_, buffer, _stream(stream)), ctx)
 
 
+def asap_drop_workers(ctx, dropped, ptr, idx, w, flags: int = 0, stream=None):
+    d, dp = _host(dropped, np.int32)
+    ptr, pp = _host(ptr, np.int32)
+    idx, ip = _host(idx, np.int32)
+    w, wp = _host(w, np.float32)
+    _check(lib().asap_drop_workers(ctx, int(d.size), dp, pp, ip, wp, flags, _stream(stream)), ctx)
+
+
 def asap_schedule_device(ctx, seed: int, round_: int, out, stream=None):
     _check(lib().asap_schedule_device(ctx, seed, round_, _dev(out), _stream(stream)), ctx)
 
@@ -315,6 +324,7 @@ class Session:
         self.ctx = asap_create(self.n, self.dim, ptr, idx, w, flags)
         self.bufs = [torch.zeros((self.n, self.ld), dtype=torch.float32, device=self.device) for _ in range(2)]
         self._keep = []
+        self._data = None
         self.ws = None
         asap_bind_models(self.ctx, self.bufs[0], self.bufs[1], self.ld)
 
@@ -324,7 +334,7 @@ class Session:
         t = self.torch
         W = t.as_tensor(W, dtype=t.float32)
         self.bufs[0].zero_()
-        self.bufs[0][:, :self.dim].copy_(W.to(self.device))
+        self.bufs[0][:self.n, :self.dim].copy_(W.to(self.device))
         asap_bind_models(self.ctx, self.bufs[0], self.bufs[1], self.ld, stream)
         self.ws = None
 
@@ -339,6 +349,7 @@ class Session:
         y = t.as_tensor(y, dtype=t.float32).to(self.device).contiguous()
         self._keep += [X, y]
         asap_bind_dense(self.ctx, X, y, S, ldx)
+        self._data = ("dense", X, y, S)
         self.ws = None
 
     def bind_csr(self, row_ptr, col, val, y, samples):
@@ -349,6 +360,7 @@ class Session:
         yy = t.as_tensor(np.asarray(y, np.float32)).to(self.device)
         self._keep += [rp, cl, vl, yy]
         asap_bind_csr(self.ctx, rp, cl, vl, yy, samples, int(cl.numel()))
+        self._data = ("csr", rp, cl, vl, yy, int(samples))
         self.ws = None
 
     def ready(self, stream=None):
@@ -376,6 +388,45 @@ class Session:
         """`rounds` rounds in one launch with per-worker NOTIFY-ACK."""
         asap_run_rounds(self.ready().ctx, params, rounds, wait_ms, stream)
 
+    def drop_workers(self, dropped, ptr, idx, w, flags=0, stream=None):
+        """Workers `dropped` leave (asap_drop_workers); the survivors keep
+        their models, renumbered in order, run on the graph (ptr, idx, w) and
+        have their shards bound again (device-side gathers of the bound
+        tensors)."""
+        t = self.torch
+        dropped = sorted(int(k) for k in dropped)
+        keep = [k for k in range(self.n) if k not in set(dropped)]
+        asap_drop_workers(self.ctx, dropped, ptr, idx, w, flags, stream)
+        self.n = len(keep)
+        self.ws = None
+        data, self._data = self._data, None
+        if data is None:
+            return
+        if data[0] == "dense":
+            _, X, y, S = data
+            sel = t.as_tensor(keep, dtype=t.long, device=self.device)
+            X2 = X.index_select(0, sel).contiguous()
+            y2 = y.index_select(0, sel).contiguous()
+            self._keep += [X2, y2]
+            asap_bind_dense(self.ctx, X2, y2, S, int(X2.shape[2]))
+            self._data = ("dense", X2, y2, S)
+        else:
+            _, rp, cl, vl, yy, S = data
+            rph = rp.cpu().numpy()
+            segs = [(int(rph[k * S]), int(rph[(k + 1) * S])) for k in keep]
+            cols = t.cat([cl[a:b] for a, b in segs]) if segs else cl[:0]
+            vals = t.cat([vl[a:b] for a, b in segs]) if segs else vl[:0]
+            yys = t.cat([yy[k * S:(k + 1) * S] for k in keep])
+            rp2 = np.concatenate([[0]] + [rph[k * S + 1:(k + 1) * S + 1] - rph[k * S] for k in keep])
+            off = np.concatenate([[0], np.cumsum([b - a for a, b in segs])])
+            for q in range(len(keep)):  # rows of survivor q start after the earlier survivors' nonzeros
+                rp2[q * S + 1:(q + 1) * S + 1] += off[q]
+            rp2 = t.as_tensor(rp2.astype(np.int64)).to(self.device)
+            cols, vals, yys = cols.contiguous(), vals.contiguous(), yys.contiguous()
+            self._keep += [rp2, cols, vals, yys]
+            asap_bind_csr(self.ctx, rp2, cols, vals, yys, S, int(cols.numel()))
+            self._data = ("csr", rp2, cols, vals, yys, S)
+
     # inspection ---------------------------------------------------------
     def current(self):
         return asap_current(self.ctx)
@@ -390,7 +441,7 @@ class Session:
         b, rnd, half = self.current()
         if half:
             raise RuntimeError("a checkpoint is taken between rounds, not after a half-step")
-        W = self.bufs[b][:, :self.dim].cpu().numpy()
+        W = self.bufs[b][:self.n, :self.dim].cpu().numpy()
         with open(path, "wb") as f:
             np.savez(f, models=W, round=np.int64(rnd), n=np.int64(self.n), dim=np.int64(self.dim))
 
@@ -407,7 +458,7 @@ class Session:
     def models(self):
         """Current models [n, dim] as a device view (no copy)."""
         b, _, _ = self.current()
-        return self.bufs[b][:, :self.dim]
+        return self.bufs[b][:self.n, :self.dim]
 
     def metrics(self, loss="logistic", l2=0.0):
         return asap_metrics(self.ready().ctx, loss, l2)

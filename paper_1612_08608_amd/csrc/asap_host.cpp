@@ -519,6 +519,32 @@ extern "C" asap_status asap_schedule(int64_t samples, uint64_t seed, int32_t wor
 // ============================================================================
 // context
 // ============================================================================
+namespace {
+// The graph of a context (host copy) and what is derived from it: its
+// transpose (the workers that read each row, ascending), the longest row and
+// column, and whether it is the complete graph with uniform weights.
+void set_graph(asap_ctx* c, int32_t n, const int32_t* nbr_ptr, const int32_t* nbr_idx, const float* nbr_w) {
+  c->n = n;
+  c->ptr.assign(nbr_ptr, nbr_ptr + n + 1);
+  c->idx.assign(nbr_idx, nbr_idx + nbr_ptr[n]);
+  c->w.assign(nbr_w, nbr_w + nbr_ptr[n]);
+  c->complete_uniform = is_complete_uniform(n, nbr_ptr, nbr_w);
+  c->max_deg = 0;
+  for (int32_t i = 0; i < n; ++i) c->max_deg = std::max(c->max_deg, nbr_ptr[i + 1] - nbr_ptr[i]);
+  c->optr.assign(size_t(n) + 1, 0);
+  for (int32_t p = 0; p < nbr_ptr[n]; ++p) ++c->optr[size_t(nbr_idx[p]) + 1];
+  c->max_out = 0;
+  for (int32_t j = 0; j < n; ++j) {
+    c->max_out = std::max(c->max_out, c->optr[size_t(j) + 1]);
+    c->optr[size_t(j) + 1] += c->optr[size_t(j)];
+  }
+  c->oidx.resize(size_t(nbr_ptr[n]));
+  std::vector<int32_t> fill(c->optr.begin(), c->optr.end() - 1);
+  for (int32_t i = 0; i < n; ++i)
+    for (int32_t p = nbr_ptr[i]; p < nbr_ptr[i + 1]; ++p) c->oidx[size_t(fill[size_t(nbr_idx[p])]++)] = i;
+}
+}  // namespace
+
 extern "C" asap_status asap_create(int32_t n, int64_t dim, const int32_t* nbr_ptr,
                                    const int32_t* nbr_idx, const float* nbr_w, uint32_t flags,
                                    asap_ctx** out) {
@@ -531,26 +557,8 @@ extern "C" asap_status asap_create(int32_t n, int64_t dim, const int32_t* nbr_pt
   asap_status s = check_graph(nullptr, n, nbr_ptr, nbr_idx, nbr_w, flags);
   if (s != ASAP_OK) return s;
   asap_ctx* c = new asap_ctx;
-  c->n = n;
   c->dim = dim;
-  c->ptr.assign(nbr_ptr, nbr_ptr + n + 1);
-  c->idx.assign(nbr_idx, nbr_idx + nbr_ptr[n]);
-  c->w.assign(nbr_w, nbr_w + nbr_ptr[n]);
-  c->complete_uniform = is_complete_uniform(n, nbr_ptr, nbr_w);
-  for (int32_t i = 0; i < n; ++i) c->max_deg = std::max(c->max_deg, nbr_ptr[i + 1] - nbr_ptr[i]);
-  {
-    // transpose of the graph rows: out-neighbours in ascending order
-    c->optr.assign(size_t(n) + 1, 0);
-    for (int32_t p = 0; p < nbr_ptr[n]; ++p) ++c->optr[size_t(nbr_idx[p]) + 1];
-    for (int32_t j = 0; j < n; ++j) {
-      c->max_out = std::max(c->max_out, c->optr[size_t(j) + 1]);
-      c->optr[size_t(j) + 1] += c->optr[size_t(j)];
-    }
-    c->oidx.resize(size_t(nbr_ptr[n]));
-    std::vector<int32_t> fill(c->optr.begin(), c->optr.end() - 1);
-    for (int32_t i = 0; i < n; ++i)
-      for (int32_t p = nbr_ptr[i]; p < nbr_ptr[i + 1]; ++p) c->oidx[size_t(fill[size_t(nbr_idx[p])]++)] = i;
-  }
+  set_graph(c, n, nbr_ptr, nbr_idx, nbr_w);
   layout(c);
   *out = c;
   return ASAP_OK;
@@ -1067,6 +1075,61 @@ extern "C" asap_status asap_set_round(asap_ctx* c, int64_t round, int32_t buffer
   c->round = round;
   c->half_done = false;
   c->half_scaled = false;
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_drop_workers(asap_ctx* c, int32_t n_drop, const int32_t* dropped,
+                                         const int32_t* nbr_ptr, const int32_t* nbr_idx, const float* nbr_w,
+                                         uint32_t flags, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!dropped || n_drop < 1 || n_drop >= c->n)
+    return fail(c, ASAP_E_INVALID_ARG, "drop between 1 and n - 1 = %d workers", c->n - 1);
+  for (int32_t q = 0; q < n_drop; ++q)
+    if (dropped[q] < 0 || dropped[q] >= c->n || (q > 0 && dropped[q] <= dropped[q - 1]))
+      return fail(c, ASAP_E_INVALID_ARG, "dropped workers must be ascending, distinct and in [0, %d)", c->n);
+  if (!nbr_ptr || !nbr_idx || !nbr_w) return fail(c, ASAP_E_INVALID_ARG, "NULL graph array");
+  if (flags & ~uint32_t(ASAP_ALLOW_NON_DS)) return fail(c, ASAP_E_INVALID_ARG, "unknown flags");
+  const int32_t n2 = c->n - n_drop;
+  asap_status st = check_graph(c, n2, nbr_ptr, nbr_idx, nbr_w, flags);
+  if (st != ASAP_OK) return st;
+  if (!c->buf[0]) return fail(c, ASAP_E_STATE, "bind the models first");
+  if (c->half_done) return fail(c, ASAP_E_STATE, "the half-step of round %lld is pending", (long long)c->round);
+  drain_ahead(c);
+  // survivors' rows of the current buffer, in order, into the other buffer
+  // (runs of consecutive survivors move in one copy)
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float* src = c->buf[c->cur];
+  float* dst = c->buf[c->cur ^ 1];
+  const size_t row = size_t(c->ld) * sizeof(float);
+  int32_t to = 0, q = 0;
+  for (int32_t i = 0; i < c->n;) {
+    if (q < n_drop && dropped[q] == i) {
+      ++q;
+      ++i;
+      continue;
+    }
+    int32_t j = i;
+    while (j < c->n && !(q < n_drop && dropped[q] == j)) ++j;
+    const hipError_t e = hipMemcpyAsync(dst + size_t(to) * c->ld, src + size_t(i) * c->ld, row * size_t(j - i),
+                                        hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(c, e, "model compaction");
+    to += j - i;
+    i = j;
+  }
+  c->cur ^= 1;
+  set_graph(c, n2, nbr_ptr, nbr_idx, nbr_w);
+  // the shards were laid out per worker of the old numbering
+  c->kind = kNoData;
+  c->X = nullptr;
+  c->y = nullptr;
+  c->row_ptr = nullptr;
+  c->col = nullptr;
+  c->val = nullptr;
+  c->S = 0;
+  c->nnz = 0;
+  c->half_scaled = false;
+  layout(c);
+  unbind_workspace(c);
   return ASAP_OK;
 }
 

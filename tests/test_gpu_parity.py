@@ -692,3 +692,60 @@ def test_metrics_match_oracle(torch):
     assert m[2] == pytest.approx(oracle.metrics.consensus_distance(W), rel=1e-9)
     assert m[3] == pytest.approx(W.mean(), rel=1e-9, abs=1e-15)
     sess.close()
+
+
+@pytest.mark.parametrize("features", ["dense", "csr"])
+def test_drop_workers_continues_on_the_new_graph(torch, features):
+    """Reconfiguration after a failure: two of eight workers leave after round
+    2; the six survivors, renumbered in order, continue on a ring built for
+    six from the models they hold.  The oracle runs the same trajectory on
+    its own state (its models of the survivors, the same new graph)."""
+    if features == "dense":
+        wl = synth.RING8_DENSE_LR.with_(samples=160)
+    else:
+        wl = synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=200)
+    p, i, w = graph("ring", 8, 2)
+    if features == "dense":
+        X, y = synth.dense_data(wl)
+        shards = [("dense", X[k], y[k]) for k in range(8)]
+    else:
+        rp, col, val, yy = synth.csr_data(wl)
+        shards = csr_shards(wl, rp, col, val, yy)
+    sess = asap.Session(8, wl.dim, p, i, w)
+    if features == "dense":
+        sess.bind_dense(X, y)
+    else:
+        sess.bind_csr(rp, col, val, yy, wl.samples)
+    prm = params(wl)
+    W = np.zeros((8, wl.dim))
+
+    def oracle_round(W, shards, p, i, w, r):
+        halves = []
+        for k, sh in enumerate(shards):
+            sched = oracle.prng.schedule(wl.samples, wl.seed, k, r)
+            if sh[0] == "dense":
+                halves.append(oracle.sgd.sgd_pass_dense(W[k], sh[1], sh[2], sched, rnd=r, **oracle_kw(wl)))
+            else:
+                halves.append(oracle.sgd.sgd_pass_csr(W[k], sh[1], sh[2], sh[3], sh[4], sched, rnd=r,
+                                                      **oracle_kw(wl)))
+        return oracle.mix.stochastic_reduce(np.stack(halves), p, i, w)
+
+    for r in range(2):
+        sess.round(prm)
+        W = oracle_round(W, shards, p, i, w, r)
+        assert_models_close(sess.models().cpu().numpy(), W, what=f"round {r}")
+    dropped, keep = [2, 5], [0, 1, 3, 4, 6, 7]
+    p6, i6, w6 = graph("ring", 6, 2)
+    before = sess.models().cpu().numpy().copy()
+    sess.drop_workers(dropped, p6, i6, w6)
+    assert sess.current()[1] == 2
+    # the survivors keep their models bit for bit, in order
+    assert np.array_equal(sess.models().cpu().numpy().view(np.uint32), before[keep].view(np.uint32))
+    W = W[keep]
+    shards = [shards[k] for k in keep]
+    for r in range(2, 4):
+        sess.round(prm)
+        W = oracle_round(W, shards, p6, i6, w6, r)
+        assert_models_close(sess.models().cpu().numpy(), W, what=f"round {r} after the drop")
+    assert sess.check()[0] == asap.OK
+    sess.close()

@@ -191,3 +191,29 @@ def test_model_row_stride_avoids_4k_multiples():
     for d in range(1, 5000, 37):
         ld = asap.model_ld(d)
         assert ld >= d and ld % 64 == 0 and ld % 1024 != 0 and ld - d < 64 + 128
+
+
+def test_drop_workers_validates_before_device_work():
+    p, i, w = _ring()
+    ctx = asap.asap_create(8, 100, p, i, w)
+    try:
+        p6, i6 = asap.asap_graph_ring(6)
+        w6 = asap.asap_metropolis_weights(p6, i6)
+        for bad in ([], [8], [3, 3], [5, 2], list(range(8))):      # empty, out of range, repeated, unsorted, all
+            with pytest.raises(asap.AsapError) as e:
+                asap.asap_drop_workers(ctx, bad, p6, i6, w6, stream=0)
+            assert e.value.status == asap.E_INVALID_ARG, bad
+        with pytest.raises(asap.AsapError) as e:                    # graph for 7 workers, 6 survive
+            p7, i7 = asap.asap_graph_ring(7)
+            asap.asap_drop_workers(ctx, [1, 2], p7, i7, asap.asap_metropolis_weights(p7, i7), stream=0)
+        assert e.value.status in (asap.E_GRAPH, asap.E_INVALID_ARG)
+        w_bad = w6.copy()
+        w_bad[0] += 0.25                                            # not doubly stochastic
+        with pytest.raises(asap.AsapError) as e:
+            asap.asap_drop_workers(ctx, [1, 2], p6, i6, w_bad, stream=0)
+        assert e.value.status == asap.E_GRAPH
+        with pytest.raises(asap.AsapError) as e:                    # no models bound yet
+            asap.asap_drop_workers(ctx, [1, 2], p6, i6, w6, stream=0)
+        assert e.value.status == asap.E_STATE
+    finally:
+        asap.asap_destroy(ctx)
