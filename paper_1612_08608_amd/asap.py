@@ -58,6 +58,12 @@ def lib():
     global _lib
     if _lib is not None:
         return _lib
+    # torch first when it is there: the library then binds to the HIP runtime
+    # torch has loaded instead of loading a second one beside it
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(_LIB_PATH):
         raise RuntimeError(f"{_LIB_PATH} is missing: build it with `python -m paper_1612_08608_amd.build`")
     L = C.CDLL(_LIB_PATH)
