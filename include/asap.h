@@ -200,7 +200,8 @@ asap_status asap_bind_dense(asap_ctx* ctx, const float* X, const float* y,
  * asap_bind_workspace scans the shards (synchronising its stream) and
  * rejects violations with ASAP_E_INVALID_ARG; rows may hold at most 4096
  * nonzeros.  It also ranks the columns by frequency: the most frequent
- * (up to 8128) are kept in on-chip memory during each SGD pass. */
+ * (up to 8128) are kept in on-chip memory during each SGD pass.  Shards of
+ * 2^29 or more nonzeros per worker always take the general SGD kernel. */
 asap_status asap_bind_csr(asap_ctx* ctx, const int64_t* row_ptr, const int32_t* col,
                           const float* val, const float* y, int64_t samples, int64_t nnz,
                           void* stream);

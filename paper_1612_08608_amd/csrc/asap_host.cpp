@@ -75,6 +75,7 @@ struct asap_ctx {
   std::vector<int32_t> hot_cols;
   std::vector<int16_t> hot_lut;
   int32_t max_row = 0;
+  int64_t max_wnnz = 0;  // most nonzeros of one worker's shard
 
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_optr = 0, off_oidx = 0, off_tag = 0, off_scale = 0, off_err = 0,
@@ -701,6 +702,7 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     if (last != c->nnz)
       return fail(c, ASAP_E_INVALID_ARG, "row_ptr[n*S] = %lld but nnz = %lld", (long long)last, (long long)c->nnz);
     c->max_row = int32_t(h[0]);
+    c->max_wnnz = h[5];
     asap_status hs = choose_hot_columns(c, s);
     if (hs != ASAP_OK) return hs;
     if (!c->ahead) {
@@ -769,6 +771,12 @@ SgdArgs sgd_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
   return a;
 }
 
+// The planned pass applies when its shape fits (csr_plan_fits) and a
+// worker's (code, value) pairs are addressed by 32-bit byte offsets.
+bool planned_pass(const asap_ctx* c, const SgdArgs& a) {
+  return csr_plan_fits(a) && c->max_wnnz < (int64_t(1) << 29);
+}
+
 PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
   PlanArgs pa{};
   pa.rowinfo = at<RowInfo>(c, rp.rowinfo);
@@ -828,7 +836,7 @@ hipError_t prepare_half_step(asap_ctx* c, const asap_sgd_params* p, hipStream_t 
       e = hipStreamWaitEvent(s, c->ev_ready[slot], 0);  // a miss rewrites that slot after it
     }
     c->ahead_valid = false;
-    const bool planned = csr_plan_fits(sgd_args(c, p, c->plan[slot]));
+    const bool planned = planned_pass(c, sgd_args(c, p, c->plan[slot]));
     if (e == hipSuccess && !hit) e = prepare_csr_round(c, p, pass, c->plan[slot], planned, s);
   } else if (dense_wide_cpq(c->dim)) {
     // the wide dense pass reads its rows' order from the schedule; the
@@ -871,7 +879,7 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
   const int slot = c->prep_slot;
   if (c->kind == kCsr) {
     SgdArgs a = sgd_args(c, p, c->plan[slot]);
-    const bool planned = csr_plan_fits(a);
+    const bool planned = planned_pass(c, a);
     const bool pass_ends = a.k1 == (c->S + p->batch - 1) / p->batch;
     if (planned) {
       // the general kernel runs only if the plan says a step does not fit;
