@@ -305,6 +305,17 @@ asap_status asap_set_round(asap_ctx* ctx, int64_t round, int32_t buffer, void* s
 asap_status asap_drop_workers(asap_ctx* ctx, int32_t n_drop, const int32_t* dropped, const int32_t* nbr_ptr,
                               const int32_t* nbr_idx, const float* nbr_w, uint32_t flags, void* stream);
 
+/* The graph the context runs on: as given to asap_create, or to the last
+ * asap_drop_workers (the survivors' graph).  Parity hook: the rows P_i. of
+ * update (A.2) that the reduce applies.  Host only, no stream.  Two calls:
+ * with nbr_ptr, nbr_idx and nbr_w all NULL it writes *n_workers and
+ * *n_entries only; then nbr_ptr [n+1], nbr_idx [n_entries] and nbr_w
+ * [n_entries] (host, caller-owned) receive the CSR bit for bit.  Either all
+ * three arrays or none: ASAP_E_INVALID_ARG otherwise, or when ctx,
+ * n_workers or n_entries is NULL. */
+asap_status asap_get_graph(const asap_ctx* ctx, int32_t* n_workers, int64_t* n_entries, int32_t* nbr_ptr,
+                           int32_t* nbr_idx, float* nbr_w);
+
 /* The schedules of all workers for `round`, computed by the same device
  * code the SGD kernels use: dev_out [n][S] int32 (device).  Parity hook. */
 asap_status asap_schedule_device(asap_ctx* ctx, uint64_t seed, int64_t round,

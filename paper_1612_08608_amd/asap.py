@@ -33,7 +33,7 @@ EXPORTS = (
     "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr",
     "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_run_rounds",
     "asap_current",
-    "asap_set_round", "asap_drop_workers", "asap_schedule_device", "asap_metrics", "asap_check",
+    "asap_set_round", "asap_drop_workers", "asap_get_graph", "asap_schedule_device", "asap_metrics", "asap_check",
     "asap_debug_set_tag", "asap_last_error", "asap_destroy",
 )
 
@@ -90,6 +90,7 @@ def lib():
         "asap_current": [p, C.POINTER(i32), C.POINTER(i64), C.POINTER(i32)],
         "asap_set_round": [p, i64, i32, p],
         "asap_drop_workers": [p, i32, p, p, p, p, u32, p],
+        "asap_get_graph": [p, C.POINTER(i32), C.POINTER(i64), p, p, p],
         "asap_schedule_device": [p, u64, i64, p, p],
         "asap_metrics": [p, i32, C.c_float, p, p],
         "asap_check": [p, p, C.POINTER(i32)],
@@ -268,6 +269,17 @@ def asap_drop_workers(ctx, dropped, ptr, idx, w, flags: int = 0, stream=None):
     idx, ip = _host(idx, np.int32)
     w, wp = _host(w, np.float32)
     _check(lib().asap_drop_workers(ctx, int(d.size), dp, pp, ip, wp, flags, _stream(stream)), ctx)
+
+
+def asap_get_graph(ctx):
+    """(nbr_ptr, nbr_idx, nbr_w) of the graph the context runs on (host copies)."""
+    n, m = C.c_int32(), C.c_int64()
+    _check(lib().asap_get_graph(ctx, C.byref(n), C.byref(m), None, None, None), ctx)
+    ptr = np.empty(n.value + 1, np.int32)
+    idx = np.empty(m.value, np.int32)
+    w = np.empty(m.value, np.float32)
+    _check(lib().asap_get_graph(ctx, C.byref(n), C.byref(m), ptr.ctypes.data, idx.ctypes.data, w.ctypes.data), ctx)
+    return ptr, idx, w
 
 
 def asap_schedule_device(ctx, seed: int, round_: int, out, stream=None):

@@ -1086,6 +1086,22 @@ extern "C" asap_status asap_set_round(asap_ctx* c, int64_t round, int32_t buffer
   return ASAP_OK;
 }
 
+extern "C" asap_status asap_get_graph(const asap_ctx* c, int32_t* n_workers, int64_t* n_entries, int32_t* nbr_ptr,
+                                      int32_t* nbr_idx, float* nbr_w) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!n_workers || !n_entries) return fail(nullptr, ASAP_E_INVALID_ARG, "NULL count output");
+  const int given = (nbr_ptr != nullptr) + (nbr_idx != nullptr) + (nbr_w != nullptr);
+  if (given != 0 && given != 3) return fail(nullptr, ASAP_E_INVALID_ARG, "give all three graph arrays or none");
+  *n_workers = c->n;
+  *n_entries = int64_t(c->idx.size());
+  if (given) {
+    std::copy(c->ptr.begin(), c->ptr.end(), nbr_ptr);
+    std::copy(c->idx.begin(), c->idx.end(), nbr_idx);
+    std::copy(c->w.begin(), c->w.end(), nbr_w);
+  }
+  return ASAP_OK;
+}
+
 extern "C" asap_status asap_drop_workers(asap_ctx* c, int32_t n_drop, const int32_t* dropped,
                                          const int32_t* nbr_ptr, const int32_t* nbr_idx, const float* nbr_w,
                                          uint32_t flags, void* stream) {

@@ -741,6 +741,8 @@ def test_drop_workers_continues_on_the_new_graph(torch, features):
     assert sess.current()[1] == 2
     # the survivors keep their models bit for bit, in order
     assert np.array_equal(sess.models().cpu().numpy().view(np.uint32), before[keep].view(np.uint32))
+    gp, gi, gw = asap.asap_get_graph(sess.ctx)  # the graph the reduce now applies
+    assert np.array_equal(gp, p6) and np.array_equal(gi, i6) and np.array_equal(gw, np.asarray(w6, np.float32))
     W = W[keep]
     shards = [shards[k] for k in keep]
     for r in range(2, 4):

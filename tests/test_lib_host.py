@@ -217,3 +217,48 @@ def test_drop_workers_validates_before_device_work():
         assert e.value.status == asap.E_STATE
     finally:
         asap.asap_destroy(ctx)
+
+
+def test_get_graph_returns_the_graph_bit_for_bit():
+    # the rows P_i. the reduce applies (update (A.2)), read back from the context
+    p, i = asap.asap_graph_random_regular(12, 4, 3)
+    w = asap.asap_metropolis_weights(p, i)
+    ctx = asap.asap_create(12, 100, p, i, w)
+    try:
+        gp, gi, gw = asap.asap_get_graph(ctx)
+        assert np.array_equal(gp, p) and np.array_equal(gi, i)
+        assert np.array_equal(gw.view(np.uint32), np.asarray(w, np.float32).view(np.uint32))
+        # a rejected reconfiguration leaves it as it was
+        with pytest.raises(asap.AsapError):
+            asap.asap_drop_workers(ctx, [20], p, i, w, stream=0)
+        gp2, gi2, gw2 = asap.asap_get_graph(ctx)
+        assert np.array_equal(gp2, p) and np.array_equal(gi2, i) and np.array_equal(gw2, gw)
+    finally:
+        asap.asap_destroy(ctx)
+    # a column-stochastic-only graph, accepted with ASAP_ALLOW_NON_DS, keeps its weights as given
+    p, i = asap.asap_graph_chain(5)
+    w = np.asarray(np.random.default_rng(0).uniform(0.1, 1.0, i.size), np.float32)
+    ctx = asap.asap_create(5, 10, p, i, w, asap.ALLOW_NON_DS)
+    try:
+        gp, gi, gw = asap.asap_get_graph(ctx)
+        assert np.array_equal(gp, p) and np.array_equal(gi, i) and np.array_equal(gw.view(np.uint32), w.view(np.uint32))
+    finally:
+        asap.asap_destroy(ctx)
+
+
+def test_get_graph_argument_errors():
+    import ctypes as C
+    p, i, w = _ring()
+    ctx = asap.asap_create(8, 100, p, i, w)
+    L = asap.lib()
+    n, m = C.c_int32(), C.c_int64()
+    buf = np.zeros(64, np.int32)
+    try:
+        assert L.asap_get_graph(ctx, C.byref(n), C.byref(m), None, None, None) == asap.OK
+        assert (n.value, m.value) == (8, 24)
+        assert L.asap_get_graph(ctx, None, C.byref(m), None, None, None) == asap.E_INVALID_ARG
+        assert L.asap_get_graph(ctx, C.byref(n), None, None, None, None) == asap.E_INVALID_ARG
+        assert L.asap_get_graph(ctx, C.byref(n), C.byref(m), buf.ctypes.data, None, None) == asap.E_INVALID_ARG
+        assert L.asap_get_graph(None, C.byref(n), C.byref(m), None, None, None) == asap.E_INVALID_ARG
+    finally:
+        asap.asap_destroy(ctx)
