@@ -751,3 +751,54 @@ def test_drop_workers_continues_on_the_new_graph(torch, features):
         assert_models_close(sess.models().cpu().numpy(), W, what=f"round {r} after the drop")
     assert sess.check()[0] == asap.OK
     sess.close()
+
+
+def _csr_run_against_oracle(wl, rp, col, val, yy, p, i, w, rounds):
+    """Stream-ordered rounds on the given shards, each checked against the
+    oracle started from the same state."""
+    shards = csr_shards(wl, rp, col, val, yy)
+    sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
+    sess.bind_csr(rp, col, val, yy, wl.samples)
+    prm = params(wl)
+    for r in range(rounds):
+        W = sess.models().cpu().numpy().astype(np.float64)
+        sess.round(prm)
+        assert sess.check()[0] == asap.OK
+        halves, amb = [], []
+        for k in range(wl.n_workers):
+            sched = oracle.prng.schedule(wl.samples, wl.seed, k, r)
+            _, rpk, ck, vk, yk = shards[k]
+            halves.append(oracle.sgd.sgd_pass_csr(W[k], rpk, ck, vk, yk, sched, rnd=r, ambiguous=amb,
+                                                  **oracle_kw(wl)))
+        if amb:
+            pytest.skip(f"{len(amb)} hinge decisions within rounding of the kink")
+        want = oracle.mix.stochastic_reduce(np.stack(halves), p, i, w)
+        assert_models_close(sess.models().cpu().numpy(), want, what=f"round {r}")
+    sess.close()
+
+
+@pytest.mark.parametrize("batch", [32, 100])  # planned pass, general kernel
+def test_csr_empty_rows_and_an_empty_shard(torch, batch):
+    # rows without nonzeros (margin 0: only their label and the batch size
+    # count) in every worker, and one worker whose whole shard is empty
+    wl = synth.SPARSE_LR_64W.with_(n_workers=6, dim=1 << 12, samples=300, batch=batch, nnz_mean=20.0)
+    rp, col, val, yy = synth.csr_data(wl)
+    S = wl.samples
+    keep_row = np.ones(wl.n_workers * S, bool)
+    keep_row[::7] = False              # every 7th row empty
+    keep_row[2 * S:3 * S] = False      # worker 2: no nonzeros at all
+    lens = np.diff(rp) * keep_row
+    rp2 = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    keep_nz = np.repeat(keep_row, np.diff(rp))
+    col2, val2 = col[keep_nz], val[keep_nz]
+    assert rp2[3 * S] == rp2[2 * S] and rp2[-1] == col2.size
+    p, i, w = graph("ring", wl.n_workers, 2)
+    _csr_run_against_oracle(wl, rp2, col2, val2, yy, p, i, w, 3)
+
+
+def test_single_worker_context(torch):
+    # n = 1: the graph is the worker itself (P = [1]), the reduce a copy
+    wl = synth.SPARSE_SVM_256W.with_(n_workers=1, dim=1 << 11, samples=200, l2=1e-3)
+    rp, col, val, yy = synth.csr_data(wl)
+    p, i, w = np.array([0, 1], np.int32), np.array([0], np.int32), np.array([1.0], np.float32)
+    _csr_run_against_oracle(wl, rp, col, val, yy, p, i, w, 3)

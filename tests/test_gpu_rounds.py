@@ -174,3 +174,43 @@ def test_run_rounds_rejects_hubs_and_bad_arguments(torch):
         sess.run_rounds(params(wl), 1)
     assert e.value.status == asap.E_STATE
     sess.close()
+
+
+def _empty_row_csr(wl):
+    """The workload's shards with every 7th row emptied and worker 1's shard
+    empty altogether."""
+    rp, col, val, yy = synth.csr_data(wl)
+    S = wl.samples
+    keep_row = np.ones(wl.n_workers * S, bool)
+    keep_row[::7] = False
+    keep_row[S:2 * S] = False
+    lens = np.diff(rp) * keep_row
+    rp2 = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    keep_nz = np.repeat(keep_row, np.diff(rp))
+    return rp2, col[keep_nz], val[keep_nz], yy
+
+
+@pytest.mark.parametrize("case", ["empty_rows", "single_worker"])
+def test_run_rounds_edge_cases_match_the_stream_path(torch, case):
+    if case == "empty_rows":
+        wl = synth.SPARSE_LR_64W.with_(n_workers=4, dim=1 << 12, samples=150, batch=100, nnz_mean=20.0)
+        data = _empty_row_csr(wl)
+        p, i, w = graph("ring", wl.n_workers, 2)
+    else:
+        wl = synth.SPARSE_SVM_256W.with_(n_workers=1, dim=1 << 11, samples=160, batch=40, l2=1e-3)
+        data = synth.csr_data(wl)
+        p, i, w = np.array([0, 1], np.int32), np.array([0], np.int32), np.array([1.0], np.float32)
+    prm = params(wl)
+    runs = []
+    for launch in (False, True):
+        sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
+        sess.bind_csr(*data, wl.samples)
+        if launch:
+            sess.run_rounds(prm, 3, wait_ms=3000)
+        else:
+            for _ in range(3):
+                sess.round(prm)
+        assert sess.check()[0] == asap.OK
+        runs.append(_bits(sess))
+        sess.close()
+    assert np.array_equal(runs[0], runs[1]), case
