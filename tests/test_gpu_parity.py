@@ -176,7 +176,8 @@ def test_ring8_dense_full_workload_every_round_and_loss_curve(torch):
 
 
 @pytest.mark.parametrize("n,dim,S,B,l2", [(4, 100, 50, 7, 0.0), (3, 1000, 64, 64, 0.01), (5, 4096, 300, 256, 0.0),
-                                         (3, 16384, 20, 3, 0.0), (4, 5, 9, 2, 0.1)])
+                                         (3, 16384, 20, 3, 0.0), (4, 5, 9, 2, 0.1),
+                                         (1, 1, 3, 1, 0.0), (2, 3, 1, 1, 0.05)])  # one worker, one feature; one sample
 def test_dense_shapes(torch, n, dim, S, B, l2):
     wl = synth.DENSE_LR_32W.with_(n_workers=n, dim=dim, samples=S, batch=B, l2=l2, lr_kind="inv_sqrt", lr0=0.3)
     W0 = synth.initial_models(wl.with_(seed=3)) * np.float32(0.01)
