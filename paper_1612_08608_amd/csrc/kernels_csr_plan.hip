@@ -13,8 +13,11 @@
 //    order (its region in the per-nonzero plan arrays);
 //  * csr_plan: per (worker, step), the distinct cold columns (slots 0..Uc-1,
 //    in `clist`), the distinct hot slots (`hlist`), and for every nonzero
-//    its "code" for this round, -(hot slot + 2) or its cold slot, packed
-//    with its value so that the pass loads both at once;
+//    its "code" for this round, -(hot slot + 2) or its cold slot: the first
+//    half of a (code, value) pair, so that the pass loads both at once (the
+//    value halves do not change from round to round and are written at
+//    bind, which keeps that traffic away from the pass the planning runs
+//    beside);
 //  * csr_link: per (worker, step), the slot each cold column had in the
 //    previous step, or -1.
 //
@@ -185,7 +188,6 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
   // every code of the step in registers (rows of at most 64 H nonzeros: H
   // per lane), all loads issued before any is used; -1 marks no entry
   int cc[kRowsPerWave][H];
-  float vv[kRowsPerWave][H];
 #pragma unroll
   for (int j = 0; j < kRowsPerWave; ++j) {
     const int b = wave + j * NW;
@@ -195,7 +197,6 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
     for (int h = 0; h < H; ++h) {
       const int e = lane + 64 * h;
       cc[j][h] = e < len ? p.code[st + e] : -1;
-      vv[j][h] = e < len ? p.val[st + e] : 0.f;
     }
   }
 #pragma unroll
@@ -245,7 +246,9 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
         const int pos = table_find(keys, bits, c);
         out = pos >= 0 ? int(ids[pos]) : 0;
       }
-      p.pack[rstart[b] + lane + 64 * h] = make_int2(out, __float_as_int(vv[j][h]));
+      // the code half of the (code, value) pair; the value halves are
+      // written once, at bind
+      reinterpret_cast<int*>(p.pack + rstart[b] + lane + 64 * h)[0] = out;
     }
   }
   if (t == 0) {
@@ -691,6 +694,11 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   }
 }
 
+__global__ void pack_values_kernel(const float* __restrict__ val, int64_t nnz, int2* __restrict__ pack) {
+  for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < nnz; q += int64_t(gridDim.x) * blockDim.x)
+    reinterpret_cast<int*>(pack + q)[1] = __float_as_int(val[q]);
+}
+
 template <int E>
 hipError_t launch_fast_e(const SgdArgs& a, const PlanArgs& p, hipStream_t s) {
   // with helpers, block n + i prefetches for block i: the same XCD when n is
@@ -736,6 +744,13 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
     hipLaunchKernelGGL(csr_link_kernel<256>, dim3(blocks), dim3(256), 0, s, p);
   else
     hipLaunchKernelGGL(csr_link_kernel<kPlanThreads>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_values(const float* val, int64_t nnz, int2* pack, hipStream_t s) {
+  if (nnz <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((nnz + 255) / 256, 65536);
+  hipLaunchKernelGGL(pack_values_kernel, dim3(uint32_t(blocks)), dim3(256), 0, s, val, nnz, pack);
   return hipGetLastError();
 }
 
