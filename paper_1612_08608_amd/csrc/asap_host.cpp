@@ -705,10 +705,11 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     c->max_wnnz = h[5];
     asap_status hs = choose_hot_columns(c, s);
     if (hs != ASAP_OK) return hs;
-    // the value half of every planned (code, value) pair does not change
-    // from round to round: written here, once per plan slot
+    // the value half of every planned (code, value) pair, and the code half
+    // of a hot entry, do not change from round to round: written here, once
+    // per plan slot (planning rewrites the cold entries' codes)
     for (int k = 0; k < 2; ++k)
-      if ((e = launch_pack_values(c->val, c->nnz, at<int2>(c, c->plan[k].pack), s)))
+      if ((e = launch_pack_values(at<int32_t>(c, c->off_code), c->val, c->nnz, at<int2>(c, c->plan[k].pack), s)))
         return hip_fail(c, e, "plan values");
     if (!c->ahead) {
       if ((e = hipStreamCreateWithFlags(&c->ahead, hipStreamNonBlocking))) {

@@ -105,8 +105,9 @@ struct PlanArgs {
 };
 bool csr_plan_fits(const SgdArgs& a);
 hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s);
-// pack[q].y = bits of val[q] for every nonzero: the round-invariant half of the plan
-hipError_t launch_pack_values(const float* val, int64_t nnz, int2* pack, hipStream_t s);
+// pack[q] = (code[q], bits of val[q]) for every nonzero: the round-invariant
+// part of the plan (the planning kernel rewrites the cold entries' codes)
+hipError_t launch_pack_values(const int32_t* code, const float* val, int64_t nnz, int2* pack, hipStream_t s);
 hipError_t launch_sgd_csr_fast(const SgdArgs& a, const PlanArgs& p, hipStream_t s);
 
 hipError_t launch_schedule(uint64_t seed, int64_t round, int32_t n, int64_t S, int32_t* out,

@@ -15,9 +15,9 @@
 //    in `clist`), the distinct hot slots (`hlist`), and for every nonzero
 //    its "code" for this round, -(hot slot + 2) or its cold slot: the first
 //    half of a (code, value) pair, so that the pass loads both at once (the
-//    value halves do not change from round to round and are written at
-//    bind, which keeps that traffic away from the pass the planning runs
-//    beside);
+//    values and the hot entries' codes do not change from round to round and
+//    are written at bind, which keeps that traffic away from the pass the
+//    planning runs beside);
 //  * csr_link: per (worker, step), the slot each cold column had in the
 //    previous step, or -1.
 //
@@ -246,9 +246,10 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
         const int pos = table_find(keys, bits, c);
         out = pos >= 0 ? int(ids[pos]) : 0;
       }
-      // the code half of the (code, value) pair; the value halves are
+      // the code half of a cold entry's (code, value) pair: a hot entry's
+      // code and every value do not change from round to round and are
       // written once, at bind
-      reinterpret_cast<int*>(p.pack + rstart[b] + lane + 64 * h)[0] = out;
+      if (!is_hot(c)) reinterpret_cast<int*>(p.pack + rstart[b] + lane + 64 * h)[0] = out;
     }
   }
   if (t == 0) {
@@ -694,9 +695,10 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   }
 }
 
-__global__ void pack_values_kernel(const float* __restrict__ val, int64_t nnz, int2* __restrict__ pack) {
+__global__ void pack_values_kernel(const int32_t* __restrict__ code, const float* __restrict__ val, int64_t nnz,
+                                   int2* __restrict__ pack) {
   for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < nnz; q += int64_t(gridDim.x) * blockDim.x)
-    reinterpret_cast<int*>(pack + q)[1] = __float_as_int(val[q]);
+    pack[q] = make_int2(code[q], __float_as_int(val[q]));
 }
 
 template <int E>
@@ -747,10 +749,10 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_pack_values(const float* val, int64_t nnz, int2* pack, hipStream_t s) {
+hipError_t launch_pack_values(const int32_t* code, const float* val, int64_t nnz, int2* pack, hipStream_t s) {
   if (nnz <= 0) return hipSuccess;
   const int64_t blocks = std::min<int64_t>((nnz + 255) / 256, 65536);
-  hipLaunchKernelGGL(pack_values_kernel, dim3(uint32_t(blocks)), dim3(256), 0, s, val, nnz, pack);
+  hipLaunchKernelGGL(pack_values_kernel, dim3(uint32_t(blocks)), dim3(256), 0, s, code, val, nnz, pack);
   return hipGetLastError();
 }
 
