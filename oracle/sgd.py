@@ -24,8 +24,15 @@ step-size schedule; these come from the workload definitions):
   q = (r L) div K and k0 = (r L) mod K (`round_steps`), and t counts
   q K + k + 1.
 
+With l2 > 0 the update multiplies every entry of w by (1 - eta_t l2) each
+step.  `sgd_pass_csr_scaled` writes w = s v (Bottou's trick for SVM-SGD, which
+Section 6 uses) so a step touches only the minibatch's columns: s <- s (1 -
+eta_t l2), v_j <- v_j - (eta_t / s) g_j over the batch's columns.  It is the
+same update up to fp64 rounding and exists to make full-size oracle runs fast.
+
 Pins: closed forms at m = 0, central finite differences of the loss on tiny
-inputs, a hand-computed step, the dense-vs-CSR agreement on the same data.
+inputs, a hand-computed step, the dense-vs-CSR agreement on the same data, the
+scale form against the plain dense decay (1e-12).
 """
 from __future__ import annotations
 
@@ -89,14 +96,13 @@ def sgd_pass_dense(w0, X, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd, steps
     steps = (k0, k1) runs only steps k0 .. k1 - 1 of the pass.
     """
     w = np.asarray(w0, np.float64).copy()
-    X = np.asarray(X, np.float64)
     y = np.asarray(y, np.float64)
     S = X.shape[0]
     K = n_steps(S, batch)
     k0, k1 = (0, K) if steps is None else steps
     for k in range(k0, k1):
         rows = sched[k * batch:min((k + 1) * batch, S)]
-        xb, yb = X[rows], y[rows]
+        xb, yb = np.asarray(X[rows], np.float64), y[rows]
         m = xb @ w
         c = loss_coef(m, yb, loss)
         g = (c @ xb) / len(rows) + l2 * w
@@ -138,9 +144,45 @@ def sgd_pass_csr(w0, row_ptr, col, val, y, sched, *, batch, loss, lr_kind, lr0, 
     return w
 
 
+def sgd_pass_csr_scaled(w0, row_ptr, col, val, y, sched, *, batch, loss, lr_kind, lr0, l2, rnd,
+                        ambiguous=None, steps=None):
+    """`sgd_pass_csr` with w kept as s * v, so that the L2 decay of a step is
+    one multiplication of s; returns the new model s * v (fp64).  The margins,
+    the hinge ambiguity test and the data gradient are those of `sgd_pass_csr`
+    evaluated at w = s v."""
+    v = np.asarray(w0, np.float64).copy()
+    s = 1.0
+    row_ptr = np.asarray(row_ptr, np.int64)
+    S = len(row_ptr) - 1
+    K = n_steps(S, batch)
+    k0, k1 = (0, K) if steps is None else steps
+    for k in range(k0, k1):
+        rows = np.asarray(sched[k * batch:min((k + 1) * batch, S)], np.int64)
+        lo, lens = row_ptr[rows], row_ptr[rows + 1] - row_ptr[rows]
+        seg = np.repeat(np.arange(len(rows)), lens)
+        pos = np.arange(lens.sum()) - np.repeat(np.cumsum(lens) - lens, lens) + np.repeat(lo, lens)
+        cols, vals = col[pos], val[pos].astype(np.float64)
+        prod = vals * (s * v[cols])
+        m = np.bincount(seg, weights=prod, minlength=len(rows))
+        yb = y[rows].astype(np.float64)
+        if ambiguous is not None and loss == HINGE:
+            absum = np.bincount(seg, weights=np.abs(prod), minlength=len(rows))
+            hit = np.abs(yb * m - 1.0) <= 1e-5 * (1.0 + absum)
+            ambiguous.extend(int(r) for r in rows[hit])
+        c = loss_coef(m, yb, loss)
+        eta = step_size(lr_kind, lr0, rnd * K + k + 1)
+        s = s * (1.0 - eta * l2)
+        np.add.at(v, cols, -(eta / s) * (c[seg] * vals / len(rows)))
+    return s * v
+
+
 def objective_dense(w, X, y, loss, l2) -> float:
-    """f_i(w) on a dense shard (fp64)."""
-    m = np.asarray(X, np.float64) @ np.asarray(w, np.float64)
+    """f_i(w) on a dense shard (fp64; the margins are formed 4096 rows at a
+    time so that a large fp32 shard is never copied to fp64 whole)."""
+    w = np.asarray(w, np.float64)
+    m = np.empty(X.shape[0])
+    for r0 in range(0, X.shape[0], 4096):
+        m[r0:r0 + 4096] = np.asarray(X[r0:r0 + 4096], np.float64) @ w
     return float(np.mean(loss_value(np.asarray(y, np.float64) * m, loss))
                  + 0.5 * l2 * np.dot(w, w))
 
@@ -157,22 +199,7 @@ def margins_csr(w, row_ptr, col, val) -> np.ndarray:
 
 def objective_csr(w, row_ptr, col, val, y, loss, l2) -> float:
     """f_i(w) on a CSR shard (fp64)."""
-    m = margins_csr(w, row_ptr, col, val)
     w = np.asarray(w, np.float64)
+    m = margins_csr(w, row_ptr, col, val)
     return float(np.mean(loss_value(np.asarray(y, np.float64) * m, loss))
                  + 0.5 * l2 * np.dot(w, w))
-
-
-def ambiguous_hinge_rows(w, row_ptr, col, val, y, rows, rel=1e-5):
-    """Rows whose hinge decision y m < 1 could flip under fp32 rounding.
-
-    A row is ambiguous when |y m - 1| <= rel * (1 + sum_j |w_j x_j|).
-    """
-    w = np.asarray(w, np.float64)
-    out = []
-    for r in rows:
-        lo, hi = row_ptr[r], row_ptr[r + 1]
-        prod = val[lo:hi].astype(np.float64) * w[col[lo:hi]]
-        if abs(y[r] * prod.sum() - 1.0) <= rel * (1.0 + np.abs(prod).sum()):
-            out.append(r)
-    return out

@@ -181,3 +181,41 @@ def test_sgd_decreases_objective_on_separable_data():
                                lr_kind="const", lr0=0.5, l2=0.0, rnd=r)
     assert sgd.objective_dense(w, X, y, "logistic", 0.0) < 0.5 * f0
     assert np.mean(np.sign(X @ w) == y) > 0.95
+
+
+@pytest.mark.parametrize("loss,l2,lr_kind", [("hinge", 1e-2, "inv_sqrt"), ("logistic", 0.3, "const"),
+                                             ("logistic", 0.0, "inv_sqrt")])
+def test_scale_form_equals_dense_decay(loss, l2, lr_kind):
+    # w = s v with s <- s (1 - eta l2) is the update w <- (1 - eta l2) w - eta g
+    # written differently: the plain dense decay of the dense pass fixes it
+    S, D, B = 41, 11, 5
+    X = RNG.standard_normal((S, D)).astype(np.float32)
+    X[RNG.random((S, D)) < 0.5] = 0.0
+    X[:, 2] = np.where(RNG.random(S) < 0.7, 0.8, 0.0)      # repeated column inside a batch
+    y = np.where(RNG.random(S) < 0.5, -1.0, 1.0).astype(np.float32)
+    rp, col, val = _dense_to_csr(X)
+    sched = prng.schedule(S, 3, 1, 2)
+    w0 = 0.05 * RNG.standard_normal(D)
+    kw = dict(batch=B, loss=loss, lr_kind=lr_kind, lr0=0.4, l2=l2, rnd=2)
+    want = sgd.sgd_pass_dense(w0, X, y, sched, **kw)
+    got = sgd.sgd_pass_csr_scaled(w0, rp, col, val, y, sched, **kw)
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-14)
+    amb_a, amb_b = [], []
+    sgd.sgd_pass_csr(w0, rp, col, val, y, sched, ambiguous=amb_a, **kw)
+    sgd.sgd_pass_csr_scaled(w0, rp, col, val, y, sched, ambiguous=amb_b, **kw)
+    assert amb_a == amb_b
+    # a step range of the scaled pass continues from the model it was given
+    mid = sgd.sgd_pass_csr_scaled(w0, rp, col, val, y, sched, steps=(0, 4), **kw)
+    end = sgd.sgd_pass_csr_scaled(mid, rp, col, val, y, sched, steps=(4, sgd.n_steps(S, B)), **kw)
+    assert np.allclose(end, want, rtol=1e-12, atol=1e-14)
+
+
+def test_scale_form_shrinks_untouched_columns():
+    # a column no sample touches decays by prod_t (1 - eta_t l2): hand-computed
+    X = np.array([[1.0, 0.0], [0.5, 0.0]], np.float32)
+    y = np.array([1.0, -1.0], np.float32)
+    rp, col, val = _dense_to_csr(X)
+    w0 = np.array([0.0, 2.0])
+    out = sgd.sgd_pass_csr_scaled(w0, rp, col, val, y, np.array([0, 1]), batch=1, loss="hinge",
+                                  lr_kind="const", lr0=0.5, l2=0.1, rnd=0)
+    assert out[1] == pytest.approx(2.0 * 0.95 * 0.95, rel=1e-15)
