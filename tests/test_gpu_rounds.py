@@ -12,7 +12,7 @@ import pytest
 from conftest import assert_models_close
 from paper_1612_08608_amd import asap, synth
 import oracle
-from test_gpu_parity import graph, params, oracle_kw, csr_shards
+from test_gpu_parity import graph, params, oracle_kw, csr_shards, ambiguity_mask
 
 pytestmark = pytest.mark.gpu
 
@@ -110,27 +110,34 @@ def test_run_rounds_against_the_oracle(torch, case):
         wl, kind, d = synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=512), "random", 4
     else:
         wl, kind, d = synth.SPARSE_SVM_256W.with_(n_workers=16, dim=1 << 12, samples=256), "random", 8
+    # the oracle first: if a round has hinge decisions within rounding of the
+    # kink, the launch covers the rounds up to and including it and that
+    # round is compared outside the entries those decisions can change
     R = 3
-    sess, (p, i, w) = _session(wl, kind, d)
-    sess.run_rounds(params(wl), R, wait_ms=3000)
-    assert sess.check()[0] == asap.OK
-    got = sess.models().cpu().numpy()
+    p, i, w = graph(kind, wl.n_workers, d)
     rp, col, val, yy = synth.csr_data(wl)
     shards = csr_shards(wl, rp, col, val, yy)
     W = np.zeros((wl.n_workers, wl.dim))
-    amb = []
+    mask = None
     for r in range(R):
-        halves = []
+        halves, amb = [], []
         for k in range(wl.n_workers):
             sched = oracle.prng.schedule(wl.samples, wl.seed, k, r)
             _, rpk, ck, vk, yk = shards[k]
             a = []
             halves.append(oracle.sgd.sgd_pass_csr(W[k], rpk, ck, vk, yk, sched, rnd=r, ambiguous=a, **oracle_kw(wl)))
-            amb += a
+            amb += [(k, q) for q in a]
         W = oracle.mix.stochastic_reduce(np.stack(halves), p, i, w)
-    if amb:
-        pytest.skip(f"{len(amb)} hinge decisions within rounding of the kink; covered by the stream-path tests")
-    assert_models_close(got, W, what=case)
+        if amb:
+            mask = ambiguity_mask(amb, shards, p, i, W.shape)
+            print(f"round {r}: {len(amb)} ambiguous hinge rows; the launch runs {r + 1} rounds", flush=True)
+            R = r + 1
+            break
+    sess, _ = _session(wl, kind, d)
+    sess.run_rounds(params(wl), R, wait_ms=3000)
+    assert sess.check()[0] == asap.OK
+    assert sess.current()[1] == R
+    assert_models_close(sess.models().cpu().numpy(), W, what=f"{case} after {R} rounds", mask=mask)
     sess.close()
 
 
