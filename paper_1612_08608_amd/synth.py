@@ -12,10 +12,12 @@ available here; the synthetic shards below stand in for them:
 
 * dense shards: x ~ N(0, I) (optionally a fixed subset of columns scaled x10),
   labels y = sign(<x, w*>) with sign(0) = +1 and i.i.d. label flips;
-* CSR shards: per row k ~ max(Poisson(lambda), 1) column draws, ranks from a
-  Zipf(s) law truncated to [1, D], mapped to columns by the bijection
-  col = ((rank - 1) * 2654435761) mod D, de-duplicated and sorted; values are
-  lognormal(0, 1) per unique column or 1 (binary); each row is L2-normalised;
+* CSR shards: per row k = min(max(Poisson(lambda), 1), D) nonzeros, so that a
+  row's nonzero count follows Poisson(lambda); the columns are the first k
+  distinct ones of the row's stream of draws, ranks from a Zipf(s) law
+  truncated to [1, D], mapped to columns by the bijection
+  col = ((rank - 1) * 2654435761) mod D, then sorted; values are
+  lognormal(0, 1) per column or 1 (binary); each row is L2-normalised;
   labels from a planted w* ~ N(0, I) as above.
 
 Every worker's shard is a pure function of (seed, worker), so any worker can be
@@ -58,7 +60,7 @@ class Workload:
     features: str = "dense"  # "dense" | "csr" | "none"
     flip: float = 0.05
     scaled_frac: float = 0.0  # dense: fraction of columns scaled x10
-    nnz_mean: float = 0.0     # csr: Poisson mean of column draws per row
+    nnz_mean: float = 0.0     # csr: Poisson mean of nonzeros per row
     zipf_s: float = 1.0       # csr: Zipf exponent of column ranks
     values: str = "lognormal"  # csr: "lognormal" | "binary"
     seed: int = 0
@@ -177,12 +179,39 @@ def csr_shard(wl: Workload, worker: int, cdf=None, wstar=None):
     cdf = zipf_cdf(D, wl.zipf_s) if cdf is None else cdf
     wstar = csr_planted(wl) if wstar is None else wstar
     rng = np.random.default_rng([wl.seed, _TAG_CSR, 1, worker])
-    k = np.maximum(rng.poisson(wl.nnz_mean, S), 1)
-    u = rng.random(int(k.sum()))
-    rank = np.minimum(np.searchsorted(cdf, u, side="right"), D - 1)  # rank - 1
-    colraw = (rank.astype(np.int64) * RANK_SCRAMBLE) % D
-    rows = np.repeat(np.arange(S, dtype=np.int64), k)
-    keys = np.unique(rows * D + colraw)
+    k = np.minimum(np.maximum(rng.poisson(wl.nnz_mean, S), 1), D)
+
+    def draw(m):
+        rank = np.minimum(np.searchsorted(cdf, rng.random(m), side="right"), D - 1)  # rank - 1
+        return (rank.astype(np.int64) * RANK_SCRAMBLE) % D
+
+    # first pass: 2k + 32 draws per row; keep each row's first k distinct
+    # columns in draw order
+    pool = 2 * k + 32
+    rows = np.repeat(np.arange(S, dtype=np.int64), pool)
+    keys, first = np.unique(rows * D + draw(int(pool.sum())), return_index=True)
+    urow = keys // D
+    order = np.lexsort((first, urow))
+    urow_o = urow[order]
+    have = np.bincount(urow, minlength=S)
+    start = np.concatenate([[0], np.cumsum(have)[:-1]])
+    within = np.arange(keys.size) - start[urow_o]
+    keep = order[within < k[urow_o]]
+    keys = np.sort(keys[keep])
+    # rows whose pool held fewer than k distinct columns draw on, one by one
+    short = np.nonzero(have < k)[0]
+    if short.size:
+        extra = []
+        for r in short:
+            seen = list(dict.fromkeys(int(c) for c in np.sort(keys[keys // D == r]) - r * D))
+            seen_set = set(seen)
+            while len(seen) < k[r]:
+                for c in draw(2 * int(k[r] - len(seen)) + 32):
+                    if int(c) not in seen_set and len(seen) < k[r]:
+                        seen_set.add(int(c))
+                        seen.append(int(c))
+            extra.append(np.int64(r) * D + np.array(seen, np.int64))
+        keys = np.sort(np.concatenate([keys[~np.isin(keys // D, short)], *extra]))
     urow = keys // D
     col = (keys - urow * D).astype(np.int32)
     counts = np.bincount(urow, minlength=S)
