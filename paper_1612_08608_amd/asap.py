@@ -485,9 +485,14 @@ class Session:
         return asap_check(self.ctx)
 
     def close(self):
+        """Ordered teardown: wait for the device, destroy the context (which
+        waits for its look-ahead stream and releases its stream and events),
+        then drop the device memory the context used."""
         if self.ctx:
+            self.torch.cuda.synchronize(self.device)
             asap_destroy(self.ctx)
             self.ctx = None
+        self.bufs, self.ws, self._keep, self._data = [], None, [], None
 
     def __del__(self):
         try:

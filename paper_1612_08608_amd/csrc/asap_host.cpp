@@ -156,7 +156,7 @@ void layout(asap_ctx* c) {
   c->off_rowok = o; o = align_up(o + n * 4);
   c->plan[0].sched = o; o = align_up(o + n * size_t(c->S) * 4);
   c->off_wbar = o;  o = align_up(o + size_t(c->dim) * 8);
-  c->off_part = o;  o = align_up(o + (2 * 4096 + 3 * n) * 8);
+  c->off_part = o;  o = align_up(o + metric_part_doubles(int64_t(n), c->S) * 8);
   c->off_out = o;   o = align_up(o + 8 * 8);
   const bool csr = c->kind == kCsr;
   c->off_code = o;    o = align_up(o + (csr ? size_t(c->nnz) * 4 : 0));
@@ -1173,29 +1173,43 @@ extern "C" asap_status asap_schedule_device(asap_ctx* c, uint64_t seed, int64_t 
   return ASAP_OK;
 }
 
-extern "C" asap_status asap_metrics(asap_ctx* c, int32_t loss, float l2, double* out, void* stream) {
+namespace {
+
+// Checks and the kernel arguments shared by asap_metrics and
+// asap_metrics_noalloc; the scratch pointers (w_bar, partials, results) are
+// left for the caller.
+asap_status metric_args(asap_ctx* c, int32_t loss, float l2, const double* out, MetricArgs* a) {
   if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
   if (!out) return fail(c, ASAP_E_INVALID_ARG, "out is NULL");
   if (loss != ASAP_LOSS_LOGISTIC && loss != ASAP_LOSS_HINGE) return fail(c, ASAP_E_INVALID_ARG, "unknown loss");
   if (!(std::isfinite(l2) && l2 >= 0.0f)) return fail(c, ASAP_E_INVALID_ARG, "l2 must be >= 0");
   asap_status st = need_device(c);
   if (st != ASAP_OK) return st;
+  *a = MetricArgs{};
+  a->W = c->buf[c->cur];
+  a->ld = c->ld;
+  a->dim = c->dim;
+  a->n = c->n;
+  a->scale = c->half_scaled ? at<float>(c, c->off_scale) : nullptr;
+  a->S = c->kind == kNoData ? 0 : c->S;
+  a->y = c->y;
+  a->X = c->X;
+  a->ldx = c->ldx;
+  a->row_ptr = c->row_ptr;
+  a->col = c->col;
+  a->val = c->val;
+  a->loss = loss;
+  a->l2 = l2;
+  return ASAP_OK;
+}
+
+}  // namespace
+
+extern "C" asap_status asap_metrics(asap_ctx* c, int32_t loss, float l2, double* out, void* stream) {
+  MetricArgs a;
+  asap_status st = metric_args(c, loss, l2, out, &a);
+  if (st != ASAP_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  MetricArgs a{};
-  a.W = c->buf[c->cur];
-  a.ld = c->ld;
-  a.dim = c->dim;
-  a.n = c->n;
-  a.scale = c->half_scaled ? at<float>(c, c->off_scale) : nullptr;
-  a.S = c->kind == kNoData ? 0 : c->S;
-  a.y = c->y;
-  a.X = c->X;
-  a.ldx = c->ldx;
-  a.row_ptr = c->row_ptr;
-  a.col = c->col;
-  a.val = c->val;
-  a.loss = loss;
-  a.l2 = l2;
   a.wbar = at<double>(c, c->off_wbar);
   a.part = at<double>(c, c->off_part);
   a.out = at<double>(c, c->off_out);

@@ -200,9 +200,23 @@ struct MetricArgs {
   int32_t loss;
   float l2;
   double* wbar;     // [dim]
-  double* part;     // partial sums: 2 * 4096 column-block + 3 * n worker doubles
+  double* part;     // partial sums: metric_part_doubles(n, S)
   double* out;      // [4] device
 };
+
+// The loss pass splits each worker's samples (and model entries) over
+// metric_chunks(n, S) workgroups, so that about 2048 workgroups share the
+// data however few workers there are.
+constexpr int kMetricColBlocks = 4096;
+inline int metric_chunks(int64_t n, int64_t S) {
+  int64_t c = n >= 2048 ? 1 : 2048 / n;
+  if (c > 64) c = 64;
+  if (S > 0 && c > S) c = S;
+  return int(c < 1 ? 1 : c);
+}
+inline size_t metric_part_doubles(int64_t n, int64_t S) {
+  return size_t(2 * kMetricColBlocks) + 3 * size_t(n) * size_t(metric_chunks(n, S));
+}
 hipError_t launch_metrics(const MetricArgs& a, hipStream_t s);
 
 }  // namespace asap

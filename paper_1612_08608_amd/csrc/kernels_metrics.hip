@@ -12,7 +12,7 @@
 namespace asap {
 namespace {
 
-constexpr int kColBlocksMax = 4096;  // partials 0 .. 2*kColBlocksMax
+constexpr int kColBlocksMax = kMetricColBlocks;  // partials 0 .. 2*kColBlocksMax
 
 __device__ __forceinline__ double wave_sum_d(double v) {
 #pragma unroll
@@ -68,12 +68,15 @@ __device__ __forceinline__ double loss_of(double ym, int loss) {
   return fmax(-ym, 0.0) + log1p(exp(-fabs(ym)));  // softplus(-ym)
 }
 
-// one block per worker: loss at own model, loss at w_bar, ||w_i||^2
-__global__ __launch_bounds__(256) void loss_kernel(MetricArgs a, int64_t base) {
+// block (i, c): worker i's samples and model entries of chunk c (contiguous
+// ranges); loss at its own model, loss at w_bar, and its part of ||w_i||^2
+__global__ __launch_bounds__(256) void loss_kernel(MetricArgs a, int64_t base, int nch) {
   __shared__ double sh[256];
-  const int i = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x / nch, ch = blockIdx.x % nch, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t r0 = a.S * ch / nch, r1 = a.S * (ch + 1) / nch;
+  const int64_t c0 = a.dim * ch / nch, c1 = a.dim * (ch + 1) / nch;
   double lown = 0.0, lbar = 0.0, nrm = 0.0;
-  for (int64_t r = wave; r < a.S; r += 4) {
+  for (int64_t r = r0 + wave; r < r1; r += 4) {
     const int64_t g = int64_t(i) * a.S + r;
     double mo = 0.0, mb = 0.0;
     if (a.row_ptr) {
@@ -99,7 +102,7 @@ __global__ __launch_bounds__(256) void loss_kernel(MetricArgs a, int64_t base) {
       lbar += loss_of(y * mb, a.loss);
     }
   }
-  for (int64_t c = threadIdx.x; c < a.dim; c += 256) {
+  for (int64_t c = c0 + threadIdx.x; c < c1; c += 256) {
     const double w = model_at(a, i, c);
     nrm += w * w;
   }
@@ -107,13 +110,14 @@ __global__ __launch_bounds__(256) void loss_kernel(MetricArgs a, int64_t base) {
   lbar = block_sum_d(lbar, sh);
   nrm = block_sum_d(nrm, sh);
   if (threadIdx.x == 0) {
-    a.part[base + 3 * i] = lown;
-    a.part[base + 3 * i + 1] = lbar;
-    a.part[base + 3 * i + 2] = nrm;
+    double* q = a.part + base + 3 * (int64_t(i) * nch + ch);
+    q[0] = lown;
+    q[1] = lbar;
+    q[2] = nrm;
   }
 }
 
-__global__ __launch_bounds__(256) void finish_kernel(MetricArgs a, int ncb, int64_t base) {
+__global__ __launch_bounds__(256) void finish_kernel(MetricArgs a, int ncb, int64_t base, int nch) {
   __shared__ double sh[256];
   double cons = 0.0, msum = 0.0, wb2 = 0.0;
   for (int b = threadIdx.x; b < ncb; b += 256) {
@@ -127,8 +131,15 @@ __global__ __launch_bounds__(256) void finish_kernel(MetricArgs a, int ncb, int6
   double own = 0.0, bar = 0.0;
   if (a.S > 0) {
     for (int i = threadIdx.x; i < a.n; i += 256) {
-      own += a.part[base + 3 * i] / double(a.S) + 0.5 * double(a.l2) * a.part[base + 3 * i + 2];
-      bar += a.part[base + 3 * i + 1] / double(a.S);
+      const double* q = a.part + base + 3 * int64_t(i) * nch;
+      double lo = 0.0, lb = 0.0, nr = 0.0;
+      for (int ch = 0; ch < nch; ++ch) {  // chunk order
+        lo += q[3 * ch];
+        lb += q[3 * ch + 1];
+        nr += q[3 * ch + 2];
+      }
+      own += lo / double(a.S) + 0.5 * double(a.l2) * nr;
+      bar += lb / double(a.S);
     }
   }
   own = block_sum_d(own, sh);
@@ -147,14 +158,15 @@ __global__ __launch_bounds__(256) void finish_kernel(MetricArgs a, int ncb, int6
 hipError_t launch_metrics(const MetricArgs& a, hipStream_t s) {
   const int ncb = int(std::min<int64_t>((a.dim + 255) / 256, kColBlocksMax));
   const int64_t base = 2 * kColBlocksMax;
+  const int nch = metric_chunks(a.n, a.S);
   hipLaunchKernelGGL(cols_kernel, dim3(ncb), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.S > 0) {
-    hipLaunchKernelGGL(loss_kernel, dim3(a.n), dim3(256), 0, s, a, base);
+    hipLaunchKernelGGL(loss_kernel, dim3(uint32_t(a.n) * uint32_t(nch)), dim3(256), 0, s, a, base, nch);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(finish_kernel, dim3(1), dim3(256), 0, s, a, ncb, base);
+  hipLaunchKernelGGL(finish_kernel, dim3(1), dim3(256), 0, s, a, ncb, base, nch);
   return hipGetLastError();
 }
 
