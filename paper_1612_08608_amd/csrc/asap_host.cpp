@@ -51,6 +51,7 @@ struct asap_ctx {
   std::vector<float> w;
   std::vector<int32_t> optr, oidx;  // the transpose: the workers that read row i
   bool complete_uniform = false;
+  bool uniform_rows = false;  // every row: the entries other than its own share one weight (bitwise)
   int32_t max_deg = 0;  // longest row of the graph (entries, self included)
   int32_t max_out = 0;  // most workers that read one row
   int32_t n_cu = 256;   // compute units of the device the workspace is on
@@ -530,6 +531,19 @@ void set_graph(asap_ctx* c, int32_t n, const int32_t* nbr_ptr, const int32_t* nb
   c->idx.assign(nbr_idx, nbr_idx + nbr_ptr[n]);
   c->w.assign(nbr_w, nbr_w + nbr_ptr[n]);
   c->complete_uniform = is_complete_uniform(n, nbr_ptr, nbr_w);
+  c->uniform_rows = true;
+  for (int32_t i = 0; i < n && c->uniform_rows; ++i) {
+    bool first = true;
+    uint32_t bits = 0;
+    for (int32_t p = nbr_ptr[i]; p < nbr_ptr[i + 1]; ++p) {
+      if (nbr_idx[p] == i) continue;
+      uint32_t b;
+      std::memcpy(&b, &nbr_w[p], 4);
+      if (!first && b != bits) c->uniform_rows = false;
+      bits = b;
+      first = false;
+    }
+  }
   c->max_deg = 0;
   for (int32_t i = 0; i < n; ++i) c->max_deg = std::max(c->max_deg, nbr_ptr[i + 1] - nbr_ptr[i]);
   c->optr.assign(size_t(n) + 1, 0);
@@ -964,6 +978,7 @@ extern "C" asap_status asap_stochastic_reduce(asap_ctx* c, void* stream) {
   a.next = tag_start(c->round + 1);
   a.err = at<int32_t>(c, c->off_err);
   a.row_ok = at<int32_t>(c, c->off_rowok);
+  a.uniform_rows = c->uniform_rows && !a.scale;
   hipError_t e = launch_epoch_check(a, s);
   if (e == hipSuccess) {
     if (c->complete_uniform) {

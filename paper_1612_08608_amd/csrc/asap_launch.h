@@ -30,6 +30,7 @@ struct MixArgs {
   int64_t next;    // tag written for every reduced row in buffer e^1
   int32_t* err;
   int32_t* row_ok;  // [n] verdict of the epoch check (1 = every in-neighbour published)
+  int32_t uniform_rows;  // 1: in every row all entries but the own one have one weight (bitwise)
 };
 
 hipError_t launch_epoch_check(const MixArgs& a, hipStream_t s);

@@ -7,15 +7,17 @@
 // has no role here.  What matters is that every model byte crosses HBM once.
 //
 // slab kernel (n a power of two in [8, 1024], rows of at most 17 entries): one
-// 1024-thread workgroup per CU owns a contiguous range of column chunks; a
-// chunk holds all n rows of 16384/n columns (64 KiB) and is staged in LDS,
-// so each neighbour re-read is an LDS read.  Thread t keeps the neighbour
-// list of row t mod n in registers and computes 4 float4 of it per chunk;
-// the next chunk's loads are in flight while the current one is computed.
+// 512-thread workgroup per CU owns a contiguous range of column chunks; a
+// chunk holds all n rows of a column range (128 KiB above 512 rows, so that
+// it holds a whole 128-byte line of every row; else 64 KiB) and is staged in
+// LDS, so each neighbour re-read is an LDS read.  The loads of the next
+// chunk (two with 64 KiB chunks) are in flight while one is computed.  A
+// thread keeps the neighbour lists of its output rows in registers (two
+// weights per row when all of a row's entries but its own share one weight).
 // LDS slots of a row are XOR-swizzled by the row's low bits so that lanes
 // reading random rows spread over the banks.  Results are transposed across
-// groups of 4 lanes (DPP) so that each store writes 64 contiguous bytes of a
-// row rather than 16 bytes in each of 64 rows.
+// groups of 8 lanes (DPP) so that each store writes a whole 128-byte line of
+// a row rather than 16 bytes in each of 64 rows.
 //
 // tile kernel (any n): a tile is one 1 KiB segment of 16 consecutive output
 // rows, one wave per row segment with 16-byte loads; the tiles of one column
@@ -153,7 +155,7 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-constexpr int kSlabThreads = 1024;
+constexpr int kOut = 8;                             // outputs transposed and stored together
 
 // x of lane i ^ S (S = 1, 2, 4) by DPP moves: quad_perm [1,0,3,2] and
 // [2,3,0,1] are the xor-1 and xor-2 exchanges; xor 4 is the mirror inside
@@ -179,17 +181,17 @@ __device__ __forceinline__ float4 xor_lane4(const float4& x) {
   return make_float4(xor_lane<S>(x.x), xor_lane<S>(x.y), xor_lane<S>(x.z), xor_lane<S>(x.w));
 }
 
-// v[k] of lane i <- v[i] of lane k, within aligned groups of PF lanes
-// (PF = 4 or 8): butterfly exchanges with the lanes i ^ s, s = PF/2 .. 1.
 __device__ __forceinline__ float4 sel4(bool c, const float4& a, const float4& b) {
   return make_float4(c ? a.x : b.x, c ? a.y : b.y, c ? a.z : b.z, c ? a.w : b.w);
 }
 
-template <int S, int PF>
-__device__ __forceinline__ void transpose_stage(float4 (&v)[PF], int lane_in) {
+// v[k] of lane i <- v[i] of lane k, within aligned groups of 8 lanes:
+// butterfly exchanges with the lanes i ^ s, s = 4, 2, 1.
+template <int S>
+__device__ __forceinline__ void transpose_stage(float4 (&v)[kOut], int lane_in) {
   const bool hi = lane_in & S;
 #pragma unroll
-  for (int k = 0; k < PF; ++k) {
+  for (int k = 0; k < kOut; ++k) {
     if (k & S) continue;
     // a lane keeps the slot whose bit S matches its own and sends the other
     // (value selects only: a select of the slot to write would put v in
@@ -201,10 +203,8 @@ __device__ __forceinline__ void transpose_stage(float4 (&v)[PF], int lane_in) {
   }
 }
 
-template <int PF>
-__device__ __forceinline__ void transpose_lanes(float4 (&v)[PF], int lane_in) {
-  static_assert(PF == 4 || PF == 8, "transpose_lanes: PF in {4, 8}");
-  if constexpr (PF == 8) transpose_stage<4>(v, lane_in);
+__device__ __forceinline__ void transpose8(float4 (&v)[kOut], int lane_in) {
+  transpose_stage<4>(v, lane_in);
   transpose_stage<2>(v, lane_in);
   transpose_stage<1>(v, lane_in);
 }
@@ -217,133 +217,231 @@ __device__ __forceinline__ void store_partial(float* d, float4 v, int k) {
 }
 
 // LDS reads in flight per thread
-template <int DEG> constexpr int slab_group() { return DEG <= 5 ? DEG : 4; }
+template <int DEG, int R> constexpr int slab_group() { return DEG <= 5 ? DEG : (R == 2 && DEG > 9 ? 2 : 4); }
 
-// PF float4 per thread per chunk: a chunk is PF*16 KiB of LDS and PF
-// registers' worth of loads in flight per thread.  Outputs are computed and
-// stored kOut float4 at a time.
-constexpr int kOut = 4;
-
-template <int DEG, int PF>
-__global__ __launch_bounds__(kSlabThreads) void mix_slab_kernel(MixArgs a, int nchunks) {
-  constexpr int kVec = PF * kSlabThreads;    // float4 slots per chunk
-  __shared__ float4 slab[kVec];
+// Slab kernel.  One THREADS-thread workgroup per CU walks a contiguous
+// range of column chunks; a chunk is all n rows of 4 VEC / n columns (VEC
+// float4), staged in LDS.  Thread t stages float4 slots t + THREADS m of the
+// chunk (m < VEC / THREADS); NBUF register buffers keep the loads of the
+// next NBUF chunks in flight while one is computed.  Outputs: with R = 2
+// (n = 2 THREADS) thread t computes rows t and t + THREADS, the whole chunk
+// of each; with R = 1 row t mod n, VEC / THREADS float4 of it from
+// (t div n) VEC / THREADS on.  Groups of 8 outputs of 8 consecutive lanes (8
+// consecutive rows) are transposed across the lanes, so that each store
+// instruction writes whole 128-byte lines: 8 lanes fill 128 contiguous
+// bytes of one row.  With UNI every entry of a row but its own carries one
+// weight, so a row keeps two weights instead of DEG.
+template <int DEG, int R, int THREADS, int NBUF, int VEC, bool UNI>
+__global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunks) {
+  constexpr int kSlabThreads = THREADS;
+  constexpr int kSlabVec = VEC;
+  constexpr int kSlabPF = kSlabVec / THREADS;      // float4 staged per thread per chunk
+  __shared__ float4 slab[kSlabVec];
   const int n = a.n;
-  const int Q = kVec / n;                    // float4 per row per chunk
+  const int Q = kSlabVec / n;                // float4 per row per chunk (>= 8)
   const int C = 4 * Q;                       // columns per chunk
   const int X = min(Q, 8) - 1;               // swizzle mask
   const int tid = threadIdx.x;
-  const int row = tid % n, grp = tid / n;    // compute: row, float4 [grp*PF, grp*PF+PF)
-  static_assert(PF % kOut == 0, "outputs go kOut float4 at a time");
-  constexpr int G = slab_group<DEG>();
+  constexpr int OPR = kSlabPF / R;           // outputs per row per thread per chunk
+  constexpr int G = slab_group<DEG, R>();
+  // this thread's output rows and first float4
+  int orow[R];
+  int oq0;
+  if constexpr (R == 2) {
+    orow[0] = tid;
+    orow[1] = tid + kSlabThreads;
+    oq0 = 0;
+  } else {
+    orow[0] = tid % n;
+    oq0 = (tid / n) * OPR;
+  }
   // jq = j*Q | (j & X): the slot of float4 q of row j is jq ^ q, because
   // X < Q and Q is a power of two (see the staging writes below).
-  // jq < n*Q <= 8192, so two of them share a register.
-  uint32_t jq2[(DEG + 1) / 2] = {};
-  float nw[DEG];
-  const int p0 = a.nbr_ptr[row], deg = a.nbr_ptr[row + 1] - p0;
+  // jq < n*Q = 8192, so two of them share a register.
+  // Weights: with UNI every entry of a row but its own has one weight (the
+  // launcher checked it bit for bit, and no scale applies), so a row keeps
+  // (own weight, other weight, own position, length) and weight p is picked
+  // by selects, the same value as the general table would give.
+  uint32_t jq2[R][(DEG + 1) / 2];
+  float nw[R][UNI ? 1 : DEG];
+  float uw_self[R], uw_off[R];
+  int upos[R], ulen[R];
+  bool ok[R];
 #pragma unroll
-  for (int u = 0; u < DEG; ++u) {
-    const bool has = u < deg;  // padding: own row, weight 0
-    const int j = has ? a.nbr_idx[p0 + u] : row;
-    float wt = has ? a.nbr_w[p0 + u] : 0.f;
-    if (a.scale && has) wt *= a.scale[j];
-    jq2[u / 2] |= uint32_t(j * Q | (j & X)) << (16 * (u & 1));
-    nw[u] = wt;
+  for (int rr = 0; rr < R; ++rr) {
+    const int row = orow[rr];
+#pragma unroll
+    for (int u = 0; u < (DEG + 1) / 2; ++u) jq2[rr][u] = 0u;
+    const int p0 = a.nbr_ptr[row], deg = a.nbr_ptr[row + 1] - p0;
+    uw_self[rr] = 0.f;
+    uw_off[rr] = 0.f;
+    upos[rr] = -1;
+    ulen[rr] = deg;
+#pragma unroll
+    for (int u = 0; u < DEG; ++u) {
+      const bool has = u < deg;  // padding: own row, weight 0
+      const int j = has ? a.nbr_idx[p0 + u] : row;
+      float wt = has ? a.nbr_w[p0 + u] : 0.f;
+      if (a.scale && has) wt *= a.scale[j];
+      jq2[rr][u / 2] |= uint32_t(j * Q | (j & X)) << (16 * (u & 1));
+      if constexpr (UNI) {
+        if (has && j == row) {
+          uw_self[rr] = wt;
+          upos[rr] = u;
+        } else if (has) {
+          uw_off[rr] = wt;
+        }
+      } else {
+        nw[rr][u] = wt;
+      }
+    }
+    ok[rr] = a.row_ok[row] != 0;
   }
-  const bool ok = a.row_ok[row] != 0;
+  auto weight = [&](int rr, int p) -> float {
+    if constexpr (UNI) {
+      const float w_in = p == upos[rr] ? uw_self[rr] : uw_off[rr];
+      return p < ulen[rr] ? w_in : 0.f;
+    } else {
+      return nw[rr][p];
+    }
+  };
   const int per = (nchunks + int(gridDim.x) - 1) / int(gridDim.x);
   const int ch0 = int(blockIdx.x) * per, ch1 = min(nchunks, ch0 + per);
 
-  // Staging: thread t always moves float4 slot q0 = t mod Q of rows
-  // r0 + m*rstep.  The per-thread part of the address is a 32-bit byte
-  // offset below 2^31 (the launcher checks it); the rest is wave-uniform.
-  const int q0 = tid % Q, r0 = tid / Q, rstep = kSlabThreads / Q;
+  // Staging: slot s = tid + 512 m of a chunk is float4 s mod Q of row s div
+  // Q.  The per-thread part of the address is a 32-bit byte offset below
+  // 2^31 (the launcher checks it); the rest is wave-uniform.
+  const int lq = __builtin_ctz(Q);
+  const bool wideq = Q > kSlabThreads;       // n == 8: Q = 1024
+  const int q0 = wideq ? tid : (tid & (Q - 1));
+  const int r0 = wideq ? 0 : (tid >> lq);
   const uint32_t voff = (uint32_t(r0) * uint32_t(a.ld) + 4u * uint32_t(q0)) * 4u;
-  float4 nxt[PF];
-  auto load = [&](int ch) {
-    const int64_t off = int64_t(ch) * C;
-    const bool in = off + 4 * q0 < a.dim;
+  auto srow = [&](int m) {                   // uniform row offset of slot m
+    return wideq ? (m >> 1) : m * (kSlabThreads >> lq);
+  };
+  auto sq = [&](int m) {                     // uniform float4 offset of slot m
+    return wideq ? (m & 1) * kSlabThreads : 0;
+  };
+  auto load = [&](float4 (&buf)[kSlabPF], int ch) {
+    const bool live = ch < ch1;
+    const int64_t off = int64_t(live ? ch : ch0) * C;
     // an empty asm makes voff opaque per chunk, so the compiler does not
-    // hoist PF 64-bit row addresses out of the chunk loop
+    // hoist 16 64-bit row addresses out of the chunk loop
     uint32_t vo = voff;
     asm volatile("" : "+v"(vo));
 #pragma unroll
-    for (int m = 0; m < PF; ++m) {
-      const char* base = reinterpret_cast<const char*>(a.src + off + int64_t(m * rstep) * a.ld);
-      nxt[m] = in ? *reinterpret_cast<const float4*>(base + vo) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int m = 0; m < kSlabPF; ++m) {
+      const bool in = live && off + 4 * (q0 + sq(m)) < a.dim;
+      const char* base = reinterpret_cast<const char*>(a.src + off + int64_t(srow(m)) * a.ld + 4 * sq(m));
+      buf[m] = in ? *reinterpret_cast<const float4*>(base + vo) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  // Output float4 q of this thread's row from the staged chunk.  Padding
+  auto stage = [&](const float4 (&buf)[kSlabPF]) {
+#pragma unroll
+    for (int m = 0; m < kSlabPF; ++m) {
+      const int r = r0 + srow(m), q = q0 + sq(m);
+      slab[(r * Q | (r & X)) ^ q] = buf[m];
+    }
+  };
+  // Output float4 q of row rr of this thread from the staged chunk.  Padding
   // entries read the own row with weight 0, which adds an exact zero, so the
   // reads of a group issue back to back with no branches.
-  auto slab_row = [&](int q) {
+  auto slab_row = [&](int rr, int q) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     // Empty asm statements pin the register plan: the packed slots stay
     // packed and the weights stay in registers (not reloaded from memory),
     // and the reads of one group are not hoisted above the previous group.
 #pragma unroll
-    for (int k = 0; k < (DEG + 1) / 2; ++k) asm volatile("" : "+v"(jq2[k]));
+    for (int k = 0; k < (DEG + 1) / 2; ++k) asm volatile("" : "+v"(jq2[rr][k]));
+    if constexpr (UNI) {
+      asm volatile("" : "+v"(uw_self[rr]), "+v"(uw_off[rr]), "+v"(upos[rr]), "+v"(ulen[rr]));
+    } else {
 #pragma unroll
-    for (int k = 0; k < DEG; ++k) asm volatile("" : "+v"(nw[k]));
+      for (int k = 0; k < DEG; ++k) asm volatile("" : "+v"(nw[rr][k]));
+    }
 #pragma unroll
     for (int p0 = 0; p0 < DEG; p0 += G) {
       if (p0 > 0) asm volatile("" ::: "memory");
       float4 x[G];
 #pragma unroll
       for (int p = p0; p < p0 + G && p < DEG; ++p)
-        x[p - p0] = slab[((jq2[p / 2] >> (16 * (p & 1))) & 0xffffu) ^ q];
+        x[p - p0] = slab[((jq2[rr][p / 2] >> (16 * (p & 1))) & 0xffffu) ^ q];
 #pragma unroll
-      for (int p = p0; p < p0 + G && p < DEG; ++p) fma4(acc, nw[p], x[p - p0]);
+      for (int p = p0; p < p0 + G && p < DEG; ++p) fma4(acc, weight(rr, p), x[p - p0]);
     }
     // all four components here, or the compiler splits 16-byte LDS reads
     asm volatile("" : "+v"(acc.x), "+v"(acc.y), "+v"(acc.z), "+v"(acc.w));
     return acc;
   };
-  // Stores: lane = row is the natural compute layout, but then every store
-  // instruction would scatter 16 bytes to each of 64 rows.  Each group of
-  // kOut outputs of kOut consecutive lanes is transposed across those lanes
-  // instead, so that store k of lane i writes float4 slot base + i of row
-  // (row & ~(kOut-1)) + k: kOut lanes fill kOut*16 contiguous bytes of one
-  // row.
-  const int lane_in = row & (kOut - 1), row_base = row & ~(kOut - 1);
-  const uint64_t okmask = __ballot(ok);
   const int lane = int(threadIdx.x) & 63;
-  if (ch0 < ch1) load(ch0);
-  for (int ch = ch0; ch < ch1; ++ch) {
-    lds_barrier();  // the previous chunk is no longer read
+  const int lane_in = lane & (kOut - 1);
+  uint64_t okmask[R];
 #pragma unroll
-    for (int m = 0; m < PF; ++m) {
-      const int r = r0 + m * rstep;
-      slab[(r * Q | (r & X)) ^ q0] = nxt[m];
-    }
-    lds_barrier();
-    if (ch + 1 < ch1) load(ch + 1);
+  for (int rr = 0; rr < R; ++rr) okmask[rr] = __ballot(ok[rr]);
+  auto compute = [&](int ch) {
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr) {
+      const int row_base = orow[rr] & ~(kOut - 1);
 #pragma unroll 1
-    for (int h = 0; h < PF / kOut; ++h) {
-      float4 res[kOut];
+      for (int h = 0; h < OPR / kOut; ++h) {
+        float4 res[kOut];
 #pragma unroll
-      for (int u = 0; u < kOut; ++u) res[u] = slab_row(grp * PF + h * kOut + u);
-      transpose_lanes<kOut>(res, lane_in);
-      const int64_t c = int64_t(ch) * C + 4 * (grp * PF + h * kOut + lane_in);
-      if (c < a.dim) {
-        const bool full = c + 4 <= a.dim;
-        const int k_tail = int(min<int64_t>(a.dim - c, 4));
+        for (int u = 0; u < kOut; ++u) res[u] = slab_row(rr, oq0 + h * kOut + u);
+        transpose8(res, lane_in);
+        const int64_t c = int64_t(ch) * C + 4 * (oq0 + h * kOut + lane_in);
+        if (c < a.dim) {
+          const bool full = c + 4 <= a.dim;
+          const int k_tail = int(min<int64_t>(a.dim - c, 4));
 #pragma unroll
-        for (int k = 0; k < kOut; ++k) {
-          if ((okmask >> (lane - lane_in + k)) & 1) {
-            float* d = a.dst + int64_t(row_base + k) * a.ld + c;
-            if (full) {
-              *reinterpret_cast<float4*>(d) = res[k];
-            } else {
-              store_partial(d, res[k], k_tail);
+          for (int k = 0; k < kOut; ++k) {
+            if ((okmask[rr] >> (lane - lane_in + k)) & 1) {
+              float* d = a.dst + int64_t(row_base + k) * a.ld + c;
+              if (full) {
+                *reinterpret_cast<float4*>(d) = res[k];
+              } else {
+                store_partial(d, res[k], k_tail);
+              }
             }
           }
         }
       }
     }
+  };
+  if constexpr (NBUF == 2) {
+    float4 bufA[kSlabPF], bufB[kSlabPF];
+    load(bufA, ch0);
+    load(bufB, ch0 + 1);
+    for (int ch = ch0; ch < ch1; ch += 2) {
+      lds_barrier();  // the previous chunk is no longer read
+      stage(bufA);
+      lds_barrier();
+      load(bufA, ch + 2);
+      compute(ch);
+      if (ch + 1 < ch1) {
+        lds_barrier();
+        stage(bufB);
+        lds_barrier();
+        load(bufB, ch + 3);
+        compute(ch + 1);
+      }
+    }
+  } else {
+    float4 bufA[kSlabPF];
+    load(bufA, ch0);
+    for (int ch = ch0; ch < ch1; ++ch) {
+      lds_barrier();  // the previous chunk is no longer read
+      stage(bufA);
+      lds_barrier();
+      load(bufA, ch + 1);
+      compute(ch);
+    }
   }
-  if (blockIdx.x == 0 && grp == 0 && ok) a.tag_dst[row] = a.next;
+  if (blockIdx.x == 0) {
+    const bool head = R == 2 || tid < n;
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr)
+      if (head && ok[rr]) a.tag_dst[orow[rr]] = a.next;
+  }
 }
 
 template <class T>
@@ -369,50 +467,57 @@ hipError_t launch_epoch_check(const MixArgs& a, hipStream_t s) {
 }
 
 namespace {
-// float4 per thread per chunk of the slab kernel for this graph (0: the slab
-// kernel does not apply).  With more than 512 rows a 64 KiB chunk holds under
-// 128 bytes of each row, half a cache line, and the other half is fetched
-// again for the next chunk; a 128 KiB chunk (8 float4 per thread) reads whole
-// lines.  Rows of 17 entries keep 4 (8 would not fit the registers).
-int slab_pf(int n, int max_deg) {
-  if (n < 8 || n > kSlabThreads || (n & (n - 1)) || max_deg > 17) return 0;
-  return (n > 512 && max_deg <= 9) ? 8 : 4;
-}
+// whether the slab kernel takes this graph: n a power of two in [8, 1024]
+// and rows of at most 17 entries
+bool slab_graph(int n, int max_deg) { return n >= 8 && n <= 1024 && !(n & (n - 1)) && max_deg <= 17; }
 
-// per-thread staging offset (rows below 1024/(C/4), float4 slots below C/4)
-// and chunk count within 31 bits
-bool slab_fits(const MixArgs& a, int PF) {
-  const int C = 4 * PF * kSlabThreads / a.n;
-  if ((int64_t(kSlabThreads / (C / 4) - 1) * a.ld + C) * 4 >= (int64_t(1) << 31)) return false;
+// per-thread staging offset (rows below 512/Q, float4 slots below Q) and
+// chunk count within 31 bits
+constexpr int kSlabThreads = 512;
+// chunk size (float4): 128 KiB above 512 rows, so that a chunk holds a whole
+// 128-byte line of every row, else 64 KiB (shorter chunks pipeline better
+// when each CU has only a few of them)
+int slab_vec(int n) { return n > 512 ? 8192 : 4096; }
+
+bool slab_fits(const MixArgs& a) {
+  const int Q = slab_vec(a.n) / a.n, C = 4 * Q;
+  const int rows = Q > kSlabThreads ? 1 : kSlabThreads / Q;
+  if ((int64_t(rows - 1) * a.ld + 4 * int64_t(std::min(Q, kSlabThreads))) * 4 >= (int64_t(1) << 31)) return false;
   return (a.dim + C - 1) / C < (int64_t(1) << 31);
 }
 }  // namespace
 
-bool mix_slab_applies(const MixArgs& a, int max_deg) {
-  const int pf = slab_pf(a.n, max_deg);
-  return pf != 0 && slab_fits(a, pf);
-}
+bool mix_slab_applies(const MixArgs& a, int max_deg) { return slab_graph(a.n, max_deg) && slab_fits(a); }
 
 // Slab kernel when n is a power of two in [8, 1024] and every row has at most
 // 17 entries (returns hipErrorNotSupported otherwise).
-template <int DEG, int PF>
+template <int DEG>
 hipError_t launch_slab(const MixArgs& a, int n_cu, hipStream_t s) {
-  if (!slab_fits(a, PF)) return hipErrorNotSupported;
-  const int C = 4 * PF * kSlabThreads / a.n;
+  if (!slab_fits(a)) return hipErrorNotSupported;
+  const int C = 4 * (slab_vec(a.n) / a.n);
   const int nchunks = int((a.dim + C - 1) / C);
   const int grid = std::max(1, std::min(nchunks, n_cu));
-  hipLaunchKernelGGL((mix_slab_kernel<DEG, PF>), dim3(grid), dim3(kSlabThreads), 0, s, a, nchunks);
+  const dim3 g(grid), b(kSlabThreads);
+  if (a.n > 512) {
+    if (a.uniform_rows)
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 2, kSlabThreads, 1, 8192, true>), g, b, 0, s, a, nchunks);
+    else
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 2, kSlabThreads, 1, 8192, false>), g, b, 0, s, a, nchunks);
+  } else {
+    if (a.uniform_rows)
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, kSlabThreads, 2, 4096, true>), g, b, 0, s, a, nchunks);
+    else
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, kSlabThreads, 2, 4096, false>), g, b, 0, s, a, nchunks);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_mix_slab(const MixArgs& a, int max_deg, int n_cu, hipStream_t s) {
-  const int pf = slab_pf(a.n, max_deg);
-  if (pf == 0) return hipErrorNotSupported;
-  const bool wide = pf == 8;
-  if (max_deg <= 3) return wide ? launch_slab<3, 8>(a, n_cu, s) : launch_slab<3, 4>(a, n_cu, s);
-  if (max_deg <= 5) return wide ? launch_slab<5, 8>(a, n_cu, s) : launch_slab<5, 4>(a, n_cu, s);
-  if (max_deg <= 9) return wide ? launch_slab<9, 8>(a, n_cu, s) : launch_slab<9, 4>(a, n_cu, s);
-  return launch_slab<17, 4>(a, n_cu, s);
+  if (!slab_graph(a.n, max_deg)) return hipErrorNotSupported;
+  if (max_deg <= 3) return launch_slab<3>(a, n_cu, s);
+  if (max_deg <= 5) return launch_slab<5>(a, n_cu, s);
+  if (max_deg <= 9) return launch_slab<9>(a, n_cu, s);
+  return launch_slab<17>(a, n_cu, s);
 }
 
 hipError_t launch_mix(const MixArgs& a, hipStream_t s) {
