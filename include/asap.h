@@ -25,7 +25,9 @@
  *    Device-side errors (an epoch-tag mismatch) are reported by asap_check.
  *  - The library never allocates device memory: the caller owns the
  *    workspace, the two model buffers and the data shards (device pointers,
- *    e.g. from torch tensors) and keeps them alive until asap_destroy.
+ *    e.g. from torch tensors) and keeps them alive until asap_destroy.  The
+ *    one exception is the static array of asap_metrics_noalloc (8.4 MiB per
+ *    GPU, created with the library's code object, never freed).
  *  - With CSR data bound, the library also owns one non-blocking stream
  *    (default priority) and a few events, created at asap_bind_workspace
  *    and released by asap_destroy; see asap_local_sgd.
@@ -329,6 +331,19 @@ asap_status asap_schedule_device(asap_ctx* ctx, uint64_t seed, int64_t round,
  *   out[3] = mean of all model entries (preserved by the reduce)
  * out[0] and out[1] are NaN when no data is bound. */
 asap_status asap_metrics(asap_ctx* ctx, int32_t loss, float l2, double* out, void* stream);
+
+/* asap_metrics for callers that cannot allocate device memory or bring a
+ * workspace for it (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same kernels and results, bit for
+ * bit, but w_bar, the partial sums and the four results live in a static
+ * device array of the library (8.4 MiB per GPU, held until the process
+ * ends) instead of the context's workspace.  Allocates nothing.  Limits:
+ * dim <= 2^20 and n_workers <= 16384, else ASAP_E_INVALID_ARG.  Every call on
+ * one GPU uses that GPU's single array, so calls that overlap on one GPU
+ * (other streams, other host threads, other contexts) race and must be
+ * serialised by the caller; the array keeps the last call's contents.
+ * Synchronises `stream`.  out[4] (host) as for asap_metrics. */
+asap_status asap_metrics_noalloc(asap_ctx* ctx, int32_t loss, float l2, double* out, void* stream);
 
 /* Synchronise `stream` and read the device error words.  Returns
  * ASAP_E_EPOCH (and clears the words) if any reduce since the last check

@@ -34,6 +34,7 @@ EXPORTS = (
     "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_run_rounds",
     "asap_current",
     "asap_set_round", "asap_drop_workers", "asap_get_graph", "asap_schedule_device", "asap_metrics", "asap_check",
+    "asap_metrics_noalloc",
     "asap_debug_set_tag", "asap_last_error", "asap_destroy",
 )
 
@@ -93,6 +94,7 @@ def lib():
         "asap_get_graph": [p, C.POINTER(i32), C.POINTER(i64), p, p, p],
         "asap_schedule_device": [p, u64, i64, p, p],
         "asap_metrics": [p, i32, C.c_float, p, p],
+        "asap_metrics_noalloc": [p, i32, C.c_float, p, p],
         "asap_check": [p, p, C.POINTER(i32)],
         "asap_debug_set_tag": [p, i32, i32, i64, p],
     }
@@ -290,6 +292,13 @@ def asap_metrics(ctx, loss="logistic", l2=0.0, stream=None):
     out = np.zeros(4, np.float64)
     _check(lib().asap_metrics(ctx, LOSS.get(loss, loss), l2, out.ctypes.data_as(C.c_void_p),
                               _stream(stream)), ctx)
+    return out
+
+
+def asap_metrics_noalloc(ctx, loss="logistic", l2=0.0, stream=None):
+    out = np.zeros(4, np.float64)
+    _check(lib().asap_metrics_noalloc(ctx, LOSS.get(loss, loss), l2, out.ctypes.data_as(C.c_void_p),
+                                      _stream(stream)), ctx)
     return out
 
 

@@ -1236,6 +1236,19 @@ extern "C" asap_status asap_metrics(asap_ctx* c, int32_t loss, float l2, double*
   return ASAP_OK;
 }
 
+extern "C" asap_status asap_metrics_noalloc(asap_ctx* c, int32_t loss, float l2, double* out, void* stream) {
+  MetricArgs a;
+  asap_status st = metric_args(c, loss, l2, out, &a);
+  if (st != ASAP_OK) return st;
+  if (c->dim > kStaticMetricMaxDim || c->n > kStaticMetricMaxWorkers)
+    return fail(c, ASAP_E_INVALID_ARG,
+                "asap_metrics_noalloc handles dim <= %lld and n <= %lld (got dim %lld, n %d); use asap_metrics",
+                (long long)kStaticMetricMaxDim, (long long)kStaticMetricMaxWorkers, (long long)c->dim, c->n);
+  hipError_t e = metrics_static_scratch(a, static_cast<hipStream_t>(stream), out);
+  if (e != hipSuccess) return hip_fail(c, e, "metrics kernels (static scratch)");
+  return ASAP_OK;
+}
+
 extern "C" asap_status asap_check(asap_ctx* c, void* stream, int32_t* bad_worker) {
   if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
   if (bad_worker) *bad_worker = -1;

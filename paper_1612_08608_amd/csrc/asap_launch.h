@@ -220,4 +220,14 @@ inline size_t metric_part_doubles(int64_t n, int64_t S) {
 }
 hipError_t launch_metrics(const MetricArgs& a, hipStream_t s);
 
+// asap_metrics with its scratch (w_bar, partial sums, the four results) in
+// the library's static device array instead of the context's workspace.
+// Fills a.wbar / a.part / a.out itself, runs the same kernels, copies the
+// results to out_host and synchronises `s`.  Returns hipErrorInvalidValue
+// when dim or n exceeds the array's limits (kStaticMetricMaxDim,
+// kStaticMetricMaxWorkers).
+constexpr int64_t kStaticMetricMaxDim = int64_t(1) << 20;
+constexpr int64_t kStaticMetricMaxWorkers = 16384;
+hipError_t metrics_static_scratch(MetricArgs a, hipStream_t s, double* out_host);
+
 }  // namespace asap

@@ -6,6 +6,7 @@
 //   mean_i f_i(w_i), F(w_bar) = (1/n) sum_i f_i(w_bar), ||W - 1 w_bar^T||_F and
 //   the mean of all model entries (which a doubly-stochastic reduce keeps).
 #include <cmath>
+#include <mutex>
 
 #include "asap_launch.h"
 
@@ -168,6 +169,65 @@ hipError_t launch_metrics(const MetricArgs& a, hipStream_t s) {
   }
   hipLaunchKernelGGL(finish_kernel, dim3(1), dim3(256), 0, s, a, ncb, base, nch);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch for callers that cannot allocate (asap_metrics_noalloc):
+// w_bar, the partial sums and the four results live in this file-scope
+// device array, one copy per GPU, kept until the process ends.  Host code
+// never passes the array's name to a kernel or a copy: it uses the device
+// address hipGetSymbolAddress returns for the current device.
+// ---------------------------------------------------------------------------
+namespace {
+
+// n * metric_chunks(n, S) <= max(2048, n), so the partial sums of at most
+// kStaticMetricMaxWorkers workers fit in kStaticPartMax bytes
+constexpr size_t kStaticWbarBytes = size_t(kStaticMetricMaxDim) * 8;
+constexpr size_t kStaticPartMax = (size_t(2 * kMetricColBlocks) + 3 * size_t(kStaticMetricMaxWorkers)) * 8;
+constexpr size_t kStaticScratchBytes = kStaticWbarBytes + kStaticPartMax + 256;  // 8.4 MiB
+
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// device address of this GPU's copy of `scratch`, looked up once per device
+// with that device current
+hipError_t scratch_for_current_device(unsigned char** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_dev[dev] = p;
+  }
+  *ptr = static_cast<unsigned char*>(g_scratch_dev[dev]);
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t metrics_static_scratch(MetricArgs a, hipStream_t s, double* out_host) {
+  if (a.dim < 1 || a.dim > kStaticMetricMaxDim || a.n < 1 || a.n > kStaticMetricMaxWorkers)
+    return hipErrorInvalidValue;
+  if (metric_part_doubles(a.n, a.S) * 8 > kStaticPartMax) return hipErrorInvalidValue;
+  unsigned char* base = nullptr;
+  hipError_t e = scratch_for_current_device(&base);
+  if (e != hipSuccess) return e;
+  // every word the kernels read is written by them first in this call
+  // (w_bar by the column pass, the partials by the column and loss passes,
+  // the results by the final pass), so nothing needs clearing
+  a.wbar = reinterpret_cast<double*>(base);
+  a.part = reinterpret_cast<double*>(base + kStaticWbarBytes);
+  a.out = reinterpret_cast<double*>(base + kStaticWbarBytes + kStaticPartMax);
+  if ((e = launch_metrics(a, s)) != hipSuccess) return e;
+  if ((e = hipMemcpyAsync(out_host, a.out, 4 * sizeof(double), hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
+  return hipStreamSynchronize(s);
 }
 
 }  // namespace asap
