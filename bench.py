@@ -397,10 +397,11 @@ def converge(wl, rounds, scale):
         else:
             sess.bind_dense(*data)
         prm = asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, wl.batch, wl.seed)
-        losses, spread = [], []
+        losses, local, spread = [], [], []
         for _ in range(rounds):
             sess.round(prm)
             m = sess.metrics(wl.loss, wl.l2)
+            local.append(float(m[0]))
             losses.append(float(m[1]))
             spread.append(float(m[2]))
         st, _ = sess.check()
@@ -412,18 +413,24 @@ def converge(wl, rounds, scale):
         for r in range(wl.n_workers):
             P[r, i[p[r]:p[r + 1]]] = w[p[r]:p[r + 1]]
         sv = np.linalg.svd(P, compute_uv=False)
+        # consensus decay per round against the bound sigma_2 of the mixing
+        # alone (the local passes push the models apart again every round)
+        decay = [spread[r] / spread[r - 1] if spread[r - 1] > 0 else None for r in range(1, rounds)]
         out["graphs"][g] = {"spectral_gap": 1.0 - float(sv[1]), "sigma2": float(sv[1]), "out_degree": out_degree,
                             "bytes_per_worker_per_round": out_degree * wl.dim * 4, "loss": losses,
-                            "consensus_distance": spread}
-        log(f"[converge] {g}: gap {1.0 - float(sv[1]):.4f}, F after {rounds} rounds {losses[-1]:.6f}")
-    # bytes each worker sends before F(w_bar) first reaches a target: the
-    # target is the complete graph's loss after a quarter of the rounds
-    target = out["graphs"]["complete"]["loss"][max(0, rounds // 4 - 1)]
-    out["target_loss"] = target
-    for g, rec in out["graphs"].items():
-        hit = next((r for r, f in enumerate(rec["loss"]) if f <= target), None)
-        rec["rounds_to_target"] = None if hit is None else hit + 1
-        rec["bytes_per_worker_to_target"] = None if hit is None else (hit + 1) * rec["bytes_per_worker_per_round"]
+                            "mean_local_loss": local, "consensus_distance": spread, "consensus_ratio": decay}
+        log(f"[converge] {g}: gap {1.0 - float(sv[1]):.4f}, F(w_bar) after {rounds} rounds {losses[-1]:.6f}, "
+            f"mean f_i(w_i) {local[-1]:.6f}, consensus distance {spread[-1]:.4e}")
+    # rounds and bytes each worker sends before a loss first reaches a
+    # target: the complete graph's value after a quarter of the rounds
+    for key, name in (("loss", "F(w_bar)"), ("mean_local_loss", "mean_i f_i(w_i)")):
+        target = out["graphs"]["complete"][key][max(0, rounds // 4 - 1)]
+        out.setdefault("targets", {})[name] = target
+        for g, rec in out["graphs"].items():
+            hit = next((r for r, f in enumerate(rec[key]) if f <= target), None)
+            rec.setdefault("rounds_to_target", {})[name] = None if hit is None else hit + 1
+            rec.setdefault("bytes_per_worker_to_target", {})[name] = (
+                None if hit is None else (hit + 1) * rec["bytes_per_worker_per_round"])
     print(json.dumps(out), flush=True)
 
 
