@@ -448,6 +448,11 @@ def run_rounds_bench(name, wl, args, torch):
         sess.bind_dense(*synth.dense_data(wl))
     prm = asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, wl.batch, wl.seed)
     K = args.steps
+    planned = wl.features == "csr" and wl.batch <= 64
+    if planned:
+        # plans for every pass of the launches below, so that the launch runs
+        # the planned pass as the stream-ordered rounds do
+        sess.bind_rounds_plan(K)
 
     def step():
         sess.prepare_sgd(prm)
@@ -480,7 +485,9 @@ def run_rounds_bench(name, wl, args, torch):
                       "batch": wl.batch, "graph": wl.graph, "degree": wl.degree},
            "stream_ms_per_round": stream_s / K * 1e3, "launch_ms_per_round": launch_s / K * 1e3,
            "stream_samples_per_s": samples * K / stream_s, "launch_samples_per_s": samples * K / launch_s,
-           "speedup": stream_s / launch_s}
+           "speedup": stream_s / launch_s,
+           "sgd_code": "planned CSR pass (plan ring bound)" if planned else
+                       ("general CSR pass" if wl.features == "csr" else "dense pass")}
     print(json.dumps(out), flush=True)
 
 

@@ -258,10 +258,11 @@ asap_status asap_round(asap_ctx* ctx, const asap_sgd_params* p, void* stream);
  * Result: bit for bit the models, buffer index, round counter and epoch
  * tags that `rounds` calls of asap_round with the same parameters leave,
  * provided asap_round runs the same half-step code: dense shards always;
- * CSR shards when the stream-ordered path takes its general kernel (the
- * planned CSR pass is not used here, so with minibatches of at most 64 rows
- * of at most 128 nonzeros the two paths agree to the oracle's tolerance but
- * not bitwise).
+ * CSR shards when the stream-ordered path takes its general kernel, or
+ * when it takes the planned pass and a plan ring holds every pass of the
+ * launch (asap_bind_rounds_plan).  With the planned pass and no ring the
+ * launch runs the general kernel, and the two paths agree to the oracle's
+ * tolerance but not bitwise.
  *
  * Requirements: state as after a reduce or asap_set_round (no half-step
  * pending); every worker has at most 64 in-neighbours and at most 64
@@ -275,6 +276,28 @@ asap_status asap_round(asap_ctx* ctx, const asap_sgd_params* p, void* stream);
  * workspace; forgets any CSR plan prepared ahead.  Asynchronous. */
 asap_status asap_run_rounds(asap_ctx* ctx, const asap_sgd_params* p, int64_t rounds, int32_t wait_ms,
                             void* stream);
+
+/* Plan ring of the multi-round launch (Section 4 with the planned CSR
+ * pass).  With CSR shards whose minibatch steps fit the planned pass
+ * (batch <= 64, rows of at most 128 nonzeros, fewer than 2^29 nonzeros per
+ * worker) the stream-ordered path plans every pass's column bookkeeping
+ * ahead of the pass.  A launch of asap_run_rounds can do the same when the
+ * caller binds device memory for the plans of the passes it covers: one
+ * area per pass (a launch of R rounds covers R passes, or ceil(R L / K) + 1
+ * at most with L local steps of a K-step pass).  asap_rounds_plan_size
+ * gives the bytes for `passes` areas (CSR data must be bound;
+ * ASAP_E_STATE otherwise); asap_bind_rounds_plan binds caller-owned memory
+ * (256-byte aligned; as many areas as fit) after the workspace, writes the
+ * round-invariant half of every area on `stream`, and keeps it until the
+ * next asap_bind_* or asap_drop_workers call, which unbind it.  A launch
+ * whose passes fit in the bound areas then runs the planned pass inside the
+ * launch: the plans are made before it on `stream`, or beside it on the
+ * library's own stream when the launch leaves compute units free (a worker
+ * waits, within wait_ms, until its pass's plan is published), and the
+ * result is bit for bit that of the stream-ordered rounds.  Otherwise the
+ * launch runs the general CSR kernel. */
+asap_status asap_rounds_plan_size(const asap_ctx* ctx, int64_t passes, size_t* bytes);
+asap_status asap_bind_rounds_plan(asap_ctx* ctx, void* dev, size_t bytes, void* stream);
 
 /* Where the live models are: index (0 or 1) of the buffer holding the
  * current round's models, the round number, and whether this round's

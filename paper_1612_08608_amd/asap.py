@@ -34,7 +34,7 @@ EXPORTS = (
     "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_run_rounds",
     "asap_current",
     "asap_set_round", "asap_drop_workers", "asap_get_graph", "asap_schedule_device", "asap_metrics", "asap_check",
-    "asap_metrics_noalloc",
+    "asap_metrics_noalloc", "asap_rounds_plan_size", "asap_bind_rounds_plan",
     "asap_debug_set_tag", "asap_last_error", "asap_destroy",
 )
 
@@ -95,6 +95,8 @@ def lib():
         "asap_schedule_device": [p, u64, i64, p, p],
         "asap_metrics": [p, i32, C.c_float, p, p],
         "asap_metrics_noalloc": [p, i32, C.c_float, p, p],
+        "asap_rounds_plan_size": [p, i64, C.POINTER(sz)],
+        "asap_bind_rounds_plan": [p, p, sz, p],
         "asap_check": [p, p, C.POINTER(i32)],
         "asap_debug_set_tag": [p, i32, i32, i64, p],
     }
@@ -302,6 +304,16 @@ def asap_metrics_noalloc(ctx, loss="logistic", l2=0.0, stream=None):
     return out
 
 
+def asap_rounds_plan_size(ctx, passes: int) -> int:
+    out = C.c_size_t(0)
+    _check(lib().asap_rounds_plan_size(ctx, int(passes), C.byref(out)), ctx)
+    return out.value
+
+
+def asap_bind_rounds_plan(ctx, dev, nbytes: int, stream=None):
+    _check(lib().asap_bind_rounds_plan(ctx, _dev(dev), int(nbytes), _stream(stream)), ctx)
+
+
 def asap_check(ctx, stream=None):
     """Returns (status, bad_worker) without raising, so callers can inspect E_EPOCH."""
     bad = C.c_int32(-1)
@@ -415,6 +427,13 @@ class Session:
         """`rounds` rounds in one launch with per-worker NOTIFY-ACK."""
         asap_run_rounds(self.ready().ctx, params, rounds, wait_ms, stream)
 
+    def bind_rounds_plan(self, passes, stream=None):
+        """Device memory for the plans of `passes` passes, so that a
+        multi-round launch over CSR shards runs the planned pass."""
+        nbytes = asap_rounds_plan_size(self.ready().ctx, passes)
+        self.ring = self.torch.empty(nbytes, dtype=self.torch.uint8, device=self.device)
+        asap_bind_rounds_plan(self.ctx, self.ring, nbytes, stream)
+
     def drop_workers(self, dropped, ptr, idx, w, flags=0, stream=None):
         """Workers `dropped` leave (asap_drop_workers); the survivors keep
         their models, renumbered in order, run on the graph (ptr, idx, w) and
@@ -501,7 +520,7 @@ class Session:
             self.torch.cuda.synchronize(self.device)
             asap_destroy(self.ctx)
             self.ctx = None
-        self.bufs, self.ws, self._keep, self._data = [], None, [], None
+        self.bufs, self.ws, self._keep, self._data, self.ring = [], None, [], None, None
 
     def __del__(self):
         try:

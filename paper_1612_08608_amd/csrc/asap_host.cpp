@@ -86,6 +86,17 @@ struct asap_ctx {
   RoundPlan plan[2];
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
+  // plan ring of the multi-round launch (asap_bind_rounds_plan): epoch
+  // tokens [areas] int64 at the start, then `areas` plan areas of
+  // ring_stride bytes laid out as ring_lay
+  char* ring = nullptr;
+  int64_t ring_areas = 0;
+  size_t ring_stride = 0;
+  RoundPlan ring_lay;
+  int64_t ring_epoch = 0;
+  bool ring_valid = false;
+  hipEvent_t ev_ring_free = nullptr;  // after the last launch that read the ring
+
   // round state
   int32_t cur = 0;
   int64_t round = 0;
@@ -199,16 +210,19 @@ void drain_ahead(asap_ctx* c) {
 void release_ahead(asap_ctx* c) {
   drain_ahead(c);
   if (c->ahead) (void)hipStreamDestroy(c->ahead);
-  for (hipEvent_t* ev : {&c->ev_start, &c->ev_ready[0], &c->ev_ready[1], &c->ev_used[0], &c->ev_used[1]})
+  for (hipEvent_t* ev : {&c->ev_start, &c->ev_ready[0], &c->ev_ready[1], &c->ev_used[0], &c->ev_used[1],
+                         &c->ev_ring_free})
     if (*ev) {
       (void)hipEventDestroy(*ev);
       *ev = nullptr;
     }
   c->ahead = nullptr;
+  c->ring_valid = false;
 }
 
 void unbind_workspace(asap_ctx* c) {
   drain_ahead(c);
+  c->ring_valid = false;  // its bind-time halves depend on the data and the workspace's codes
   c->ws = nullptr;
   c->ws_bytes = 0;
   c->tags_ready = false;
@@ -653,6 +667,7 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     return fail(c, ASAP_E_INVALID_ARG, "workspace too small: %zu < %zu bytes", bytes, c->total);
   if (!c->buf[0]) return fail(c, ASAP_E_STATE, "bind the models before the workspace");
   drain_ahead(c);
+  c->ring_valid = false;
   hipStream_t s = static_cast<hipStream_t>(stream);
   {
     int dev_id = 0, cus = 0;
@@ -797,24 +812,28 @@ bool planned_pass(const asap_ctx* c, const SgdArgs& a) {
   return csr_plan_fits(a) && c->max_wnnz < (int64_t(1) << 29);
 }
 
-PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
+// The plan arrays of rp live at `base` + their offsets: the workspace by
+// default, or an area of the multi-round launch's plan ring.
+PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp, char* base = nullptr) {
+  if (!base) base = c->ws;
+  auto at = [base](size_t off) { return base + off; };
   PlanArgs pa{};
-  pa.rowinfo = at<RowInfo>(c, rp.rowinfo);
-  pa.code = at<int32_t>(c, c->off_code);
+  pa.rowinfo = reinterpret_cast<RowInfo*>(at(rp.rowinfo));
+  pa.code = ::at<int32_t>(c, c->off_code);
   pa.row_ptr = c->row_ptr;
   pa.n = c->n;
   pa.S = c->S;
   pa.batch = p->batch;
   pa.K = int32_t((c->S + p->batch - 1) / p->batch);
-  pa.step_off = at<int32_t>(c, rp.soff);
+  pa.step_off = reinterpret_cast<int32_t*>(at(rp.soff));
   pa.val = c->val;
-  pa.pack = at<int2>(c, rp.pack);
-  pa.clist = at<int32_t>(c, rp.clist);
-  pa.clink = at<int32_t>(c, rp.clink);
-  pa.hlist = at<int32_t>(c, rp.hlist);
-  pa.cnt = at<int32_t>(c, rp.cnt);
-  pa.flag = at<int32_t>(c, rp.flag);
-  pa.progress = at<int64_t>(c, c->off_progress);
+  pa.pack = reinterpret_cast<int2*>(at(rp.pack));
+  pa.clist = reinterpret_cast<int32_t*>(at(rp.clist));
+  pa.clink = reinterpret_cast<int32_t*>(at(rp.clink));
+  pa.hlist = reinterpret_cast<int32_t*>(at(rp.hlist));
+  pa.cnt = reinterpret_cast<int32_t*>(at(rp.cnt));
+  pa.flag = reinterpret_cast<int32_t*>(at(rp.flag));
+  pa.progress = ::at<int64_t>(c, c->off_progress);
   // a prefetch workgroup per worker when both fit beside each other and
   // worker i's pair lands on one XCD
   pa.helpers = (c->n % 8 == 0 && 2 * c->n <= c->n_cu) ? 1 : 0;
@@ -825,12 +844,14 @@ PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
 // schedule of (seed, round), the row descriptors and, when the planned pass
 // applies, the column plan of every worker and step.
 hipError_t prepare_csr_round(asap_ctx* c, const asap_sgd_params* p, int64_t round, const RoundPlan& rp, bool planned,
-                             hipStream_t s) {
-  hipError_t e = launch_schedule(p->seed, round, c->n, c->S, at<int32_t>(c, rp.sched), s);
+                             hipStream_t s, char* base = nullptr) {
+  if (!base) base = c->ws;
+  int32_t* sched = reinterpret_cast<int32_t*>(base + rp.sched);
+  hipError_t e = launch_schedule(p->seed, round, c->n, c->S, sched, s);
   if (e == hipSuccess)
-    e = launch_rowinfo(at<int32_t>(c, rp.sched), c->row_ptr, c->y, c->n, c->S, at<RowInfo>(c, rp.rowinfo), s);
+    e = launch_rowinfo(sched, c->row_ptr, c->y, c->n, c->S, reinterpret_cast<RowInfo*>(base + rp.rowinfo), s);
   if (planned) {
-    const PlanArgs pa = plan_args(c, p, rp);
+    const PlanArgs pa = plan_args(c, p, rp, base);
     if (e == hipSuccess) e = launch_fill_i32(pa.flag, 1, 0, s);
     if (e == hipSuccess) e = launch_csr_plan(pa, c->max_row, s);
   }
@@ -1002,6 +1023,71 @@ extern "C" asap_status asap_round(asap_ctx* c, const asap_sgd_params* p, void* s
   return asap_stochastic_reduce(c, stream);
 }
 
+namespace {
+
+// One area of the plan ring: the arrays of one pass's plan (as a RoundPlan
+// slot of the workspace); returns its size.
+size_t ring_layout(const asap_ctx* c, RoundPlan* lay) {
+  const size_t n = size_t(c->n), nS = n * size_t(c->S), nz = size_t(c->nnz);
+  size_t o = 0;
+  lay->sched = o;   o = align_up(o + nS * 4);
+  lay->rowinfo = o; o = align_up(o + nS * sizeof(RowInfo));
+  lay->soff = o;    o = align_up(o + n * (size_t(c->S) + 1) * 4);
+  lay->pack = o;    o = align_up(o + nz * 8);
+  lay->clist = o;   o = align_up(o + nz * 4);
+  lay->clink = o;   o = align_up(o + nz * 4);
+  lay->hlist = o;   o = align_up(o + nz * 4);
+  lay->cnt = o;     o = align_up(o + nS * 2 * 4);
+  lay->flag = o;    o = align_up(o + 4);
+  return o;
+}
+
+size_t ring_head(int64_t areas) { return align_up(size_t(areas) * 8); }
+
+}  // namespace
+
+extern "C" asap_status asap_rounds_plan_size(const asap_ctx* c, int64_t passes, size_t* bytes) {
+  if (!c || !bytes) return fail(const_cast<asap_ctx*>(c), ASAP_E_INVALID_ARG, "ctx or bytes is NULL");
+  if (passes < 1 || passes > (int64_t(1) << 20)) return fail(const_cast<asap_ctx*>(c), ASAP_E_INVALID_ARG,
+                                                             "passes must be in [1, 2^20]");
+  if (c->kind != kCsr) return fail(const_cast<asap_ctx*>(c), ASAP_E_STATE, "no CSR data bound");
+  RoundPlan lay;
+  *bytes = ring_head(passes) + size_t(passes) * ring_layout(c, &lay);
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_bind_rounds_plan(asap_ctx* c, void* dev, size_t bytes, void* stream) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (!dev || uintptr_t(dev) % kAlign) return fail(c, ASAP_E_INVALID_ARG, "plan ring must be 256-byte aligned");
+  if (c->kind != kCsr) return fail(c, ASAP_E_STATE, "no CSR data bound");
+  if (!c->ws || !c->tags_ready) return fail(c, ASAP_E_STATE, "bind the workspace before the plan ring");
+  RoundPlan lay;
+  const size_t stride = ring_layout(c, &lay);
+  int64_t areas = 0;
+  while (ring_head(areas + 1) + size_t(areas + 1) * stride <= bytes) ++areas;
+  if (areas < 1) return fail(c, ASAP_E_INVALID_ARG, "plan ring too small for one pass (%zu bytes)", bytes);
+  drain_ahead(c);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(dev);
+  hipError_t e = launch_fill_i64(reinterpret_cast<int64_t*>(base), areas, -1, s);
+  // the bind-time halves of every area's (code, value) pairs, as for the
+  // workspace's two plan slots
+  for (int64_t u = 0; u < areas && e == hipSuccess; ++u)
+    e = launch_pack_values(at<int32_t>(c, c->off_code), c->val, c->nnz,
+                           reinterpret_cast<int2*>(base + ring_head(areas) + size_t(u) * stride + lay.pack), s);
+  if (e == hipSuccess && !c->ev_ring_free) {
+    if ((e = hipEventCreateWithFlags(&c->ev_ring_free, hipEventDisableTiming))) c->ev_ring_free = nullptr;
+  }
+  if (e == hipSuccess) e = hipEventRecord(c->ev_ring_free, s);
+  if (e != hipSuccess) return hip_fail(c, e, "plan ring");
+  c->ring = base;
+  c->ring_areas = areas;
+  c->ring_stride = stride;
+  c->ring_lay = lay;
+  c->ring_valid = true;
+  return ASAP_OK;
+}
+
 extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, int64_t rounds, int32_t wait_ms,
                                        void* stream) {
   if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
@@ -1053,7 +1139,37 @@ extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, in
   ra.sched = at<int32_t>(c, c->plan[0].sched);
   ra.rowinfo = at<RowInfo>(c, c->plan[0].rowinfo);
   if (c->kind == kCsr) {
-    e = launch_rounds_csr(a, ra, c->n_cu, s);
+    // the passes this launch covers
+    const int64_t K = (c->S + p->batch - 1) / p->batch;
+    auto pass_of = [&](int64_t r) { return p->local_steps == 0 ? r : r * p->local_steps / K; };
+    const int64_t first = pass_of(c->round), npass = pass_of(c->round + rounds - 1) - first + 1;
+    if (c->ring_valid && planned_pass(c, a) && npass <= c->ring_areas) {
+      // every pass gets its plan in its own ring area: beside the launch on
+      // the look-ahead stream when the launch leaves compute units free
+      // (workers wait for their pass's plan), else before it on `stream`
+      RoundsPlan rp{};
+      rp.area0 = plan_args(c, p, c->ring_lay, c->ring + ring_head(c->ring_areas));
+      rp.stride = int64_t(c->ring_stride);
+      rp.first_pass = first;
+      rp.npass = npass;
+      rp.ready = reinterpret_cast<const int64_t*>(c->ring);
+      rp.token0 = (++c->ring_epoch) << 24;
+      const int64_t blocks = int64_t(c->n) * (rp.area0.helpers ? 2 : 1);
+      const bool beside = c->ahead && blocks + 64 <= c->n_cu;
+      hipStream_t ps = beside ? c->ahead : s;
+      if (beside) e = hipStreamWaitEvent(ps, c->ev_ring_free, 0);
+      else e = hipSuccess;
+      for (int64_t u = 0; u < npass && e == hipSuccess; ++u) {
+        char* area = c->ring + ring_head(c->ring_areas) + size_t(u) * c->ring_stride;
+        e = prepare_csr_round(c, p, first + u, c->ring_lay, true, ps, area);
+        if (e == hipSuccess) e = launch_fill_i64(reinterpret_cast<int64_t*>(c->ring) + u, 1, rp.token0 + u, ps);
+      }
+      if (e != hipSuccess) return hip_fail(c, e, "launch planning");
+      e = launch_rounds_csr_planned(a, ra, rp, c->n_cu, s);
+      if (e == hipSuccess) e = hipEventRecord(c->ev_ring_free, s);
+    } else {
+      e = launch_rounds_csr(a, ra, c->n_cu, s);
+    }
   } else if (dense_wide_cpq(c->dim)) {
     DenseSync ds{};
     ds.part = at<float>(c, c->off_dacc);

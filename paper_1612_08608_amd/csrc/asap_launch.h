@@ -155,10 +155,22 @@ struct RoundsArgs {
   int32_t* sched;      // [n][S] dense: this pass's schedule rows
   RowInfo* rowinfo;    // [n][S] CSR: this pass's row descriptors
 };
+// Plans of the passes of a multi-round launch on planned CSR passes: pass
+// first_pass + u has its plan in area u (the pointers of area0 advanced by
+// u * stride bytes); the area is published when ready[u] == token0 + u.
+struct RoundsPlan {
+  PlanArgs area0;
+  int64_t stride;
+  int64_t first_pass, npass;
+  const int64_t* ready;
+  int64_t token0;
+};
 constexpr int kRoundsMaxDeg = 64;  // in- and out-neighbours of a worker in a multi-round launch
 hipError_t launch_rounds_dense(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s);
 hipError_t launch_rounds_dense_wide(const SgdArgs& a, const DenseSync& ds, const RoundsArgs& ra, hipStream_t s);
 hipError_t launch_rounds_csr(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s);
+hipError_t launch_rounds_csr_planned(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
+                                     hipStream_t s);
 // whether the stream-ordered reduce of this graph runs the slab kernel
 bool mix_slab_applies(const MixArgs& a, int max_deg);
 

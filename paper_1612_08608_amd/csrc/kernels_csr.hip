@@ -34,6 +34,7 @@
 #include "asap_launch.h"
 #include "rounds_device.h"
 #include "csr_device.h"
+#include "csr_fast.h"
 
 namespace asap {
 namespace {
@@ -197,8 +198,7 @@ __device__ __forceinline__ void count_stats(Shared& sh, int slot, const DataReg<
 }
 
 template <int E, bool PIPE>
-__device__ __forceinline__ void csr_pass(const SgdArgs& a, int i) {
-  __shared__ Shared sh;
+__device__ __forceinline__ void csr_pass(const SgdArgs& a, int i, Shared& sh) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane & (kRowLanes - 1);
   const int brow = wave * (64 / kRowLanes) + (lane / kRowLanes);  // fast-path row of this lane
@@ -403,7 +403,8 @@ __device__ __forceinline__ void csr_pass(const SgdArgs& a, int i) {
 template <int E, bool PIPE>
 __global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
   if (a.run_if && *a.run_if == 0) return;  // the planned kernel took this round
-  csr_pass<E, PIPE>(a, int(blockIdx.x));
+  __shared__ Shared sh;
+  csr_pass<E, PIPE>(a, int(blockIdx.x), sh);
 }
 
 // Several rounds in one launch (rounds_device.h): one workgroup per worker
@@ -411,13 +412,110 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_kernel(SgdArgs a) {
 template <int E, bool PIPE>
 __global__ __launch_bounds__(kThreads) void rounds_csr_kernel(SgdArgs a, RoundsArgs ra) {
   const int i = int(blockIdx.x);
+  __shared__ Shared sh;
   rounds::drive(
       a, ra, i, 0,
       [&](int64_t pass) {
         rounds::fill_rowinfo(ra.seed, i, pass, a.S, a.row_ptr, a.y, ra.rowinfo + int64_t(i) * a.S);
       },
       [&](const SgdArgs& ar) {
-        csr_pass<E, PIPE>(ar, i);
+        csr_pass<E, PIPE>(ar, i, sh);
+        return true;
+      });
+}
+
+// The plan of pass u of a planned launch (area u of the plan ring).
+__device__ __forceinline__ PlanArgs ring_area(const RoundsPlan& rp, int64_t u) {
+  PlanArgs p = rp.area0;
+  const int64_t d = u * rp.stride;
+  p.rowinfo = reinterpret_cast<const RowInfo*>(reinterpret_cast<const char*>(p.rowinfo) + d);
+  p.step_off = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.step_off) + d);
+  p.pack = reinterpret_cast<int2*>(reinterpret_cast<char*>(p.pack) + d);
+  p.clist = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.clist) + d);
+  p.clink = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.clink) + d);
+  p.hlist = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.hlist) + d);
+  p.cnt = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.cnt) + d);
+  p.flag = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.flag) + d);
+  return p;
+}
+
+// One thread: wait until pass u's plan is published (ready[u] carries this
+// launch's token for it) or the wall clock passes `deadline`.
+__device__ inline bool wait_plan(const RoundsPlan& rp, int64_t u, long long deadline) {
+  while (rounds::tag_peek(rp.ready + u) != rp.token0 + u) {
+    if (wall_clock64() > deadline) return false;
+    __builtin_amdgcn_s_sleep(4);
+  }
+  return true;
+}
+
+// Several rounds in one launch on planned passes: every pass the launch
+// covers has its plan in its own area of the ring (planned before the
+// launch, or beside it on the library's look-ahead stream: a worker waits,
+// bounded, until its pass's plan is published).  A pass whose plan
+// overflowed runs the general pass code, as the stream-ordered path does,
+// so both give the same bits.  With helpers, block n + i prefetches for
+// worker i, pass after pass.
+template <int E>
+__global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a, RoundsArgs ra, RoundsPlan rp) {
+  union LdsUnion {
+    Shared g;
+    FastShared f;
+  };
+  __shared__ LdsUnion sh;
+  __shared__ int plan_ok;
+  const int64_t K = (a.S + a.batch - 1) / a.batch;
+  if (int(blockIdx.x) >= ra.n) {
+    // prefetch workgroup: the steps of each pass that this launch runs
+    const int i = int(blockIdx.x) - ra.n;
+    for (int64_t u = 0; u < rp.npass; ++u) {
+      if (threadIdx.x == 0) plan_ok = wait_plan(rp, u, wall_clock64() + ra.wait_ticks);
+      __syncthreads();
+      if (!plan_ok) return;  // only costs time: the worker reports it
+      rounds::acquire_fence();
+      const PlanArgs p = ring_area(rp, u);
+      if (__hip_atomic_load(p.flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) continue;
+      const int64_t pass = rp.first_pass + u;
+      int64_t q0, k0, k1, q1, j0, j1;
+      rounds::steps_of(ra.r0, ra.local_steps, K, q0, k0, k1);
+      rounds::steps_of(ra.r0 + ra.R - 1, ra.local_steps, K, q1, j0, j1);
+      // the model buffer of the pass's first round in this launch (later
+      // rounds of a pass split by local steps alternate: only a prefetch)
+      int64_t rfirst = ra.local_steps == 0 ? pass : (pass * K + ra.local_steps - 1) / ra.local_steps;
+      if (rfirst < ra.r0) rfirst = ra.r0;
+      SgdArgs ah = a;
+      ah.round = pass;
+      ah.k0 = pass == q0 ? k0 : 0;
+      ah.k1 = pass == q1 ? j1 : K;
+      ah.rowinfo = p.rowinfo;
+      ah.models = ra.buf[ra.cur ^ int((rfirst - ra.r0) & 1)];
+      prefetch_pass<E>(ah, p, i);
+      __syncthreads();
+    }
+    return;
+  }
+  const int i = int(blockIdx.x);
+  PlanArgs pu = ring_area(rp, 0);
+  rounds::drive(
+      a, ra, i, 0,
+      [&](int64_t pass) {
+        const int64_t u = pass - rp.first_pass;
+        if (threadIdx.x == 0) {
+          plan_ok = wait_plan(rp, u, wall_clock64() + ra.wait_ticks);
+          if (!plan_ok) rounds::report_stale(ra.err, i);
+        }
+        __syncthreads();
+        rounds::acquire_fence();  // the plan was written by other kernels
+        pu = ring_area(rp, u);
+      },
+      [&](const SgdArgs& ar) {
+        if (!plan_ok) return false;
+        SgdArgs ap = ar;
+        ap.rowinfo = pu.rowinfo;
+        if (__hip_atomic_load(pu.flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+          csr_pass<E, true>(ap, i, sh.g);
+        else
+          fast_pass<E>(ap, pu, i, sh.f);
         return true;
       });
 }
@@ -439,6 +537,22 @@ hipError_t launch_rounds_e(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hip
 template <int E>
 hipError_t launch_rounds_pipe(const SgdArgs& a, const RoundsArgs& ra, int n_cu, hipStream_t s, bool pipe) {
   return pipe ? launch_rounds_e<E, true>(a, ra, n_cu, s) : launch_rounds_e<E, false>(a, ra, n_cu, s);
+}
+
+template <int E>
+hipError_t launch_rounds_planned_e(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
+                                   hipStream_t s) {
+  int per = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_csr_planned_kernel<E>, kThreads, 0);
+  if (e != hipSuccess) return e;
+  const int64_t grid = int64_t(a.n) * (rp.area0.helpers ? 2 : 1);
+  if (int64_t(per) * n_cu < grid) return hipErrorCooperativeLaunchTooLarge;
+  SgdArgs aa = a;
+  RoundsArgs rr = ra;
+  RoundsPlan pp = rp;
+  void* args[] = {&aa, &rr, &pp};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&rounds_csr_planned_kernel<E>),
+                                    dim3(uint32_t(grid)), dim3(kThreads), args, 0, s);
 }
 
 // ----------------------------------------------------------------------------
@@ -518,6 +632,17 @@ hipError_t launch_rounds_csr(const SgdArgs& a, const RoundsArgs& ra, int n_cu, h
   if (a.max_row <= kRowLanes * 4) return launch_rounds_pipe<4>(a, ra, n_cu, s, pipe);
   if (a.max_row <= kRowLanes * 6) return launch_rounds_pipe<6>(a, ra, n_cu, s, pipe);
   return launch_rounds_pipe<8>(a, ra, n_cu, s, pipe);
+}
+
+// the same entry count per lane as launch_sgd_csr_fast and launch_sgd_csr
+hipError_t launch_rounds_csr_planned(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
+                                     hipStream_t s) {
+  if (a.batch > kFastRows || a.n_hot > kHotMax) return hipErrorInvalidValue;
+  if (a.max_row <= kRowLanes * 2) return launch_rounds_planned_e<2>(a, ra, rp, n_cu, s);
+  if (a.max_row <= kRowLanes * 3) return launch_rounds_planned_e<3>(a, ra, rp, n_cu, s);
+  if (a.max_row <= kRowLanes * 4) return launch_rounds_planned_e<4>(a, ra, rp, n_cu, s);
+  if (a.max_row <= kRowLanes * 6) return launch_rounds_planned_e<6>(a, ra, rp, n_cu, s);
+  return launch_rounds_planned_e<8>(a, ra, rp, n_cu, s);
 }
 
 hipError_t launch_col_hist(const int32_t* col, int64_t nnz, int64_t stride, int32_t* counts, hipStream_t s) {

@@ -221,3 +221,71 @@ def test_run_rounds_edge_cases_match_the_stream_path(torch, case):
         runs.append(_bits(sess))
         sess.close()
     assert np.array_equal(runs[0], runs[1]), case
+
+
+# Planned CSR passes inside the launch: with a plan ring bound, every pass of
+# the launch runs the same planned-pass code as the stream-ordered rounds
+# (or, where a step overflows the plan, the same general code), so the bits
+# must be equal.  Small worker counts plan beside the launch on the library's
+# look-ahead stream; 128 workers with their prefetch workgroups fill the
+# device, so their plans are made before the launch.
+PLANNED = {
+    "c2_shape": (synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=512), "random", 4, 3, 0),
+    "c3_shape_128w": (synth.SPARSE_SVM_256W.with_(n_workers=128, dim=1 << 13, samples=256), "random", 8, 3, 0),
+    "local_steps": (synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=512, batch=64), "chain", 0, 7, 2),
+    # ~3800 distinct rarely used columns per step: every plan overflows and
+    # every pass runs the general code, on both paths
+    "overflow": (synth.SPARSE_LR_64W.with_(n_workers=4, samples=256, nnz_mean=60.0, zipf_s=0.3), "ring", 2, 2, 0),
+}
+
+
+@pytest.mark.parametrize("case", list(PLANNED))
+def test_run_rounds_planned_pass_is_bitwise_the_stream_path(torch, case):
+    wl, kind, d, R, L = PLANNED[case]
+    prm = params(wl, L)
+    a, _ = _session(wl, kind, d)
+    b, _ = _session(wl, kind, d)
+    for _ in range(R):
+        a.round(prm)
+    K = -(-wl.samples // wl.batch)
+    passes = R if L == 0 else (R * L) // K + 2
+    b.bind_rounds_plan(passes)
+    b.run_rounds(prm, R, wait_ms=3000)
+    assert b.check()[0] == asap.OK
+    assert b.current() == a.current()
+    assert np.array_equal(_bits(b), _bits(a)), case
+    # the stream-ordered path continues from the launch, and a second launch
+    # (the ring reused, its plans remade) from the stream-ordered path
+    for s in (a, b):
+        s.round(prm)
+    assert np.array_equal(_bits(b), _bits(a)), case
+    for _ in range(2):
+        a.round(prm)
+    b.run_rounds(prm, 2, wait_ms=3000)
+    assert a.check()[0] == asap.OK and b.check()[0] == asap.OK
+    assert b.current() == a.current()
+    assert np.array_equal(_bits(b), _bits(a)), case
+    a.close()
+    b.close()
+
+
+def test_rounds_plan_ring_arguments(torch):
+    wl = synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 12, samples=128)
+    sess, _ = _session(wl, "ring", 2)
+    one = asap.asap_rounds_plan_size(sess.ready().ctx, 1)
+    assert asap.asap_rounds_plan_size(sess.ctx, 3) > 2 * one
+    for bad in (0, -1):
+        with pytest.raises(asap.AsapError) as e:
+            asap.asap_rounds_plan_size(sess.ctx, bad)
+        assert e.value.status == asap.E_INVALID_ARG
+    small = torch.empty(one // 2, dtype=torch.uint8, device="cuda")
+    with pytest.raises(asap.AsapError) as e:
+        asap.asap_bind_rounds_plan(sess.ctx, small, small.numel())
+    assert e.value.status == asap.E_INVALID_ARG
+    sess.close()
+    dw = synth.RING8_DENSE_LR.with_(samples=64)
+    dense, _ = _session(dw, "ring", 2)
+    with pytest.raises(asap.AsapError) as e:
+        asap.asap_rounds_plan_size(dense.ready().ctx, 1)
+    assert e.value.status == asap.E_STATE
+    dense.close()
