@@ -419,10 +419,10 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
 
   // Rows of the next sub-batch of the same step load into xb while xa is
   // processed; the copy xa = xb then waits for loads that had the whole
-  // sub-batch to land.  The first sub-batch of a new step loads into xa
-  // during the exchange that ends the step before it (its row indices are
-  // staged by then), so the members' wait overlaps HBM reads and a member
-  // arrives without waiting for them.  Every member finishes every step
+  // sub-batch to land.  The first two sub-batches of a new step load into xa
+  // and xb during the exchange that ends the step before it (their row
+  // indices are staged by then), so the members' wait overlaps HBM reads and
+  // a member arrives without waiting for them.  Every member finishes every step
   // (exchange + update), also the steps in which it has no samples.
   float4 xa[SR][CPQ], xb[SR][CPQ];
   float ya = 0.f, yb = 0.f;
@@ -452,10 +452,12 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
   cur = settle(cur);
   if (cur.t < KE) load(xa, ya, cur);
   while (ok && done < min(cur.t, KE)) ok = finish_step(done++, [] {});  // steps without samples
+  bool xb_loaded = false;  // the exchange that ended the last step also loaded xb
   while (ok && cur.t < KE) {
     const Pos nx = settle(Pos{cur.t, cur.sb + SR, cur.lo, cur.hi});
     const bool same = nx.t == cur.t;
-    if (same) load(xb, yb, nx);
+    if (same && !xb_loaded) load(xb, yb, nx);
+    xb_loaded = false;
     process(xa, ya, cur);
     if (same) {
 #pragma unroll
@@ -467,7 +469,16 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
       while (ok && done < min(nx.t, KE)) {
         const int t = done++;
         ok = finish_step(t, [&]() {
-          if (t + 1 == nx.t && nx.t < KE) load(xa, ya, nx);
+          // both buffers are free during the exchange: the first two
+          // sub-batches of the next step load while the members gather
+          if (t + 1 == nx.t && nx.t < KE) {
+            load(xa, ya, nx);
+            const Pos n2 = settle(Pos{nx.t, nx.sb + SR, nx.lo, nx.hi});
+            if (n2.t == nx.t) {
+              load(xb, yb, n2);
+              xb_loaded = true;
+            }
+          }
         });
       }
     }
