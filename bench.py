@@ -151,15 +151,19 @@ def csr_bytes(wl, rp, col, sample_workers=4):
     return alg, alg + 8 * n * S + 4 * uniq * n / sample_workers
 
 
+SYNTH = os.path.join(ROOT, "paper_1612_08608_amd", "synth.py")
+
+
 def traffic_for(kernel_key, source):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when absent or taken on a different kernel source."""
+    None when absent or taken on a different kernel source or different data
+    (the generator of the synthetic inputs)."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     with open(TRAFFIC_FILE) as f:
         tab = json.load(f)
     ent = tab.get(kernel_key)
-    if not ent or ent.get("source_sha256") != sha256(source):
+    if not ent or ent.get("source_sha256") != sha256(source) or ent.get("data_sha256") != sha256(SYNTH):
         return None
     return ent["fetch_bytes"] + ent["write_bytes"]
 
