@@ -18,8 +18,9 @@ included, also has its own entry under `configs` (samples/s, or GB/s for the
 mixing stress, with its roofline and the oracle's CPU rate).
 `--workload NAME` measures one workload only.
 
-Other modes: `--copy-probe GIB` runs a plain device copy of known size (HBM
-counter calibration); `--run-rounds` times the multi-round NOTIFY-ACK launch
+Other modes: `--copy-probe GIB` runs a plain device copy of known size and
+`--gather-probe GIB` a random 4-byte gather of known size (HBM counter
+calibration); `--run-rounds` times the multi-round NOTIFY-ACK launch
 beside stream-ordered rounds; `--converge R` runs the convergence-versus-
 network-cost comparison of Section 6 on three graphs.
 """
@@ -100,6 +101,31 @@ def copy_probe(gib: int):
     ms = t0.elapsed_time(t1) / 3
     print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 3,
                       "ms_per_copy": ms, "GB/s": 8 * n / ms / 1e6}))
+
+
+def gather_probe(gib: int):
+    """A random 4-byte gather of known traffic (torch.index_select over a
+    `gib` GiB fp32 array at 2^24 random positions): reads the int64 indices
+    (8 B each, in order), one random 4-byte element per index, and writes 4 B
+    per index.  Calibrates what the HBM byte counters report for random
+    4-byte reads (the model gathers of the CSR pass)."""
+    import torch
+    n_src, n_idx = gib << 28, 1 << 24
+    src = torch.ones(n_src, dtype=torch.float32, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    idx = torch.randint(0, n_src, (n_idx,), device="cuda", generator=g, dtype=torch.int64)
+    out = torch.empty(n_idx, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(3):
+        torch.index_select(src, 0, idx, out=out)
+    t1.record()
+    torch.cuda.synchronize()
+    lines = torch.unique(idx // 32).numel()  # distinct 128-byte lines touched
+    print(json.dumps({"gather_probe_indices": n_idx, "index_bytes": 8 * n_idx, "output_bytes": 4 * n_idx,
+                      "distinct_128B_lines": lines, "launches": 3, "ms_per_gather": t0.elapsed_time(t1) / 3}))
 
 
 def graph_for(wl):
@@ -518,6 +544,7 @@ def main():
                     help="instead of the headline line: time the rounds as one multi-round launch "
                          "(asap_run_rounds, per-worker NOTIFY-ACK) beside the same rounds stream-ordered")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="GIB")
+    ap.add_argument("--gather-probe", type=int, default=0, metavar="GIB")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: every logical worker runs on a single MI355X "
@@ -525,6 +552,9 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.gather_probe:
+        gather_probe(args.gather_probe)
         return
 
     import torch
