@@ -44,6 +44,7 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD public spec
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 CSRC = os.path.join(ROOT, "paper_1612_08608_amd", "csrc")
 HEADLINE = "dense_lr_32w"
+CSR_MEMBERS = 0  # --csr-members
 # (entry name, workload, graph override, degree override)
 ALL_CONFIGS = [
     ("ring8_dense_lr", "ring8_dense_lr", None, None),
@@ -302,6 +303,9 @@ def measure(entry, wl, steps, warmup, cpu_budget, torch):
     if wl.features == "csr":
         rp, col, val, y = synth.csr_data(wl)
         sess.bind_csr(rp, col, val, y, wl.samples)
+        if CSR_MEMBERS:
+            sess.set_csr_members(CSR_MEMBERS)
+        members = sess.csr_members()
         alg, alg_wide = csr_bytes(wl, rp, col)
         S = wl.samples
         cpu_in = [("csr", rp[k * S:(k + 1) * S + 1] - rp[k * S], col[rp[k * S]:rp[(k + 1) * S]],
@@ -388,6 +392,7 @@ def measure(entry, wl, steps, warmup, cpu_budget, torch):
                 else:
                     kernel, src = "sgd_csr_kernel", os.path.join(CSRC, "kernels_csr.hip")
                 cfg["mean_nnz_per_row"] = (alg - 8 * samples) / 12 / samples
+                cfg["pass_workgroups_per_worker"] = members
             elif 1024 < D <= 8192:
                 kernel, src = "sgd_dense_wide_kernel", os.path.join(CSRC, "kernels_dense.hip")
             else:
@@ -424,6 +429,8 @@ def converge(wl, rounds, scale):
         sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
         if wl.features == "csr":
             sess.bind_csr(*data, wl.samples)
+            if CSR_MEMBERS:
+                sess.set_csr_members(CSR_MEMBERS)
         else:
             sess.bind_dense(*data)
         prm = asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, wl.batch, wl.seed)
@@ -474,6 +481,8 @@ def run_rounds_bench(name, wl, args, torch):
     sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
     if wl.features == "csr":
         sess.bind_csr(*synth.csr_data(wl), wl.samples)
+        if CSR_MEMBERS:
+            sess.set_csr_members(CSR_MEMBERS)
     else:
         sess.bind_dense(*synth.dense_data(wl))
     prm = asap.sgd_params(wl.loss, wl.lr_kind, wl.lr0, wl.l2, wl.batch, wl.seed)
@@ -543,6 +552,8 @@ def main():
     ap.add_argument("--run-rounds", action="store_true",
                     help="instead of the headline line: time the rounds as one multi-round launch "
                          "(asap_run_rounds, per-worker NOTIFY-ACK) beside the same rounds stream-ordered")
+    ap.add_argument("--csr-members", type=int, default=0, choices=[0, 1, 2, 4],
+                    help="workgroups per worker of the planned CSR pass (0: the library's choice)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="GIB")
     ap.add_argument("--gather-probe", type=int, default=0, metavar="GIB")
     args = ap.parse_args()
@@ -560,6 +571,8 @@ def main():
     import torch
     from paper_1612_08608_amd import asap
 
+    global CSR_MEMBERS
+    CSR_MEMBERS = args.csr_members
     asap.lib()  # fail loudly without the HIP library
     cpu_budget = 0.0 if args.no_cpu_baseline else args.cpu_seconds
     if args.workload == "all":

@@ -208,6 +208,22 @@ asap_status asap_bind_csr(asap_ctx* ctx, const int64_t* row_ptr, const int32_t* 
                           const float* val, const float* y, int64_t samples, int64_t nnz,
                           void* stream);
 
+/* Members of the planned CSR pass (Appendix A, update (A.2), first line: a
+ * worker's minibatch step): `members` workgroups (1, 2 or 4) share each
+ * worker's pass, member m owning the model columns c with c mod members ==
+ * m; once per step they exchange their partial margins (fp64) and add them
+ * in member order, so every member takes the same loss derivative.  0 (the
+ * default) chooses 4 or 2 while members * n_workers is at most half the
+ * device's compute units, else 1.  With several members the multi-round
+ * launch needs members * n_workers workgroups resident at once.  The
+ * result differs from one member's only in how the margins' fp64 sums are
+ * grouped.  Call before asap_workspace_size: it re-lays out the workspace
+ * (a bound workspace is unbound).  Errors: ASAP_E_INVALID_ARG for any
+ * other value. */
+asap_status asap_set_csr_members(asap_ctx* ctx, int32_t members);
+/* The members in effect (after asap_bind_csr; 1 before). */
+asap_status asap_get_csr_members(const asap_ctx* ctx, int32_t* members);
+
 /* Half-step of (A.2) for all workers: worker i runs one pass of minibatch
  * SGD over its shard, in the order of asap_schedule(S, seed, i, round), on
  * its row of the current buffer, and tags it (NOTIFY).  Margins of a step
@@ -279,7 +295,7 @@ asap_status asap_run_rounds(asap_ctx* ctx, const asap_sgd_params* p, int64_t rou
 
 /* Plan ring of the multi-round launch (Section 4 with the planned CSR
  * pass).  With CSR shards whose minibatch steps fit the planned pass
- * (batch <= 64, rows of at most 128 nonzeros, fewer than 2^29 nonzeros per
+ * (batch <= 64, rows of at most 128 nonzeros in each member's columns, fewer than 2^29 nonzeros per
  * worker) the stream-ordered path plans every pass's column bookkeeping
  * ahead of the pass.  A launch of asap_run_rounds can do the same when the
  * caller binds device memory for the plans of the passes it covers: one

@@ -30,7 +30,8 @@ EXPORTS = (
     "asap_graph_ring", "asap_graph_root_expander", "asap_graph_chain", "asap_graph_complete",
     "asap_graph_random_regular",
     "asap_metropolis_weights", "asap_schedule", "asap_create", "asap_workspace_size",
-    "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr",
+    "asap_bind_workspace", "asap_bind_models", "asap_bind_dense", "asap_bind_csr", "asap_set_csr_members",
+    "asap_get_csr_members",
     "asap_local_sgd", "asap_prepare_sgd", "asap_stochastic_reduce", "asap_round", "asap_run_rounds",
     "asap_current",
     "asap_set_round", "asap_drop_workers", "asap_get_graph", "asap_schedule_device", "asap_metrics", "asap_check",
@@ -83,6 +84,8 @@ def lib():
         "asap_bind_models": [p, p, p, i64, p],
         "asap_bind_dense": [p, p, p, i64, i64],
         "asap_bind_csr": [p, p, p, p, p, i64, i64, p],
+        "asap_set_csr_members": [p, i32],
+        "asap_get_csr_members": [p, C.POINTER(i32)],
         "asap_local_sgd": [p, C.POINTER(SgdParams), p],
         "asap_prepare_sgd": [p, C.POINTER(SgdParams), p],
         "asap_stochastic_reduce": [p, p],
@@ -226,6 +229,16 @@ def asap_bind_models(ctx, buf0, buf1, ld: int, stream=None):
 
 def asap_bind_dense(ctx, X, y, samples: int, ldx: int):
     _check(lib().asap_bind_dense(ctx, _dev(X), _dev(y), samples, ldx), ctx)
+
+
+def asap_set_csr_members(ctx, members: int):
+    _check(lib().asap_set_csr_members(ctx, int(members)), ctx)
+
+
+def asap_get_csr_members(ctx) -> int:
+    m = C.c_int32(0)
+    _check(lib().asap_get_csr_members(ctx, C.byref(m)), ctx)
+    return m.value
 
 
 def asap_bind_csr(ctx, row_ptr, col, val, y, samples: int, nnz: int, stream=None):
@@ -401,6 +414,14 @@ class Session:
         asap_bind_csr(self.ctx, rp, cl, vl, yy, samples, int(cl.numel()))
         self._data = ("csr", rp, cl, vl, yy, int(samples))
         self.ws = None
+
+    def set_csr_members(self, members):
+        """Workgroups per worker of the planned CSR pass (0: the library's choice)."""
+        asap_set_csr_members(self.ctx, members)
+        self.ws = None
+
+    def csr_members(self):
+        return asap_get_csr_members(self.ctx)
 
     def ready(self, stream=None):
         """(Re)bind a workspace of the size the current bindings need."""

@@ -39,8 +39,11 @@ constexpr int32_t kRoundsWaitMs = 10000;  // default bound on one neighbour wait
 // and the column plan.  CSR workspaces hold two, so that the next round can
 // be planned while this one runs.
 struct RoundPlan {
-  size_t sched = 0, rowinfo = 0, soff = 0, pack = 0, clist = 0, clink = 0, hlist = 0, cnt = 0, flag = 0;
+  size_t sched = 0, rowinfo = 0, vrowinfo = 0, soff = 0, pack = 0, clist = 0, clink = 0, hlist = 0, cnt = 0,
+         flag = 0;
 };
+
+constexpr long long kMemberWaitMs = 2000;  // bound on one wait of a planned-pass member for a partner
 
 }  // namespace
 
@@ -55,6 +58,7 @@ struct asap_ctx {
   int32_t max_deg = 0;  // longest row of the graph (entries, self included)
   int32_t max_out = 0;  // most workers that read one row
   int32_t n_cu = 256;   // compute units of the device the workspace is on
+  long long clock_khz = 100000;  // its wall clock (s_memrealtime) rate
 
   // caller-owned device memory
   char* ws = nullptr;
@@ -77,12 +81,19 @@ struct asap_ctx {
   std::vector<int16_t> hot_lut;
   int32_t max_row = 0;
   int64_t max_wnnz = 0;  // most nonzeros of one worker's shard
+  // members of the planned CSR pass: workgroups per worker, member m owning
+  // the columns c mod members == m (1: the worker's pass is one workgroup)
+  int32_t members = 1;
+  int32_t members_req = 0;   // asap_set_csr_members (0: chosen from the worker and compute-unit counts)
+  int32_t max_slice = 0;     // longest row of one member's columns
+  int32_t n_mhot[kMaxMembers] = {0, 0, 0, 0};
+  uint64_t xseq = 1;         // exchange tag of the next planned step (never reused by a context)
 
   // workspace layout (byte offsets)
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_optr = 0, off_oidx = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
          off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dxcd = 0, off_dcount = 0, off_progress = 0,
-         total = 0;
+         off_vrp = 0, off_vcode = 0, off_mlut = 0, off_mhot = 0, off_xch = 0, off_done = 0, total = 0;
   RoundPlan plan[2];
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
@@ -152,6 +163,23 @@ T* at(asap_ctx* c, size_t off) {
   return reinterpret_cast<T*>(c->ws + off);
 }
 
+// Members of the planned CSR pass: the caller's choice, else 4 or 2
+// workgroups per worker while they take at most half the compute units
+// (the other half plans the next pass beside it), else 1.
+int32_t csr_members(asap_ctx* c) {
+  if (c->members_req > 0) return c->members_req;
+  int cus = c->n_cu;
+  {
+    int dev_id = 0, q = 0;
+    if (hipGetDevice(&dev_id) == hipSuccess &&
+        hipDeviceGetAttribute(&q, hipDeviceAttributeMultiprocessorCount, dev_id) == hipSuccess && q > 0)
+      cus = q;
+  }
+  for (int32_t m = kMaxMembers; m > 1; m /= 2)
+    if (int64_t(c->n) * m <= cus / 2) return m;
+  return 1;
+}
+
 void layout(asap_ctx* c) {
   const size_t n = size_t(c->n), nnz = c->idx.size();
   size_t o = 0;
@@ -175,18 +203,28 @@ void layout(asap_ctx* c) {
   c->off_lut = o;     o = align_up(o + (csr ? size_t(c->dim) * 2 : 0));
   c->off_hot = o;     o = align_up(o + (csr ? size_t(kHotMax) * 4 : 0));
   c->off_progress = o; o = align_up(o + (csr ? n * 8 : 0));
+  c->members = csr ? csr_members(c) : 1;
+  const size_t M = size_t(c->members), split = csr && M > 1 ? 1 : 0;
+  c->off_vrp = o;   o = align_up(o + split * (n * M * size_t(c->S) + 1) * 8);
+  c->off_vcode = o; o = align_up(o + split * size_t(c->nnz) * 4);
+  c->off_mlut = o;  o = align_up(o + split * size_t(c->dim) * 2);
+  c->off_mhot = o;  o = align_up(o + split * M * kHotMax * 4);
+  c->off_xch = o;   o = align_up(o + split * 2 * n * M * 128 * 8);
+  c->off_done = o;  o = align_up(o + split * n * M * 8);
   // per-round buffers of the CSR pass, twice: one entry per nonzero per list
   const size_t nz = csr ? size_t(c->nnz) : 0, nS = csr ? n * size_t(c->S) : 0;
   for (int k = 0; k < 2; ++k) {
     RoundPlan& r = c->plan[k];
     if (k == 1) { r.sched = o; o = align_up(o + (csr ? nS * 4 : 0)); }
     r.rowinfo = o; o = align_up(o + nS * sizeof(RowInfo));
-    r.soff = o;    o = align_up(o + (csr ? n * (size_t(c->S) + 1) * 4 : 0));
+    r.vrowinfo = r.rowinfo;
+    if (split) { r.vrowinfo = o; o = align_up(o + M * nS * sizeof(RowInfo)); }
+    r.soff = o;    o = align_up(o + (csr ? M * n * (size_t(c->S) + 1) * 4 : 0));
     r.pack = o;    o = align_up(o + nz * 8);
     r.clist = o;   o = align_up(o + nz * 4);
     r.clink = o;   o = align_up(o + nz * 4);
     r.hlist = o;   o = align_up(o + nz * 4);
-    r.cnt = o;     o = align_up(o + nS * 2 * 4);
+    r.cnt = o;     o = align_up(o + M * nS * 2 * 4);
     r.flag = o;    o = align_up(o + (csr ? 4 : 0));
   }
   const int cpq = c->kind == kDense ? dense_wide_cpq(c->dim) : 0;
@@ -343,7 +381,78 @@ asap_status choose_hot_columns(asap_ctx* c, hipStream_t s) {
       (e = launch_codes(c->col, c->nnz, lut, at<int32_t>(c, c->off_code), s)) ||
       (e = hipStreamSynchronize(s)))
     return hip_fail(c, e, "hot column tables");
+  c->n_mhot[0] = int32_t(H);
+  if (c->members > 1) {
+    // each member keeps the most frequent of its own columns, by the same
+    // order
+    const int32_t M = c->members;
+    std::vector<int32_t> mhot(size_t(M) * kHotMax, 0);
+    std::vector<int16_t> mlut(size_t(D), int16_t(-1));
+    for (int32_t m = 0; m < M; ++m) {
+      std::vector<int32_t> own;
+      for (int32_t j : cols)
+        if (j % M == m) own.push_back(j);
+      const size_t Hm = std::min<size_t>(own.size(), kHotMax);
+      std::partial_sort(own.begin(), own.begin() + Hm, own.end(), [&](int32_t x, int32_t y) {
+        return h[x] != h[y] ? h[x] > h[y] : x < y;
+      });
+      for (size_t k = 0; k < Hm; ++k) {
+        mhot[size_t(m) * kHotMax + k] = own[k];
+        mlut[own[k]] = int16_t(k);
+      }
+      c->n_mhot[m] = int32_t(Hm);
+    }
+    if ((e = hipMemcpyAsync(at<int32_t>(c, c->off_mhot), mhot.data(), mhot.size() * 4, hipMemcpyHostToDevice, s)) ||
+        (e = hipMemcpyAsync(at<int16_t>(c, c->off_mlut), mlut.data(), size_t(D) * 2, hipMemcpyHostToDevice, s)) ||
+        (e = hipStreamSynchronize(s)))
+      return hip_fail(c, e, "member hot column tables");
+  }
   return ASAP_OK;
+}
+
+// Members > 1: the slices' row offsets (each worker's rows restricted to
+// each member's columns, slice v = worker * members + member, laid out one
+// after another) and every nonzero's code in slice order.  One member: the
+// slices are the workers.
+asap_status split_members(asap_ctx* c, hipStream_t s) {
+  c->max_slice = c->max_row;
+  if (c->members == 1) return ASAP_OK;
+  hipError_t e;
+  const int32_t M = c->members;
+  const size_t rows = size_t(c->n) * size_t(M) * size_t(c->S);
+  // the counts (int32) go to the slice-offset array first, which the
+  // offsets (int64, summed on the host) then replace
+  int32_t* cnt = at<int32_t>(c, c->off_vrp);
+  int32_t* mx = at<int32_t>(c, c->off_scan);
+  std::vector<int32_t> h(rows);
+  if ((e = launch_fill_i32(mx, 1, 0, s)) ||
+      (e = launch_member_count(c->row_ptr, c->col, c->n, c->S, M, cnt, mx, s)) ||
+      (e = hipMemcpyAsync(h.data(), cnt, rows * 4, hipMemcpyDeviceToHost, s)) ||
+      (e = hipMemcpyAsync(&c->max_slice, mx, 4, hipMemcpyDeviceToHost, s)) || (e = hipStreamSynchronize(s)))
+    return hip_fail(c, e, "member split counts");
+  std::vector<int64_t> vrp(rows + 1);
+  int64_t acc = 0;
+  for (size_t q = 0; q < rows; ++q) {
+    vrp[q] = acc;
+    acc += h[q];
+  }
+  vrp[rows] = acc;
+  if (acc != c->nnz) return fail(c, ASAP_E_INVALID_ARG, "member split counted %lld of %lld nonzeros",
+                                 (long long)acc, (long long)c->nnz);
+  int64_t* d_vrp = at<int64_t>(c, c->off_vrp);
+  if ((e = hipMemcpyAsync(d_vrp, vrp.data(), (rows + 1) * 8, hipMemcpyHostToDevice, s)) ||
+      (e = launch_member_scatter(c->row_ptr, c->col, c->val, at<int16_t>(c, c->off_mlut), c->n, c->S, M, d_vrp,
+                                 at<int32_t>(c, c->off_vcode), nullptr, s)) ||
+      (e = hipStreamSynchronize(s)))
+    return hip_fail(c, e, "member split");
+  return ASAP_OK;
+}
+
+// The bind-time halves of a plan's (code, value) pairs, in slice order.
+hipError_t write_pack(asap_ctx* c, int2* pack, hipStream_t s) {
+  if (c->members == 1) return launch_pack_values(at<int32_t>(c, c->off_code), c->val, c->nnz, pack, s);
+  return launch_member_scatter(c->row_ptr, c->col, c->val, at<int16_t>(c, c->off_mlut), c->n, c->S, c->members,
+                               at<int64_t>(c, c->off_vrp), nullptr, pack, s);
 }
 
 }  // namespace
@@ -660,6 +769,24 @@ extern "C" asap_status asap_bind_csr(asap_ctx* c, const int64_t* row_ptr, const 
   return ASAP_OK;
 }
 
+extern "C" asap_status asap_set_csr_members(asap_ctx* c, int32_t members) {
+  if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
+  if (members != 0 && members != 1 && members != 2 && members != 4)
+    return fail(c, ASAP_E_INVALID_ARG, "members must be 0, 1, 2 or 4 (got %d)", members);
+  c->members_req = members;
+  if (c->kind == kCsr) {
+    layout(c);
+    unbind_workspace(c);
+  }
+  return ASAP_OK;
+}
+
+extern "C" asap_status asap_get_csr_members(const asap_ctx* c, int32_t* members) {
+  if (!c || !members) return fail(const_cast<asap_ctx*>(c), ASAP_E_INVALID_ARG, "ctx or members is NULL");
+  *members = c->members;
+  return ASAP_OK;
+}
+
 extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes, void* stream) {
   if (!c) return fail(nullptr, ASAP_E_INVALID_ARG, "ctx is NULL");
   if (!dev || uintptr_t(dev) % kAlign) return fail(c, ASAP_E_INVALID_ARG, "workspace must be 256-byte aligned");
@@ -674,6 +801,9 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     if (hipGetDevice(&dev_id) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev_id) == hipSuccess && cus > 0)
       c->n_cu = cus;
+    int khz = 0;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev_id) == hipSuccess && khz > 0)
+      c->clock_khz = khz;
   }
   c->ws = static_cast<char*>(dev);
   c->ws_bytes = bytes;
@@ -734,12 +864,17 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     c->max_wnnz = h[5];
     asap_status hs = choose_hot_columns(c, s);
     if (hs != ASAP_OK) return hs;
+    hs = split_members(c, s);
+    if (hs != ASAP_OK) return hs;
     // the value half of every planned (code, value) pair, and the code half
     // of a hot entry, do not change from round to round: written here, once
     // per plan slot (planning rewrites the cold entries' codes)
     for (int k = 0; k < 2; ++k)
-      if ((e = launch_pack_values(at<int32_t>(c, c->off_code), c->val, c->nnz, at<int2>(c, c->plan[k].pack), s)))
-        return hip_fail(c, e, "plan values");
+      if ((e = write_pack(c, at<int2>(c, c->plan[k].pack), s))) return hip_fail(c, e, "plan values");
+    if (c->members > 1 &&
+        (e = launch_fill_i64(at<int64_t>(c, c->off_xch), 2 * int64_t(n) * c->members * 128, 0, s)) ||
+        (c->members > 1 && (e = launch_fill_i64(at<int64_t>(c, c->off_done), int64_t(n) * c->members, 0, s))))
+      return hip_fail(c, e, "member exchange init");
     if (!c->ahead) {
       if ((e = hipStreamCreateWithFlags(&c->ahead, hipStreamNonBlocking))) {
         c->ahead = nullptr;
@@ -806,10 +941,26 @@ SgdArgs sgd_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp) {
   return a;
 }
 
-// The planned pass applies when its shape fits (csr_plan_fits) and a
-// worker's (code, value) pairs are addressed by 32-bit byte offsets.
+// The planned pass applies when its shape fits (csr_plan_fits, on the
+// members' slices) and a worker's (code, value) pairs are addressed by
+// 32-bit byte offsets.
 bool planned_pass(const asap_ctx* c, const SgdArgs& a) {
-  return csr_plan_fits(a) && c->max_wnnz < (int64_t(1) << 29);
+  SgdArgs f = a;
+  f.max_row = c->max_slice;
+  return csr_plan_fits(f) && c->max_wnnz < (int64_t(1) << 29);
+}
+
+// The planned pass's arguments: the exchange tags of its `steps` steps
+// (unique for the life of the context).  The pass gives the same bits for
+// any entries-per-lane count that covers its rows, so the stream-ordered
+// launch sizes it for the slices' rows; the multi-round launch keeps the
+// general pass's (whole rows), which shares its kernel.
+SgdArgs fast_args(asap_ctx* c, const SgdArgs& a, int64_t steps) {
+  SgdArgs f = a;
+  f.xtag = uint32_t(c->xseq);
+  f.xg0 = a.round * ((c->S + a.batch - 1) / a.batch) + a.k0;
+  c->xseq += uint64_t(steps);
+  return f;
 }
 
 // The plan arrays of rp live at `base` + their offsets: the workspace by
@@ -817,11 +968,21 @@ bool planned_pass(const asap_ctx* c, const SgdArgs& a) {
 PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp, char* base = nullptr) {
   if (!base) base = c->ws;
   auto at = [base](size_t off) { return base + off; };
+  const bool split = c->members > 1;
   PlanArgs pa{};
-  pa.rowinfo = reinterpret_cast<RowInfo*>(at(rp.rowinfo));
-  pa.code = ::at<int32_t>(c, c->off_code);
-  pa.row_ptr = c->row_ptr;
-  pa.n = c->n;
+  pa.rowinfo = reinterpret_cast<RowInfo*>(at(rp.vrowinfo));
+  pa.rows_real = reinterpret_cast<RowInfo*>(at(rp.rowinfo));
+  pa.code = split ? ::at<int32_t>(c, c->off_vcode) : ::at<int32_t>(c, c->off_code);
+  pa.row_ptr = split ? ::at<int64_t>(c, c->off_vrp) : c->row_ptr;
+  pa.n = c->n * c->members;  // slices
+  pa.members = c->members;
+  pa.workers = c->n;
+  pa.mhot = split ? ::at<int32_t>(c, c->off_mhot) : ::at<int32_t>(c, c->off_hot);
+  for (int m = 0; m < kMaxMembers; ++m) pa.n_mhot[m] = m < c->members ? c->n_mhot[m] : 0;
+  pa.xch = split ? ::at<unsigned long long>(c, c->off_xch) : nullptr;
+  pa.done = split ? ::at<unsigned long long>(c, c->off_done) : nullptr;
+  pa.xerr = ::at<int32_t>(c, c->off_err) + kErrRendezvous;
+  pa.xwait = kMemberWaitMs * c->clock_khz;
   pa.S = c->S;
   pa.batch = p->batch;
   pa.K = int32_t((c->S + p->batch - 1) / p->batch);
@@ -835,8 +996,8 @@ PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp, c
   pa.flag = reinterpret_cast<int32_t*>(at(rp.flag));
   pa.progress = ::at<int64_t>(c, c->off_progress);
   // a prefetch workgroup per worker when both fit beside each other and
-  // worker i's pair lands on one XCD
-  pa.helpers = (c->n % 8 == 0 && 2 * c->n <= c->n_cu) ? 1 : 0;
+  // worker i's pair lands on one XCD (one member per worker only)
+  pa.helpers = (!split && c->n % 8 == 0 && 2 * c->n <= c->n_cu) ? 1 : 0;
   return pa;
 }
 
@@ -852,8 +1013,11 @@ hipError_t prepare_csr_round(asap_ctx* c, const asap_sgd_params* p, int64_t roun
     e = launch_rowinfo(sched, c->row_ptr, c->y, c->n, c->S, reinterpret_cast<RowInfo*>(base + rp.rowinfo), s);
   if (planned) {
     const PlanArgs pa = plan_args(c, p, rp, base);
+    if (e == hipSuccess && c->members > 1)
+      e = launch_rowinfo(sched, pa.row_ptr, c->y, c->n, c->S, reinterpret_cast<RowInfo*>(base + rp.vrowinfo), s,
+                         c->members);
     if (e == hipSuccess) e = launch_fill_i32(pa.flag, 1, 0, s);
-    if (e == hipSuccess) e = launch_csr_plan(pa, c->max_row, s);
+    if (e == hipSuccess) e = launch_csr_plan(pa, c->max_slice, s);
   }
   return e;
 }
@@ -930,7 +1094,11 @@ extern "C" asap_status asap_local_sgd(asap_ctx* c, const asap_sgd_params* p, voi
       a.run_if = pa.flag;
       if (e == hipSuccess) e = launch_sgd_csr(a, s);
       if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_start, s);
-      if (e == hipSuccess) e = launch_sgd_csr_fast(a, pa, s);
+      if (e == hipSuccess) {
+        SgdArgs f = fast_args(c, a, a.k1 - a.k0);
+        f.max_row = c->max_slice;
+        e = launch_sgd_csr_fast(f, pa, s);
+      }
     } else {
       if (e == hipSuccess && c->ahead) e = hipEventRecord(c->ev_start, s);
       if (e == hipSuccess) e = launch_sgd_csr(a, s);
@@ -1028,16 +1196,18 @@ namespace {
 // One area of the plan ring: the arrays of one pass's plan (as a RoundPlan
 // slot of the workspace); returns its size.
 size_t ring_layout(const asap_ctx* c, RoundPlan* lay) {
-  const size_t n = size_t(c->n), nS = n * size_t(c->S), nz = size_t(c->nnz);
+  const size_t n = size_t(c->n), nS = n * size_t(c->S), nz = size_t(c->nnz), M = size_t(c->members);
   size_t o = 0;
   lay->sched = o;   o = align_up(o + nS * 4);
   lay->rowinfo = o; o = align_up(o + nS * sizeof(RowInfo));
-  lay->soff = o;    o = align_up(o + n * (size_t(c->S) + 1) * 4);
+  lay->vrowinfo = lay->rowinfo;
+  if (M > 1) { lay->vrowinfo = o; o = align_up(o + M * nS * sizeof(RowInfo)); }
+  lay->soff = o;    o = align_up(o + M * n * (size_t(c->S) + 1) * 4);
   lay->pack = o;    o = align_up(o + nz * 8);
   lay->clist = o;   o = align_up(o + nz * 4);
   lay->clink = o;   o = align_up(o + nz * 4);
   lay->hlist = o;   o = align_up(o + nz * 4);
-  lay->cnt = o;     o = align_up(o + nS * 2 * 4);
+  lay->cnt = o;     o = align_up(o + M * nS * 2 * 4);
   lay->flag = o;    o = align_up(o + 4);
   return o;
 }
@@ -1073,8 +1243,7 @@ extern "C" asap_status asap_bind_rounds_plan(asap_ctx* c, void* dev, size_t byte
   // the bind-time halves of every area's (code, value) pairs, as for the
   // workspace's two plan slots
   for (int64_t u = 0; u < areas && e == hipSuccess; ++u)
-    e = launch_pack_values(at<int32_t>(c, c->off_code), c->val, c->nnz,
-                           reinterpret_cast<int2*>(base + ring_head(areas) + size_t(u) * stride + lay.pack), s);
+    e = write_pack(c, reinterpret_cast<int2*>(base + ring_head(areas) + size_t(u) * stride + lay.pack), s);
   if (e == hipSuccess && !c->ev_ring_free) {
     if ((e = hipEventCreateWithFlags(&c->ev_ring_free, hipEventDisableTiming))) c->ev_ring_free = nullptr;
   }
@@ -1154,7 +1323,7 @@ extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, in
       rp.npass = npass;
       rp.ready = reinterpret_cast<const int64_t*>(c->ring);
       rp.token0 = (++c->ring_epoch) << 24;
-      const int64_t blocks = int64_t(c->n) * (rp.area0.helpers ? 2 : 1);
+      const int64_t blocks = int64_t(c->n) * c->members + (rp.area0.helpers ? c->n : 0);
       const bool beside = c->ahead && blocks + 64 <= c->n_cu;
       hipStream_t ps = beside ? c->ahead : s;
       if (beside) e = hipStreamWaitEvent(ps, c->ev_ring_free, 0);
@@ -1165,7 +1334,9 @@ extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, in
         if (e == hipSuccess) e = launch_fill_i64(reinterpret_cast<int64_t*>(c->ring) + u, 1, rp.token0 + u, ps);
       }
       if (e != hipSuccess) return hip_fail(c, e, "launch planning");
-      e = launch_rounds_csr_planned(a, ra, rp, c->n_cu, s);
+      // exchange tags of every step the launch runs (rounds are consecutive steps)
+      const int64_t per_round = p->local_steps == 0 ? K : p->local_steps;
+      e = launch_rounds_csr_planned(fast_args(c, a, rounds * per_round), ra, rp, c->n_cu, s);
       if (e == hipSuccess) e = hipEventRecord(c->ev_ring_free, s);
     } else {
       e = launch_rounds_csr(a, ra, c->n_cu, s);
@@ -1379,7 +1550,7 @@ extern "C" asap_status asap_check(asap_ctx* c, void* stream, int32_t* bad_worker
     if ((e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)) ||
         (e = hipStreamSynchronize(s)))
       return hip_fail(c, e, "error reset");
-    return fail(c, ASAP_E_DEVICE, "dense SGD: %d workgroup rendezvous timed out; the pass was cut short",
+    return fail(c, ASAP_E_DEVICE, "SGD: %d waits of a worker's workgroups for each other timed out; the pass was cut short",
                 h[kErrRendezvous]);
   }
   if (h[0] != 0) {

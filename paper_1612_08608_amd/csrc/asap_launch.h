@@ -79,6 +79,11 @@ struct SgdArgs {
   int64_t* tag;     // [n] tags of the current buffer
   int64_t tag_value;
   const int32_t* run_if;  // CSR general kernel: when set, run only if *run_if != 0
+  // planned CSR pass with members (PlanArgs::members > 1): the exchange tag
+  // of global step g = round * K + k is xtag + (g - xg0); the library keeps
+  // tags unique for the life of a context
+  uint32_t xtag;
+  int64_t xg0;
 };
 
 // Per-round plan of a CSR pass (see kernels_csr_plan.hip).  The per-step
@@ -87,6 +92,7 @@ struct SgdArgs {
 // entry per nonzero.
 struct PlanArgs {
   const RowInfo* rowinfo;   // [n][S] this round's rows in schedule order
+  const RowInfo* rows_real; // [workers][S] the same for whole workers (the general pass; = rowinfo with one member)
   const int32_t* code;      // [nnz] static codes: -(hot slot + 2) or column
   const int64_t* row_ptr;   // [n*S+1]
   int32_t n;
@@ -103,7 +109,21 @@ struct PlanArgs {
   int32_t* flag;            // [1] set when some step does not fit the fast kernel
   int64_t* progress;        // [n] global step the pass of each worker is on (round * K + k)
   int32_t helpers;          // 1: one prefetch workgroup per worker beside the pass
+  // Members: `members` workgroups share a worker, member m owning the
+  // columns c with c mod members == m.  The plan arrays above then describe
+  // n * members "slices" (slice v = worker * members + member: the worker's
+  // rows restricted to the member's columns, laid out like a worker of their
+  // own), and n counts slices.  With one member a slice is the worker.
+  int32_t members;
+  int32_t workers;          // real workers
+  const int32_t* mhot;      // [members][kHotMax] column of each member's hot slot
+  int32_t n_mhot[4];        // hot slots of each member
+  unsigned long long* xch;  // [2][workers][members][64][2] tagged halves of partial margins
+  unsigned long long* done; // [workers][members] multi-round launch: tag of a member's last step
+  int32_t* xerr;            // error word: a member waited too long for a partner
+  long long xwait;          // wall-clock ticks a member waits for a partner
 };
+constexpr int kMaxMembers = 4;
 bool csr_plan_fits(const SgdArgs& a);
 hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s);
 // pack[q] = (code[q], bits of val[q]) for every nonzero: the round-invariant
@@ -181,7 +201,17 @@ int dense_wide_max_members(const SgdArgs& a, int n_cu);        // co-resident wo
 hipError_t launch_sgd_dense_wide(const SgdArgs& a, const DenseSync& ds, hipStream_t s);
 hipError_t launch_sgd_csr(const SgdArgs& a, hipStream_t s);
 hipError_t launch_rowinfo(const int32_t* sched, const int64_t* row_ptr, const float* y, int32_t n, int64_t S,
-                          RowInfo* out, hipStream_t s);
+                          RowInfo* out, hipStream_t s, int32_t members = 1);
+// Bind time, members > 1: cnt[(i * members + m) * S + r] = nonzeros of row r
+// of worker i in member m's columns; *maxlen (zeroed before) = the largest.
+hipError_t launch_member_count(const int64_t* row_ptr, const int32_t* col, int32_t n, int64_t S, int32_t members,
+                               int32_t* cnt, int32_t* maxlen, hipStream_t s);
+// Bind time, members > 1: each nonzero to its slice position (vrow_ptr, rows
+// keep their entries' order): vcode (if not null) gets its code from mlut
+// (member-local hot slot or -1), pack (if not null) its (code, value) pair.
+hipError_t launch_member_scatter(const int64_t* row_ptr, const int32_t* col, const float* val, const int16_t* mlut,
+                                 int32_t n, int64_t S, int32_t members, const int64_t* vrow_ptr, int32_t* vcode,
+                                 int2* pack, hipStream_t s);
 hipError_t launch_col_hist(const int32_t* col, int64_t nnz, int64_t stride, int32_t* counts, hipStream_t s);
 hipError_t launch_codes(const int32_t* col, int64_t nnz, const int16_t* lut, int32_t* code, hipStream_t s);
 

@@ -28,6 +28,7 @@ struct FastShared {
   unsigned long long acch[kHotMax];
   float cval[2][kCMax];  // cold values of steps k (slot k & 1) and k - 1
   unsigned long long cacc[kCMax];
+  int xabort;            // members: a partner's partial margin did not arrive in time
 };
 static_assert(sizeof(FastShared) <= 160 * 1024, "LDS budget of one workgroup");
 
@@ -102,6 +103,23 @@ __device__ __forceinline__ void hold(float (&v)[N]) {
     asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7]));
 }
 
+// Worker i and member m of workgroup b (grid n * members): a worker's
+// members on one XCD when the grid allows (workgroups are dealt to the 8
+// XCDs round-robin), so that their exchange stays in one L2.
+__device__ __forceinline__ void member_of(int b, int n, int M, int& i, int& m) {
+  if (M == 1) {
+    i = b;
+    m = 0;
+  } else if (n % 8 == 0) {
+    const int j = b / 8;
+    i = (b % 8) * (n / 8) + j / M;
+    m = j % M;
+  } else {
+    i = b / M;
+    m = b % M;
+  }
+}
+
 constexpr uint32_t kPrefetchSpin = 1u << 16;  // polls of the pass's progress per step (bounded)
 constexpr int kPrefetchLead = 3;              // steps ahead of the pass
 
@@ -117,9 +135,9 @@ template <int E>
 __device__ void prefetch_pass(const SgdArgs& a, const PlanArgs& p, int i) {
   const int tid = threadIdx.x, sub = tid & (kRowLanes - 1), b = tid / kRowLanes;
   const int64_t K = (a.S + a.batch - 1) / a.batch;
-  const RowInfo* ri = a.rowinfo + int64_t(i) * a.S;
-  const long long seg = a.row_ptr[int64_t(i) * a.S];
-  const uint32_t nnz_w = uint32_t(a.row_ptr[int64_t(i + 1) * a.S] - seg);
+  const RowInfo* ri = p.rowinfo + int64_t(i) * a.S;
+  const long long seg = p.row_ptr[int64_t(i) * a.S];
+  const uint32_t nnz_w = uint32_t(p.row_ptr[int64_t(i + 1) * a.S] - seg);
   const auto pk = rsrc(p.pack + seg, nnz_w * 8u);
   const auto model = rsrc(a.models + int64_t(i) * a.ld, uint32_t(a.dim) * 4u);
   const auto clist = rsrc(p.clist + seg, nnz_w * 4u);
@@ -163,35 +181,87 @@ __device__ void prefetch_pass(const SgdArgs& a, const PlanArgs& p, int i) {
   asm volatile("" ::"v"(sink));
 }
 
-// Worker i's planned pass (steps [a.k0, a.k1) of pass a.round on the plan
-// p); `sh` is the workgroup's LDS for it.  Writes the final L2 scale, and
-// the epoch tag when a.tag is set.
-template <int E>
-__device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, FastShared& sh) {
+// Members (p.members > 1): the partial margins of one step are exchanged
+// through p.xch, two tagged 64-bit words per (member, row): the low and
+// the high half of the fp64 partial, each beside the step's 32-bit tag, so
+// a word is whole or stale, never torn, and no fence or counter is needed.
+// Lanes 0, 1 of each 16-lane row publish; lanes 2 m', 2 m' + 1 read member
+// m''s halves (a bounded wait), and every lane of the row adds the members'
+// partials in member order, so all members get the same margin bit for bit.
+__device__ __forceinline__ double member_exchange(const PlanArgs& p, int i, int m, int brow, int lane, uint32_t tag,
+                                                  double part, bool live, FastShared& sh) {
+  const int M = p.members, sub = lane & (kRowLanes - 1), mm = sub >> 1;
+  unsigned long long* slot = p.xch + ((size_t(tag & 1u) * size_t(p.workers) + size_t(i)) * size_t(M)) * 128u;
+  const uint32_t lo = uint32_t(__double2loint(part)), hi = uint32_t(__double2hiint(part));
+  if (live && sub < 2)
+    __hip_atomic_store(slot + (m * 64 + brow) * 2 + sub,
+                       (static_cast<unsigned long long>(tag) << 32) | (sub ? hi : lo), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  uint32_t half = 0;
+  if (live && mm < M) {
+    if (mm == m) {
+      half = (sub & 1) ? hi : lo;
+    } else {
+      const unsigned long long* src = slot + (mm * 64 + brow) * 2 + (sub & 1);
+      unsigned long long w = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (uint32_t(w >> 32) != tag) {
+        const long long deadline = wall_clock64() + p.xwait;
+        do {
+          __builtin_amdgcn_s_sleep(1);
+          w = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } while (uint32_t(w >> 32) != tag && wall_clock64() < deadline);
+        if (uint32_t(w >> 32) != tag) {
+          sh.xabort = 1;
+          atomicAdd(p.xerr, 1);
+        }
+      }
+      half = uint32_t(w);
+    }
+  }
+  const int base = lane & ~(kRowLanes - 1);
+  double dot = 0.0;
+  for (int q = 0; q < M; ++q) {
+    const int l = __shfl(int(half), base + 2 * q, 64);
+    const int h = __shfl(int(half), base + 2 * q + 1, 64);
+    dot += __hiloint2double(h, l);
+  }
+  return dot;
+}
+
+// Member m of worker i: its slice's planned pass (steps [a.k0, a.k1) of
+// pass a.round on the plan p); `sh` is the workgroup's LDS for it.  Member 0
+// writes the final L2 scale, and the epoch tag when a.tag is set.  MEM:
+// p.members > 1 (with one member the slice is the whole worker and nothing
+// is exchanged).
+template <int E, bool MEM>
+__device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, FastShared& sh) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane & (kRowLanes - 1);
   const int brow = wave * (64 / kRowLanes) + (lane / kRowLanes);
+  const int M = MEM ? p.members : 1, v = i * M + m;
   float* vrow = a.models + int64_t(i) * a.ld;
-  const RowInfo* ri = a.rowinfo + int64_t(i) * a.S;
-  const int H = a.n_hot;
+  const RowInfo* ri = p.rowinfo + int64_t(v) * a.S;
+  const int H = p.n_mhot[m];
+  const int32_t* hot_cols = p.mhot + m * kHotMax;
   const int64_t K = (a.S + a.batch - 1) / a.batch;
   const int64_t k0 = a.k0, kend = a.k1;  // steps [k0, kend) of the pass run here
   Views w;
-  w.seg = a.row_ptr[int64_t(i) * a.S];
-  const uint32_t nnz_w = uint32_t(a.row_ptr[int64_t(i + 1) * a.S] - w.seg);
+  w.seg = p.row_ptr[int64_t(v) * a.S];
+  const uint32_t nnz_w = uint32_t(p.row_ptr[int64_t(v + 1) * a.S] - w.seg);
   const auto pk = rsrc(p.pack + w.seg, nnz_w * 8u);
   w.model = rsrc(vrow, uint32_t(a.dim) * 4u);
   const auto clist = rsrc(p.clist + w.seg, nnz_w * 4u);
   const auto clink = rsrc(p.clink + w.seg, nnz_w * 4u);
   const auto hlist = rsrc(p.hlist + w.seg, nnz_w * 4u);
-  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(a.k1) * 4u);  // steps past the launch read 0
-  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(a.k1) * 8u);
+  const auto so_v = rsrc(p.step_off + int64_t(v) * (a.S + 1), uint32_t(a.k1) * 4u);  // steps past the launch read 0
+  const auto cn_v = rsrc(p.cnt + int64_t(v) * K * 2, uint32_t(a.k1) * 8u);
 
   for (int h = tid; h < H; h += kThreads) {
-    sh.vhot[h] = vrow[a.hot_cols[h]];
+    sh.vhot[h] = vrow[hot_cols[h]];
     sh.acch[h] = 0ull;
   }
   for (int q = tid; q < kCMax; q += kThreads) sh.cacc[q] = 0ull;
+  if (tid == 0) sh.xabort = 0;
   // fixed point as in the general kernel: |column sum| <= B vmax < 2^e
   int e2 = 0;
   frexp(double(a.batch) * double(a.vmax[i]), &e2);
@@ -327,7 +397,10 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, FastShared
     double part = 0.0;
 #pragma unroll
     for (int j = 0; j < E; ++j) part = fma(double(d0.val[j]), double(code_at(d0, j) == -1 ? 0.f : v[j]), part);
-    const double dot = row16_sum(part);
+    double dot = row16_sum(part);
+    if constexpr (MEM)
+      dot = member_exchange(p, i, m, brow, lane, a.xtag + uint32_t(a.round * K + k - a.xg0), dot,
+                            row_valid(a, k, kend, brow), sh);
     const double cf = (d0.ok & kRowExists) ? loss_coef(s * dot, double(d0.y), a.loss) : 0.0;
     if (cf != 0.0) {
 #pragma unroll
@@ -395,7 +468,7 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, FastShared
       const float sf = float(s);
       __syncthreads();
       for (int h = tid; h < H; h += kThreads) sh.vhot[h] *= sf;
-      for (int64_t c = tid; c < a.dim; c += kThreads) vrow[c] *= sf;
+      for (int64_t c = m + int64_t(tid) * M; c < a.dim; c += int64_t(kThreads) * M) vrow[c] *= sf;  // own columns
 #pragma unroll
       for (int j = 0; j < kColdPer; ++j) {
         const int u = tid + j * kThreads;
@@ -405,12 +478,16 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, FastShared
       s = 1.0;
     }
     __syncthreads();  // full fence: model stores complete, LDS updates visible
+    if constexpr (MEM)
+      if (sh.xabort) break;  // reported through p.xerr; the partners time out too
   }
 
-  for (int h = tid; h < H; h += kThreads) vrow[a.hot_cols[h]] = sh.vhot[h];
+  for (int h = tid; h < H; h += kThreads) vrow[hot_cols[h]] = sh.vhot[h];
   if (tid == 0) {
-    a.scale[i] = float(s);
-    if (a.tag) a.tag[i] = a.tag_value;
+    if (m == 0) {
+      a.scale[i] = float(s);
+      if (a.tag) a.tag[i] = a.tag_value;
+    }
     if (p.helpers)
       __hip_atomic_store(p.progress + i, a.round * K + kend, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }

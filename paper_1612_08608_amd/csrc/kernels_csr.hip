@@ -429,6 +429,7 @@ __device__ __forceinline__ PlanArgs ring_area(const RoundsPlan& rp, int64_t u) {
   PlanArgs p = rp.area0;
   const int64_t d = u * rp.stride;
   p.rowinfo = reinterpret_cast<const RowInfo*>(reinterpret_cast<const char*>(p.rowinfo) + d);
+  p.rows_real = reinterpret_cast<const RowInfo*>(reinterpret_cast<const char*>(p.rows_real) + d);
   p.step_off = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.step_off) + d);
   p.pack = reinterpret_cast<int2*>(reinterpret_cast<char*>(p.pack) + d);
   p.clist = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(p.clist) + d);
@@ -456,7 +457,7 @@ __device__ inline bool wait_plan(const RoundsPlan& rp, int64_t u, long long dead
 // overflowed runs the general pass code, as the stream-ordered path does,
 // so both give the same bits.  With helpers, block n + i prefetches for
 // worker i, pass after pass.
-template <int E>
+template <int E, bool MEM>
 __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a, RoundsArgs ra, RoundsPlan rp) {
   union LdsUnion {
     Shared g;
@@ -465,8 +466,10 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
   __shared__ LdsUnion sh;
   __shared__ int plan_ok;
   const int64_t K = (a.S + a.batch - 1) / a.batch;
-  if (int(blockIdx.x) >= ra.n) {
-    // prefetch workgroup: the steps of each pass that this launch runs
+  const int M = MEM ? rp.area0.members : 1;
+  if (int(blockIdx.x) >= ra.n * M) {
+    // prefetch workgroup (one member per worker): the steps of each pass
+    // that this launch runs
     const int i = int(blockIdx.x) - ra.n;
     for (int64_t u = 0; u < rp.npass; ++u) {
       if (threadIdx.x == 0) plan_ok = wait_plan(rp, u, wall_clock64() + ra.wait_ticks);
@@ -494,15 +497,16 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
     }
     return;
   }
-  const int i = int(blockIdx.x);
+  int i, m;
+  member_of(int(blockIdx.x), ra.n, M, i, m);
   PlanArgs pu = ring_area(rp, 0);
   rounds::drive(
-      a, ra, i, 0,
+      a, ra, i, m,
       [&](int64_t pass) {
         const int64_t u = pass - rp.first_pass;
         if (threadIdx.x == 0) {
           plan_ok = wait_plan(rp, u, wall_clock64() + ra.wait_ticks);
-          if (!plan_ok) rounds::report_stale(ra.err, i);
+          if (!plan_ok && m == 0) rounds::report_stale(ra.err, i);
         }
         __syncthreads();
         rounds::acquire_fence();  // the plan was written by other kernels
@@ -511,12 +515,40 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
       [&](const SgdArgs& ar) {
         if (!plan_ok) return false;
         SgdArgs ap = ar;
-        ap.rowinfo = pu.rowinfo;
-        if (__hip_atomic_load(pu.flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-          csr_pass<E, true>(ap, i, sh.g);
-        else
-          fast_pass<E>(ap, pu, i, sh.f);
-        return true;
+        if (__hip_atomic_load(pu.flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+          // the general pass is one workgroup's: member 0 runs it alone
+          ap.rowinfo = pu.rows_real;
+          if (m == 0) csr_pass<E, true>(ap, i, sh.g);
+          return true;
+        }
+        fast_pass<E, MEM>(ap, pu, i, m, sh.f);
+        if constexpr (!MEM) return true;
+        // members: member 0 publishes the worker's half-step only after
+        // every member's model stores are complete and released
+        const uint32_t last = ap.xtag + uint32_t(ap.round * K + ap.k1 - 1 - ap.xg0);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          if (m != 0) {
+            __hip_atomic_store(pu.done + i * M + m, static_cast<unsigned long long>(last), __ATOMIC_RELEASE,
+                               __HIP_MEMORY_SCOPE_AGENT);
+          } else {
+            const long long deadline = wall_clock64() + ra.wait_ticks;
+            for (int q = 1; q < M && plan_ok; ++q)
+              while (__hip_atomic_load(pu.done + i * M + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) !=
+                     static_cast<unsigned long long>(last)) {
+                if (wall_clock64() > deadline) {
+                  plan_ok = 0;
+                  atomicAdd(pu.xerr, 1);
+                  break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+              }
+            rounds::acquire_fence();
+          }
+        }
+        __syncthreads();
+        return plan_ok != 0 && sh.f.xabort == 0;
       });
 }
 
@@ -539,38 +571,88 @@ hipError_t launch_rounds_pipe(const SgdArgs& a, const RoundsArgs& ra, int n_cu, 
   return pipe ? launch_rounds_e<E, true>(a, ra, n_cu, s) : launch_rounds_e<E, false>(a, ra, n_cu, s);
 }
 
-template <int E>
-hipError_t launch_rounds_planned_e(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
-                                   hipStream_t s) {
+template <int E, bool MEM>
+hipError_t launch_rounds_planned_em(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
+                                    hipStream_t s) {
   int per = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_csr_planned_kernel<E>, kThreads, 0);
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_csr_planned_kernel<E, MEM>, kThreads, 0);
   if (e != hipSuccess) return e;
-  const int64_t grid = int64_t(a.n) * (rp.area0.helpers ? 2 : 1);
+  const int64_t grid = int64_t(a.n) * rp.area0.members + (rp.area0.helpers ? a.n : 0);
   if (int64_t(per) * n_cu < grid) return hipErrorCooperativeLaunchTooLarge;
   SgdArgs aa = a;
   RoundsArgs rr = ra;
   RoundsPlan pp = rp;
   void* args[] = {&aa, &rr, &pp};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&rounds_csr_planned_kernel<E>),
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&rounds_csr_planned_kernel<E, MEM>),
                                     dim3(uint32_t(grid)), dim3(kThreads), args, 0, s);
+}
+
+template <int E>
+hipError_t launch_rounds_planned_e(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
+                                   hipStream_t s) {
+  return rp.area0.members > 1 ? launch_rounds_planned_em<E, true>(a, ra, rp, n_cu, s)
+                              : launch_rounds_planned_em<E, false>(a, ra, rp, n_cu, s);
 }
 
 // ----------------------------------------------------------------------------
 // per-round row descriptors in schedule order
 // ----------------------------------------------------------------------------
+// With members > 1, position q = (v, pos) of slice v = worker * members + m
+// describes the slice's part of the row the worker's schedule puts there
+// (row_ptr then holds the slices' offsets, [n * members * S + 1]).
 __global__ __launch_bounds__(256) void rowinfo_kernel(const int32_t* sched, const int64_t* row_ptr,
                                                       const float* y, int64_t S, int64_t total,
-                                                      RowInfo* out) {
+                                                      int32_t members, RowInfo* out) {
   const int64_t q = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (q >= total) return;
-  const int64_t worker = q / S;
-  const int64_t g = worker * S + sched[q];
+  const int64_t v = q / S, pos = q - v * S, worker = v / members;
+  const int64_t r = sched[worker * S + pos];
+  const int64_t g = v * S + r;
   const int64_t p0 = row_ptr[g], p1 = row_ptr[g + 1];
-  RowInfo r;
-  r.start = p0;
-  r.len = int(p1 - p0);
-  r.y = y[g];
-  out[q] = r;
+  RowInfo ri;
+  ri.start = p0;
+  ri.len = int(p1 - p0);
+  ri.y = y[worker * S + r];
+  out[q] = ri;
+}
+
+// ----------------------------------------------------------------------------
+// bind time, members > 1: the rows of each worker split by member (column
+// c belongs to member c mod members), one thread per row
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void member_count_kernel(const int64_t* row_ptr, const int32_t* col, int64_t rows,
+                                                           int64_t S, int32_t members, int32_t* cnt,
+                                                           int32_t* maxlen) {
+  const int64_t g = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (g >= rows) return;
+  const int64_t i = g / S, r = g - i * S;
+  int c[kMaxMembers] = {0, 0, 0, 0};
+  for (int64_t p = row_ptr[g]; p < row_ptr[g + 1]; ++p) ++c[col[p] % members];
+  int most = 0;
+  for (int m = 0; m < members; ++m) {
+    cnt[(i * members + m) * S + r] = c[m];
+    most = max(most, c[m]);
+  }
+  atomicMax(maxlen, most);
+}
+
+__global__ __launch_bounds__(256) void member_scatter_kernel(const int64_t* row_ptr, const int32_t* col,
+                                                             const float* val, const int16_t* mlut, int64_t rows,
+                                                             int64_t S, int32_t members, const int64_t* vrow_ptr,
+                                                             int32_t* vcode, int2* pack) {
+  const int64_t g = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (g >= rows) return;
+  const int64_t i = g / S, r = g - i * S;
+  int64_t pos[kMaxMembers];
+  for (int m = 0; m < members; ++m) pos[m] = vrow_ptr[(i * members + m) * S + r];
+  for (int64_t p = row_ptr[g]; p < row_ptr[g + 1]; ++p) {
+    const int c = col[p];
+    const int h = mlut[c];
+    const int code = h >= 0 ? -h - 2 : c;
+    const int64_t q = pos[c % members]++;
+    if (vcode) vcode[q] = code;
+    if (pack) pack[q] = make_int2(code, __float_as_int(val[p]));
+  }
 }
 
 // ----------------------------------------------------------------------------
@@ -604,11 +686,30 @@ hipError_t launch_e(const SgdArgs& a, hipStream_t s, bool pipe) {
 }  // namespace
 
 hipError_t launch_rowinfo(const int32_t* sched, const int64_t* row_ptr, const float* y, int32_t n, int64_t S,
-                          RowInfo* out, hipStream_t s) {
-  const int64_t total = int64_t(n) * S;
+                          RowInfo* out, hipStream_t s, int32_t members) {
+  const int64_t total = int64_t(n) * members * S;
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(rowinfo_kernel, dim3(uint32_t((total + 255) / 256)), dim3(256), 0, s, sched, row_ptr, y, S,
-                     total, out);
+                     total, members, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_member_count(const int64_t* row_ptr, const int32_t* col, int32_t n, int64_t S, int32_t members,
+                               int32_t* cnt, int32_t* maxlen, hipStream_t s) {
+  const int64_t rows = int64_t(n) * S;
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(member_count_kernel, dim3(uint32_t((rows + 255) / 256)), dim3(256), 0, s, row_ptr, col, rows, S,
+                     members, cnt, maxlen);
+  return hipGetLastError();
+}
+
+hipError_t launch_member_scatter(const int64_t* row_ptr, const int32_t* col, const float* val, const int16_t* mlut,
+                                 int32_t n, int64_t S, int32_t members, const int64_t* vrow_ptr, int32_t* vcode,
+                                 int2* pack, hipStream_t s) {
+  const int64_t rows = int64_t(n) * S;
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(member_scatter_kernel, dim3(uint32_t((rows + 255) / 256)), dim3(256), 0, s, row_ptr, col, val,
+                     mlut, rows, S, members, vrow_ptr, vcode, pack);
   return hipGetLastError();
 }
 

@@ -296,15 +296,18 @@ __global__ __launch_bounds__(NT) void csr_link_kernel(PlanArgs p) {
 // ----------------------------------------------------------------------------
 // the pass on the plan (csr_fast.h); block n + i prefetches for worker i
 // ----------------------------------------------------------------------------
-template <int E>
+template <int E, bool MEM>
 __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanArgs p) {
   if (*p.flag) return;  // the general kernel takes this round
-  if (int(blockIdx.x) >= a.n) {
+  const int M = MEM ? p.members : 1;
+  if (int(blockIdx.x) >= a.n * M) {
     prefetch_pass<E>(a, p, int(blockIdx.x) - a.n);
     return;
   }
   __shared__ FastShared sh;
-  fast_pass<E>(a, p, int(blockIdx.x), sh);
+  int i, m;
+  member_of(int(blockIdx.x), a.n, M, i, m);
+  fast_pass<E, MEM>(a, p, i, m, sh);
 }
 
 __global__ void pack_values_kernel(const int32_t* __restrict__ code, const float* __restrict__ val, int64_t nnz,
@@ -315,10 +318,20 @@ __global__ void pack_values_kernel(const int32_t* __restrict__ code, const float
 
 template <int E>
 hipError_t launch_fast_e(const SgdArgs& a, const PlanArgs& p, hipStream_t s) {
+  if (p.members > 1) {
+    // members wait for each other every step: cooperative, so that all are
+    // resident at once
+    const uint32_t grid = uint32_t(a.n) * uint32_t(p.members);
+    SgdArgs aa = a;
+    PlanArgs pp = p;
+    void* args[] = {&aa, &pp};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&sgd_csr_fast_kernel<E, true>), dim3(grid),
+                                      dim3(kThreads), args, 0, s);
+  }
   // with helpers, block n + i prefetches for block i: the same XCD when n is
   // a multiple of the 8 XCDs (blocks are dealt to them round-robin)
   const uint32_t grid = uint32_t(a.n) * (p.helpers ? 2u : 1u);
-  hipLaunchKernelGGL((sgd_csr_fast_kernel<E>), dim3(grid), dim3(kThreads), 0, s, a, p);
+  hipLaunchKernelGGL((sgd_csr_fast_kernel<E, false>), dim3(grid), dim3(kThreads), 0, s, a, p);
   return hipGetLastError();
 }
 
@@ -372,6 +385,7 @@ hipError_t launch_sgd_csr_fast(const SgdArgs& a, const PlanArgs& p, hipStream_t 
   if (a.max_row <= kRowLanes * 2) return launch_fast_e<2>(a, p, s);
   if (a.max_row <= kRowLanes * 3) return launch_fast_e<3>(a, p, s);
   if (a.max_row <= kRowLanes * 4) return launch_fast_e<4>(a, p, s);
+  if (a.max_row <= kRowLanes * 5) return launch_fast_e<5>(a, p, s);
   if (a.max_row <= kRowLanes * 6) return launch_fast_e<6>(a, p, s);
   return launch_fast_e<8>(a, p, s);
 }

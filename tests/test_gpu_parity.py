@@ -116,10 +116,11 @@ def test_schedule_device_matches_oracle(torch, n, S, rnd):
 # free-running rounds: both sides start from the same seeded models and run
 # independently; models are compared after every round
 # ----------------------------------------------------------------------------
-def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False, local_steps=0, data=None, gr=None):
+def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False, local_steps=0, data=None, gr=None, members=0):
     """`rounds` rounds on the GPU and in the oracle from the same seeded start,
     compared after every round.  `data` (CSR arrays) and `gr` (graph) replace
-    the workload's own.  A round in which the oracle finds hinge decisions
+    the workload's own; `members` sets the workgroups per worker of the
+    planned CSR pass (0: the library's choice).  A round in which the oracle finds hinge decisions
     within rounding of the kink is compared outside the entries they can
     change (`ambiguity_mask`), and the comparison ends there: from then on
     the two runs may legitimately differ.  Round 0 is always compared."""
@@ -138,6 +139,8 @@ def _free_run(torch, wl, kind, d, rounds, W0=None, loss_curve=False, local_steps
         sess.bind_dense(X, y)
     else:
         sess.bind_csr(rp, col, val, yy, wl.samples)
+        if members:
+            sess.set_csr_members(members)
     prm = params(wl, local_steps)
     K = oracle.sgd.n_steps(wl.samples, wl.batch)
     for r in range(rounds):
@@ -237,6 +240,31 @@ def test_csr_logistic_ragged_batches(torch):
 def test_csr_hinge_l2_scale_form(torch):
     wl = synth.SPARSE_SVM_256W.with_(n_workers=32, dim=1 << 12, samples=700, l2=1e-3)
     _free_run(torch, wl, "random", 8, 4, loss_curve=True)
+
+
+# The planned CSR pass with 1, 2 and 4 workgroups per worker: member m owns
+# the columns c mod members == m, and the members exchange their partial
+# margins once per step (Appendix A, update (A.2), first line).
+@pytest.mark.parametrize("members", [1, 2, 4])
+@pytest.mark.parametrize("case", ["logistic_ragged", "hinge_l2"])
+def test_csr_members_against_the_oracle(torch, case, members):
+    if case == "logistic_ragged":
+        wl = synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=1000)  # 15 steps of 64 + one of 40
+        _free_run(torch, wl, "random", 4, 3, loss_curve=True, members=members)
+    else:
+        wl = synth.SPARSE_SVM_256W.with_(n_workers=16, dim=1 << 12, samples=700, l2=1e-3)
+        _free_run(torch, wl, "random", 8, 3, loss_curve=True, members=members)
+
+
+@pytest.mark.parametrize("members", [1, 4])
+def test_csr_l2_scale_fold(torch, members):
+    # strong L2 with a constant step: the pass's scale s = prod (1 - eta l2)
+    # drops below 1e-6 after 48 steps of a pass and is folded back into the model (each
+    # member folds its own columns)
+    wl = synth.SPARSE_SVM_256W.with_(n_workers=8, dim=1 << 12, samples=704, batch=8, l2=0.5, lr_kind="const",
+                                   lr0=0.5)  # 88 steps per pass
+    W0 = synth.initial_models(wl.with_(seed=5))
+    _free_run(torch, wl, "random", 4, 3, W0=W0, members=members)
 
 
 def test_csr_hinge_complete_graph(torch):

@@ -31,7 +31,7 @@ def _announce(request):
     yield
 
 
-def _session(wl, kind, d, W0=None):
+def _session(wl, kind, d, W0=None, members=0):
     p, i, w = graph(kind, wl.n_workers, d)
     sess = asap.Session(wl.n_workers, wl.dim, p, i, w)
     if W0 is not None:
@@ -42,6 +42,8 @@ def _session(wl, kind, d, W0=None):
     else:
         rp, col, val, yy = synth.csr_data(wl)
         sess.bind_csr(rp, col, val, yy, wl.samples)
+        if members:
+            sess.set_csr_members(members)
     return sess, (p, i, w)
 
 
@@ -78,8 +80,11 @@ CASES = {
 def test_run_rounds_is_bitwise_the_stream_path(torch, case):
     wl, kind, d, R, L = CASES[case]
     prm = params(wl, L)
-    a, _ = _session(wl, kind, d)
-    b, _ = _session(wl, kind, d)
+    # rows of ~200 nonzeros: one member per worker keeps them on the general
+    # kernel (a member's share of them would fit the planned pass)
+    members = 1 if case == "csr_long_rows_ring" else 0
+    a, _ = _session(wl, kind, d, members=members)
+    b, _ = _session(wl, kind, d, members=members)
     for _ in range(R):
         a.round(prm)
     b.run_rounds(prm, R, wait_ms=3000)
@@ -228,23 +233,31 @@ def test_run_rounds_edge_cases_match_the_stream_path(torch, case):
 # (or, where a step overflows the plan, the same general code), so the bits
 # must be equal.  Small worker counts plan beside the launch on the library's
 # look-ahead stream; 128 workers with their prefetch workgroups fill the
-# device, so their plans are made before the launch.
+# device, so their plans are made before the launch.  The last field sets the
+# workgroups per worker of the planned pass (0: the library's choice: 4 up
+# to 32 workers, 2 up to 64, else 1); members of a worker exchange partial
+# margins every step and publish the half-step only when all have finished.
 PLANNED = {
-    "c2_shape": (synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=512), "random", 4, 3, 0),
-    "c3_shape_128w": (synth.SPARSE_SVM_256W.with_(n_workers=128, dim=1 << 13, samples=256), "random", 8, 3, 0),
-    "local_steps": (synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=512, batch=64), "chain", 0, 7, 2),
+    "c2_shape": (synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=512), "random", 4, 3, 0, 0),
+    "c2_shape_64w": (synth.SPARSE_LR_64W.with_(n_workers=64, dim=1 << 14, samples=256), "random", 4, 3, 0, 0),
+    "c2_shape_one_member": (synth.SPARSE_LR_64W.with_(n_workers=16, dim=1 << 14, samples=512), "random", 4, 3, 0, 1),
+    "c3_shape_128w": (synth.SPARSE_SVM_256W.with_(n_workers=128, dim=1 << 13, samples=256), "random", 8, 3, 0, 0),
+    "hinge_l2_2_members": (synth.SPARSE_SVM_256W.with_(n_workers=32, dim=1 << 13, samples=256, l2=1e-3), "random",
+                           8, 3, 0, 2),
+    "local_steps": (synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=512, batch=64), "chain", 0, 7, 2, 0),
     # ~3800 distinct rarely used columns per step: every plan overflows and
     # every pass runs the general code, on both paths
-    "overflow": (synth.SPARSE_LR_64W.with_(n_workers=4, samples=256, nnz_mean=60.0, zipf_s=0.3), "ring", 2, 2, 0),
+    "overflow": (synth.SPARSE_LR_64W.with_(n_workers=4, samples=256, nnz_mean=60.0, zipf_s=0.3), "ring", 2, 2, 0,
+                 0),
 }
 
 
 @pytest.mark.parametrize("case", list(PLANNED))
 def test_run_rounds_planned_pass_is_bitwise_the_stream_path(torch, case):
-    wl, kind, d, R, L = PLANNED[case]
+    wl, kind, d, R, L, members = PLANNED[case]
     prm = params(wl, L)
-    a, _ = _session(wl, kind, d)
-    b, _ = _session(wl, kind, d)
+    a, _ = _session(wl, kind, d, members=members)
+    b, _ = _session(wl, kind, d, members=members)
     for _ in range(R):
         a.round(prm)
     K = -(-wl.samples // wl.batch)

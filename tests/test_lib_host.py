@@ -173,6 +173,31 @@ def test_state_errors_before_device_work():
         asap.asap_destroy(ctx)
 
 
+def test_csr_members_setting():
+    p, i, w = _ring()
+    ctx = asap.asap_create(8, 100, p, i, w)
+    try:
+        fake = 1 << 40
+        asap.asap_bind_models(ctx, fake, fake + (1 << 20), 128, stream=0)
+        asap.asap_bind_csr(ctx, fake, fake, fake, fake, 1000, 5000, stream=0)
+        for bad in (-1, 3, 5, 8):
+            with pytest.raises(asap.AsapError) as e:
+                asap.asap_set_csr_members(ctx, bad)
+            assert e.value.status == asap.E_INVALID_ARG
+        sizes = {}
+        for m in (1, 2, 4):
+            asap.asap_set_csr_members(ctx, m)
+            sizes[m] = asap.asap_workspace_size(ctx)
+        # the members' slice offsets, codes, row descriptors and exchange words
+        assert sizes[1] < sizes[2] < sizes[4]
+        assert sizes[4] - sizes[1] >= 8 * 8 * 1000 * 4 + 5000 * 4
+        asap.asap_set_csr_members(ctx, 0)
+        assert asap.asap_workspace_size(ctx) == sizes[4]   # 8 workers: four members each
+        assert asap.asap_get_csr_members(ctx) == 4
+    finally:
+        asap.asap_destroy(ctx)
+
+
 def test_dense_dim_limit():
     p, i, w = _ring()
     ctx = asap.asap_create(8, 20000, p, i, w)
