@@ -93,7 +93,8 @@ struct asap_ctx {
   size_t off_ptr = 0, off_idx = 0, off_w = 0, off_optr = 0, off_oidx = 0, off_tag = 0, off_scale = 0, off_err = 0,
          off_vmax = 0, off_scan = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
          off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dxcd = 0, off_dcount = 0, off_progress = 0,
-         off_vrp = 0, off_vcode = 0, off_mlut = 0, off_mhot = 0, off_xch = 0, off_done = 0, total = 0;
+         off_vrp = 0, off_vcode = 0, off_mlut = 0, off_mhot = 0, off_xch = 0, off_done = 0, off_xid = 0,
+         total = 0;
   RoundPlan plan[2];
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
@@ -211,6 +212,7 @@ void layout(asap_ctx* c) {
   c->off_mhot = o;  o = align_up(o + split * M * kHotMax * 4);
   c->off_xch = o;   o = align_up(o + split * 2 * n * M * 128 * 8);
   c->off_done = o;  o = align_up(o + split * n * M * 8);
+  c->off_xid = o;   o = align_up(o + split * n * M * 8);
   // per-round buffers of the CSR pass, twice: one entry per nonzero per list
   const size_t nz = csr ? size_t(c->nnz) : 0, nS = csr ? n * size_t(c->S) : 0;
   for (int k = 0; k < 2; ++k) {
@@ -871,10 +873,13 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
     // per plan slot (planning rewrites the cold entries' codes)
     for (int k = 0; k < 2; ++k)
       if ((e = write_pack(c, at<int2>(c, c->plan[k].pack), s))) return hip_fail(c, e, "plan values");
-    if (c->members > 1 &&
-        (e = launch_fill_i64(at<int64_t>(c, c->off_xch), 2 * int64_t(n) * c->members * 128, 0, s)) ||
-        (c->members > 1 && (e = launch_fill_i64(at<int64_t>(c, c->off_done), int64_t(n) * c->members, 0, s))))
-      return hip_fail(c, e, "member exchange init");
+    if (c->members > 1) {
+      const int64_t nm = int64_t(n) * c->members;
+      if ((e = launch_fill_i64(at<int64_t>(c, c->off_xch), 2 * nm * 128, 0, s)) ||
+          (e = launch_fill_i64(at<int64_t>(c, c->off_done), nm, 0, s)) ||
+          (e = launch_fill_i64(at<int64_t>(c, c->off_xid), nm, 0, s)))
+        return hip_fail(c, e, "member exchange init");
+    }
     if (!c->ahead) {
       if ((e = hipStreamCreateWithFlags(&c->ahead, hipStreamNonBlocking))) {
         c->ahead = nullptr;
@@ -981,6 +986,7 @@ PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp, c
   for (int m = 0; m < kMaxMembers; ++m) pa.n_mhot[m] = m < c->members ? c->n_mhot[m] : 0;
   pa.xch = split ? ::at<unsigned long long>(c, c->off_xch) : nullptr;
   pa.done = split ? ::at<unsigned long long>(c, c->off_done) : nullptr;
+  pa.xid = split ? ::at<unsigned long long>(c, c->off_xid) : nullptr;
   pa.xerr = ::at<int32_t>(c, c->off_err) + kErrRendezvous;
   pa.xwait = kMemberWaitMs * c->clock_khz;
   pa.S = c->S;

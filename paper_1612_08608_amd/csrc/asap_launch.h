@@ -12,6 +12,13 @@ namespace asap {
 __host__ __device__ inline int64_t tag_start(int64_t r) { return 2 * r; }
 __host__ __device__ inline int64_t tag_half(int64_t r) { return 2 * r + 1; }
 
+// The XCD (accelerator complex die) the calling wave runs on: hardware
+// register XCC_ID, bits [3:0].  Workgroups of a launch are dealt to the
+// XCDs round-robin.
+__device__ __forceinline__ int xcd_id() {
+  return int(__builtin_amdgcn_s_getreg(20 | (0 << 6) | ((16 - 1) << 11)) & 0xfu);
+}
+
 // Device error words (int32 each).
 enum { kErrEpochCount = 0, kErrEpochWorker = 1, kErrRendezvous = 2, kErrWords = 16 };
 
@@ -118,8 +125,9 @@ struct PlanArgs {
   int32_t workers;          // real workers
   const int32_t* mhot;      // [members][kHotMax] column of each member's hot slot
   int32_t n_mhot[4];        // hot slots of each member
-  unsigned long long* xch;  // [2][workers][members][64][2] tagged halves of partial margins
+  unsigned long long* xch;  // [workers][2][members][64][2] tagged halves of partial margins (step parity 2nd)
   unsigned long long* done; // [workers][members] multi-round launch: tag of a member's last step
+  unsigned long long* xid;  // [workers][members] (tag of a pass's first step, XCD) of each member
   int32_t* xerr;            // error word: a member waited too long for a partner
   long long xwait;          // wall-clock ticks a member waits for a partner
 };

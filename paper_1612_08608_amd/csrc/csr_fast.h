@@ -29,6 +29,7 @@ struct FastShared {
   float cval[2][kCMax];  // cold values of steps k (slot k & 1) and k - 1
   unsigned long long cacc[kCMax];
   int xabort;            // members: a partner's partial margin did not arrive in time
+  int xlocal;            // members: all of this worker's members run on this XCD
 };
 static_assert(sizeof(FastShared) <= 160 * 1024, "LDS budget of one workgroup");
 
@@ -188,34 +189,48 @@ __device__ void prefetch_pass(const SgdArgs& a, const PlanArgs& p, int i) {
 // Lanes 0, 1 of each 16-lane row publish; lanes 2 m', 2 m' + 1 read member
 // m''s halves (a bounded wait), and every lane of the row adds the members'
 // partials in member order, so all members get the same margin bit for bit.
-__device__ __forceinline__ double member_exchange(const PlanArgs& p, int i, int m, int brow, int lane, uint32_t tag,
-                                                  double part, bool live, FastShared& sh) {
+// Reads are device-scope (a narrower load may be served by a stale line of
+// the reader's L1).  Members on one XCD write with plain stores, which the
+// L1 writes through to the XCD's shared L2 where the readers find them;
+// members on several XCDs write device-scope, past the L2.
+__device__ __forceinline__ double member_exchange(const PlanArgs& p, __amdgpu_buffer_rsrc_t xr, int m, int brow,
+                                                  int lane, uint32_t tag, double part, bool live, bool local,
+                                                  FastShared& sh) {
+  typedef unsigned int v2u __attribute__((ext_vector_type(2)));
   const int M = p.members, sub = lane & (kRowLanes - 1), mm = sub >> 1;
-  unsigned long long* slot = p.xch + ((size_t(tag & 1u) * size_t(p.workers) + size_t(i)) * size_t(M)) * 128u;
+  const uint32_t slot = (tag & 1u) * uint32_t(M) * 128u;  // words
   const uint32_t lo = uint32_t(__double2loint(part)), hi = uint32_t(__double2hiint(part));
-  if (live && sub < 2)
-    __hip_atomic_store(slot + (m * 64 + brow) * 2 + sub,
-                       (static_cast<unsigned long long>(tag) << 32) | (sub ? hi : lo), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
+  if (live && sub < 2) {
+    const v2u word = {sub ? hi : lo, tag};
+    const uint32_t off = (slot + uint32_t((m * 64 + brow) * 2 + sub)) * 8u;
+    if (local)
+      __builtin_amdgcn_raw_buffer_store_b64(word, xr, off, 0, 0);
+    else
+      __builtin_amdgcn_raw_buffer_store_b64(word, xr, off, 0, 16);  // sc1: device scope
+  }
   uint32_t half = 0;
   if (live && mm < M) {
     if (mm == m) {
       half = (sub & 1) ? hi : lo;
     } else {
-      const unsigned long long* src = slot + (mm * 64 + brow) * 2 + (sub & 1);
-      unsigned long long w = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (uint32_t(w >> 32) != tag) {
+      const uint32_t off = (slot + uint32_t((mm * 64 + brow) * 2 + (sub & 1))) * 8u;
+      auto load = [&]() {
+        asm volatile("" ::: "memory");  // a fresh load every poll
+        return __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 16);  // sc1: device scope
+      };
+      v2u w = load();
+      if (uint32_t(w[1]) != tag) {
         const long long deadline = wall_clock64() + p.xwait;
         do {
           __builtin_amdgcn_s_sleep(1);
-          w = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        } while (uint32_t(w >> 32) != tag && wall_clock64() < deadline);
-        if (uint32_t(w >> 32) != tag) {
+          w = load();
+        } while (uint32_t(w[1]) != tag && wall_clock64() < deadline);
+        if (uint32_t(w[1]) != tag) {
           sh.xabort = 1;
           atomicAdd(p.xerr, 1);
         }
       }
-      half = uint32_t(w);
+      half = uint32_t(w[0]);
     }
   }
   const int base = lane & ~(kRowLanes - 1);
@@ -255,13 +270,43 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
   const auto hlist = rsrc(p.hlist + w.seg, nnz_w * 4u);
   const auto so_v = rsrc(p.step_off + int64_t(v) * (a.S + 1), uint32_t(a.k1) * 4u);  // steps past the launch read 0
   const auto cn_v = rsrc(p.cnt + int64_t(v) * K * 2, uint32_t(a.k1) * 8u);
+  // members: this worker's exchange words, [2][M][64][2] (unused with one member)
+  const auto xr = rsrc(MEM ? p.xch + size_t(i) * size_t(M) * 256u : nullptr, MEM ? uint32_t(M) * 2048u : 0u);
 
   for (int h = tid; h < H; h += kThreads) {
     sh.vhot[h] = vrow[hot_cols[h]];
     sh.acch[h] = 0ull;
   }
   for (int q = tid; q < kCMax; q += kThreads) sh.cacc[q] = 0ull;
-  if (tid == 0) sh.xabort = 0;
+  bool local = false;
+  if (tid == 0) {
+    sh.xabort = 0;
+    sh.xlocal = 0;
+    if constexpr (MEM) {
+      // the members publish their XCD, tagged with the pass's first step,
+      // and see whether all of them share one
+      const uint32_t tag0 = a.xtag + uint32_t(a.round * K + k0 - a.xg0);
+      const uint32_t me = uint32_t(xcd_id());
+      unsigned long long* xid = p.xid + size_t(i) * size_t(M);
+      __hip_atomic_store(xid + m, (static_cast<unsigned long long>(tag0) << 32) | me, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      const long long deadline = wall_clock64() + p.xwait;
+      int same = 1;
+      for (int q = 0; q < M; ++q) {
+        unsigned long long w;
+        while (uint32_t((w = __hip_atomic_load(xid + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) >> 32) != tag0) {
+          if (wall_clock64() > deadline) break;
+          __builtin_amdgcn_s_sleep(2);
+        }
+        if (uint32_t(w >> 32) != tag0) {
+          sh.xabort = 1;
+          atomicAdd(p.xerr, 1);
+        }
+        same &= uint32_t(w) == me;
+      }
+      sh.xlocal = same;
+    }
+  }
   // fixed point as in the general kernel: |column sum| <= B vmax < 2^e
   int e2 = 0;
   frexp(double(a.batch) * double(a.vmax[i]), &e2);
@@ -325,6 +370,7 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
     m1 = uniform(m1);
     m2 = uniform(m2);
     __syncthreads();
+    local = sh.xlocal != 0;
     load_packed<E>(pk, w.seg, ra, row_valid(a, k0, kend, brow), sub, d0);
     load_cols(m0, cl0);
     load_links(m0, lk0);
@@ -399,8 +445,8 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
     for (int j = 0; j < E; ++j) part = fma(double(d0.val[j]), double(code_at(d0, j) == -1 ? 0.f : v[j]), part);
     double dot = row16_sum(part);
     if constexpr (MEM)
-      dot = member_exchange(p, i, m, brow, lane, a.xtag + uint32_t(a.round * K + k - a.xg0), dot,
-                            row_valid(a, k, kend, brow), sh);
+      dot = member_exchange(p, xr, m, brow, lane, a.xtag + uint32_t(a.round * K + k - a.xg0), dot,
+                            row_valid(a, k, kend, brow), local, sh);
     const double cf = (d0.ok & kRowExists) ? loss_coef(s * dot, double(d0.y), a.loss) : 0.0;
     if (cf != 0.0) {
 #pragma unroll

@@ -12,10 +12,12 @@
 // member order, so every member gets the same sum whatever the order they
 // arrive in.  Members of a worker are placed on one XCD when the grid
 // allows (workgroups are dealt to the XCDs round-robin; each member checks
-// the XCD it runs on), and then meet in that XCD's L2: 16-byte stores and
-// loads that only bypass the CU's L1.  Device-scope accesses, which go past
-// the L2, made the exchange cost a third of the pass; integer atomics on
-// shared lines and a reduce-scatter with a second meeting were slower still.
+// the XCD it runs on), and then meet in that XCD's L2: plain 16-byte stores
+// (the CU's L1 writes through to the L2) and device-scope loads (a load of
+// narrower scope may be served by a line the reader's L1 kept from two
+// steps earlier).  Device-scope stores, which go past the L2, made the
+// exchange cost a third of the pass; integer atomics on shared lines and a
+// reduce-scatter with a second meeting were slower still.
 // The launch is cooperative, so every member is resident and the rendezvous
 // cannot wait on a workgroup that has not started; the wait is bounded
 // anyway and reports a timeout instead of spinning for ever.
@@ -101,11 +103,6 @@ __device__ __forceinline__ double row_reduce(double (&d)[16], int lane) {
   return d[0];
 }
 
-// The XCD (accelerator complex die) this wave runs on: hardware register
-// XCC_ID, bits [3:0].  Workgroups are dealt to the XCDs round-robin.
-__device__ __forceinline__ int xcd_id() {
-  return int(__builtin_amdgcn_s_getreg(20 | (0 << 6) | ((16 - 1) << 11)) & 0xfu);
-}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
@@ -375,9 +372,9 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
     if (K > 1) {
       if (!gather(ds.base + uint32_t(K) * uint32_t(t - K0 + 2))) return false;
       // ... and every member sums all K partials in fp64 in member order,
-      // so all members get the same gradient bit for bit.  Members on one
-      // XCD meet in its L2 (loads that bypass only the CU's L1); otherwise
-      // the accesses are device-scope.
+      // so all members get the same gradient bit for bit.  The loads are
+      // device-scope: they never hit a stale line of this CU's L1 (members
+      // on one XCD find the partials in its L2, the others in memory).
 #pragma unroll
       for (int q = 0; q < CPQ; ++q)
 #pragma unroll
@@ -386,8 +383,7 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
 #pragma unroll
         for (int q = 0; q < CPQ; ++q) {
           const uint32_t off = uint32_t((m * ds.ldp + (q * kThreads + tid) * 4) * 4);
-          const auto u = local ? __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, 1)    // sc0: past the L1
-                               : __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, 16);  // sc1: device scope
+          const auto u = __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, 16);  // sc1: device scope
           const unsigned u0 = u[0], u1 = u[1], u2 = u[2], u3 = u[3];
           g[q][0] += double(__uint_as_float(u0));
           g[q][1] += double(__uint_as_float(u1));
