@@ -145,8 +145,9 @@ __global__ __launch_bounds__(kScanThreads) void step_scan_kernel(PlanArgs p) {
 // ----------------------------------------------------------------------------
 // plan of one (worker, step): distinct columns, slots, per-nonzero codes
 // ----------------------------------------------------------------------------
-// TB: table positions 2^TB >= 2 * (the step's nonzeros), LDS sized to
-// match; NT threads; H nonzeros per lane and row (rows of at most 64 H).
+// TB: LDS for 2^TB table positions; a step uses the smallest power of two
+// >= 2 * (its nonzeros), at most 2^TB.  NT threads; H nonzeros per lane and
+// row (rows of at most 64 H).
 template <int TB, int NT, int H>
 __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
   constexpr int NW = NT / 64;
@@ -344,8 +345,13 @@ bool csr_plan_fits(const SgdArgs& a) {
 hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   const uint32_t blocks = uint32_t(int64_t(p.n) * p.K);
   hipLaunchKernelGGL(step_scan_kernel, dim3(uint32_t(p.n)), dim3(kScanThreads), 0, s, p);
-  // the largest step holds at most batch * max_row nonzeros
-  const int64_t most = 2 * int64_t(std::min(p.batch, kFastRows)) * max_row;
+  // the largest step holds at most batch * max_row nonzeros; the table
+  // holds its distinct cold columns, of which a plan that the pass can take
+  // has at most kCMax, so 2 kCMax positions (TB = 12) always suffice (a
+  // fuller table overflows into the general kernel, as does a step over
+  // kCMax).  Smaller tables keep more blocks resident.
+  static_assert((1 << 12) >= 2 * kCMax, "a 2^12-position table holds twice the cold slots");
+  const int64_t most = std::min<int64_t>(2 * int64_t(std::min(p.batch, kFastRows)) * max_row, 2 * kCMax);
   // rows of at most 64 nonzeros: one per lane and 256 threads (a small
   // step leaves most of a larger block idle); else two and 512
   if (max_row <= 64) {
@@ -353,19 +359,15 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
       hipLaunchKernelGGL((csr_plan_kernel<10, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
     else if (most <= (1 << 11))
       hipLaunchKernelGGL((csr_plan_kernel<11, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
-    else if (most <= (1 << 12))
-      hipLaunchKernelGGL((csr_plan_kernel<12, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
     else
-      hipLaunchKernelGGL((csr_plan_kernel<13, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
+      hipLaunchKernelGGL((csr_plan_kernel<12, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
   } else {
     if (most <= (1 << 10))
       hipLaunchKernelGGL((csr_plan_kernel<10, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
     else if (most <= (1 << 11))
       hipLaunchKernelGGL((csr_plan_kernel<11, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
-    else if (most <= (1 << 12))
-      hipLaunchKernelGGL((csr_plan_kernel<12, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
     else
-      hipLaunchKernelGGL((csr_plan_kernel<13, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
+      hipLaunchKernelGGL((csr_plan_kernel<12, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
   }
   if (max_row <= 64)
     hipLaunchKernelGGL(csr_link_kernel<256>, dim3(blocks), dim3(256), 0, s, p);
