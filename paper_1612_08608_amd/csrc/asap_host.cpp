@@ -203,7 +203,7 @@ void layout(asap_ctx* c) {
   c->off_code = o;    o = align_up(o + (csr ? size_t(c->nnz) * 4 : 0));
   c->off_lut = o;     o = align_up(o + (csr ? size_t(c->dim) * 2 : 0));
   c->off_hot = o;     o = align_up(o + (csr ? size_t(kHotMax) * 4 : 0));
-  c->off_progress = o; o = align_up(o + (csr ? n * 8 : 0));
+  c->off_progress = o; o = align_up(o + (csr ? n * kMaxMembers * 8 : 0));  // one word per slice
   c->members = csr ? csr_members(c) : 1;
   const size_t M = size_t(c->members), split = csr && M > 1 ? 1 : 0;
   c->off_vrp = o;   o = align_up(o + split * (n * M * size_t(c->S) + 1) * 8);
@@ -824,7 +824,7 @@ extern "C" asap_status asap_bind_workspace(asap_ctx* c, void* dev, size_t bytes,
       (e = launch_fill_i32(at<int32_t>(c, c->off_err), 1, 0, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err) + 1, 1, INT_MAX, s)) ||
       (e = launch_fill_i32(at<int32_t>(c, c->off_err) + kErrRendezvous, 1, 0, s)) ||
-      (c->kind == kCsr && (e = launch_fill_i64(at<int64_t>(c, c->off_progress), int64_t(n), -1, s))))
+      (c->kind == kCsr && (e = launch_fill_i64(at<int64_t>(c, c->off_progress), int64_t(n) * kMaxMembers, -1, s))))
     return hip_fail(c, e, "workspace init");
   if (c->kind == kDense && dense_wide_cpq(c->dim)) {
     // max |x| per shard (the fixed-point scale of the member exchange),
@@ -1001,9 +1001,13 @@ PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp, c
   pa.cnt = reinterpret_cast<int32_t*>(at(rp.cnt));
   pa.flag = reinterpret_cast<int32_t*>(at(rp.flag));
   pa.progress = ::at<int64_t>(c, c->off_progress);
-  // a prefetch workgroup per worker when both fit beside each other and
-  // worker i's pair lands on one XCD (one member per worker only)
-  pa.helpers = (!split && c->n % 8 == 0 && 2 * c->n <= c->n_cu) ? 1 : 0;
+  // a prefetch workgroup per slice when each pair lands on one XCD and the
+  // pairs fit on the device; with several members only while they leave half
+  // of it to the next round's planning (64 workers x 2 members with helpers:
+  // pass 2.30 -> 1.92 ms, but the planning then waited for the pass and the
+  // round took 2.9 instead of 2.4 ms)
+  const int64_t pairs = 2 * int64_t(c->n) * c->members;
+  pa.helpers = (c->n % 8 == 0 && pairs <= (split ? c->n_cu / 2 : c->n_cu)) ? 1 : 0;
   return pa;
 }
 
@@ -1329,7 +1333,7 @@ extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, in
       rp.npass = npass;
       rp.ready = reinterpret_cast<const int64_t*>(c->ring);
       rp.token0 = (++c->ring_epoch) << 24;
-      const int64_t blocks = int64_t(c->n) * c->members + (rp.area0.helpers ? c->n : 0);
+      const int64_t blocks = int64_t(c->n) * c->members * (rp.area0.helpers ? 2 : 1);
       const bool beside = c->ahead && blocks + 64 <= c->n_cu;
       hipStream_t ps = beside ? c->ahead : s;
       if (beside) e = hipStreamWaitEvent(ps, c->ev_ring_free, 0);

@@ -124,34 +124,35 @@ __device__ __forceinline__ void member_of(int b, int n, int M, int& i, int& m) {
 constexpr uint32_t kPrefetchSpin = 1u << 16;  // polls of the pass's progress per step (bounded)
 constexpr int kPrefetchLead = 3;              // steps ahead of the pass
 
-// Prefetch workgroup of worker i (on the pass's XCD): what step k of the
-// pass reads -- its rows' (code, value) pairs, its lists and the model
-// entries of its cold columns -- is loaded into the XCD's L2 while the pass
-// is at step k - 2, one step before the pass loads it itself.  A random
+// Prefetch workgroup of slice v of worker i (on the XCD of the slice's
+// pass): what step k of the pass reads -- its rows' (code, value) pairs, its
+// lists and the model entries of its cold columns -- is loaded into the
+// XCD's L2 while the pass is at step k - 2, one step before the pass loads
+// it itself.  A random
 // 4-byte model read costs a whole line from memory, and one compute unit
 // only has so many in flight: the pass's step time was bound by them.  This
 // workgroup only loads (the values are discarded) and waits for the pass
 // with a bounded spin, so it cannot change any result.
 template <int E>
-__device__ void prefetch_pass(const SgdArgs& a, const PlanArgs& p, int i) {
+__device__ void prefetch_pass(const SgdArgs& a, const PlanArgs& p, int v, int i) {
   const int tid = threadIdx.x, sub = tid & (kRowLanes - 1), b = tid / kRowLanes;
   const int64_t K = (a.S + a.batch - 1) / a.batch;
-  const RowInfo* ri = p.rowinfo + int64_t(i) * a.S;
-  const long long seg = p.row_ptr[int64_t(i) * a.S];
-  const uint32_t nnz_w = uint32_t(p.row_ptr[int64_t(i + 1) * a.S] - seg);
+  const RowInfo* ri = p.rowinfo + int64_t(v) * a.S;
+  const long long seg = p.row_ptr[int64_t(v) * a.S];
+  const uint32_t nnz_w = uint32_t(p.row_ptr[int64_t(v + 1) * a.S] - seg);
   const auto pk = rsrc(p.pack + seg, nnz_w * 8u);
   const auto model = rsrc(a.models + int64_t(i) * a.ld, uint32_t(a.dim) * 4u);
   const auto clist = rsrc(p.clist + seg, nnz_w * 4u);
   const auto clink = rsrc(p.clink + seg, nnz_w * 4u);
   const auto hlist = rsrc(p.hlist + seg, nnz_w * 4u);
-  const auto so_v = rsrc(p.step_off + int64_t(i) * (a.S + 1), uint32_t(a.k1) * 4u);
-  const auto cn_v = rsrc(p.cnt + int64_t(i) * K * 2, uint32_t(a.k1) * 8u);
+  const auto so_v = rsrc(p.step_off + int64_t(v) * (a.S + 1), uint32_t(a.k1) * 4u);
+  const auto cn_v = rsrc(p.cnt + int64_t(v) * K * 2, uint32_t(a.k1) * 8u);
   const int64_t base = a.round * K;
   float sink = 0.f;
   for (int64_t k = a.k0 + 2; k < a.k1; ++k) {
     if (tid == 0) {
       uint32_t spins = 0;
-      while (__hip_atomic_load(p.progress + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < base + k - kPrefetchLead &&
+      while (__hip_atomic_load(p.progress + v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < base + k - kPrefetchLead &&
              ++spins < kPrefetchSpin)
         __builtin_amdgcn_s_sleep(4);
     }
@@ -383,7 +384,7 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
 
   for (int64_t k = k0; k < kend; ++k) {
     if (p.helpers && tid == 0)
-      __hip_atomic_store(p.progress + i, a.round * K + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.progress + v, a.round * K + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (k > k0) {  // rotate what the previous step loaded
       d0 = d1;
       r1 = r2;
@@ -535,7 +536,7 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
       if (a.tag) a.tag[i] = a.tag_value;
     }
     if (p.helpers)
-      __hip_atomic_store(p.progress + i, a.round * K + kend, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.progress + v, a.round * K + kend, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 

@@ -468,9 +468,10 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
   const int64_t K = (a.S + a.batch - 1) / a.batch;
   const int M = MEM ? rp.area0.members : 1;
   if (int(blockIdx.x) >= ra.n * M) {
-    // prefetch workgroup (one member per worker): the steps of each pass
-    // that this launch runs
-    const int i = int(blockIdx.x) - ra.n;
+    // prefetch workgroup of the slice of block blockIdx.x - n M: the steps
+    // of each pass that this launch runs
+    int i, m;
+    member_of(int(blockIdx.x) - ra.n * M, ra.n, M, i, m);
     for (int64_t u = 0; u < rp.npass; ++u) {
       if (threadIdx.x == 0) plan_ok = wait_plan(rp, u, wall_clock64() + ra.wait_ticks);
       __syncthreads();
@@ -492,7 +493,7 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
       ah.k1 = pass == q1 ? j1 : K;
       ah.rowinfo = p.rowinfo;
       ah.models = ra.buf[ra.cur ^ int((rfirst - ra.r0) & 1)];
-      prefetch_pass<E>(ah, p, i);
+      prefetch_pass<E>(ah, p, i * M + m, i);
       __syncthreads();
     }
     return;
@@ -577,7 +578,7 @@ hipError_t launch_rounds_planned_em(const SgdArgs& a, const RoundsArgs& ra, cons
   int per = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_csr_planned_kernel<E, MEM>, kThreads, 0);
   if (e != hipSuccess) return e;
-  const int64_t grid = int64_t(a.n) * rp.area0.members + (rp.area0.helpers ? a.n : 0);
+  const int64_t grid = int64_t(a.n) * rp.area0.members * (rp.area0.helpers ? 2 : 1);
   if (int64_t(per) * n_cu < grid) return hipErrorCooperativeLaunchTooLarge;
   SgdArgs aa = a;
   RoundsArgs rr = ra;

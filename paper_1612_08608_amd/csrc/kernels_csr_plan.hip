@@ -301,12 +301,15 @@ template <int E, bool MEM>
 __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanArgs p) {
   if (*p.flag) return;  // the general kernel takes this round
   const int M = MEM ? p.members : 1;
+  int i, m;
   if (int(blockIdx.x) >= a.n * M) {
-    prefetch_pass<E>(a, p, int(blockIdx.x) - a.n);
+    // block n M + b prefetches for the slice of block b (same XCD when n M
+    // is a multiple of 8)
+    member_of(int(blockIdx.x) - a.n * M, a.n, M, i, m);
+    prefetch_pass<E>(a, p, i * M + m, i);
     return;
   }
   __shared__ FastShared sh;
-  int i, m;
   member_of(int(blockIdx.x), a.n, M, i, m);
   fast_pass<E, MEM>(a, p, i, m, sh);
 }
@@ -322,7 +325,7 @@ hipError_t launch_fast_e(const SgdArgs& a, const PlanArgs& p, hipStream_t s) {
   if (p.members > 1) {
     // members wait for each other every step: cooperative, so that all are
     // resident at once
-    const uint32_t grid = uint32_t(a.n) * uint32_t(p.members);
+    const uint32_t grid = uint32_t(a.n) * uint32_t(p.members) * (p.helpers ? 2u : 1u);
     SgdArgs aa = a;
     PlanArgs pp = p;
     void* args[] = {&aa, &pp};
