@@ -123,6 +123,7 @@ struct PlanArgs {
   // own), and n counts slices.  With one member a slice is the worker.
   int32_t members;
   int32_t workers;          // real workers
+  int32_t max_slice;        // longest row of one member's columns
   const int32_t* mhot;      // [members][kHotMax] column of each member's hot slot
   int32_t n_mhot[4];        // hot slots of each member
   unsigned long long* xch;  // [workers][2][members][64][2] tagged halves of partial margins (step parity 2nd)

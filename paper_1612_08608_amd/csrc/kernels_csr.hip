@@ -457,7 +457,10 @@ __device__ inline bool wait_plan(const RoundsPlan& rp, int64_t u, long long dead
 // overflowed runs the general pass code, as the stream-ordered path does,
 // so both give the same bits.  With helpers, block n + i prefetches for
 // worker i, pass after pass.
-template <int E, bool MEM>
+// EG: entries per lane of the general pass (the stream-ordered general
+// kernel's, so that both give the same bits); EF: of the planned pass, sized
+// for the members' slices (its bits do not depend on it).
+template <int EG, int EF, bool MEM>
 __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a, RoundsArgs ra, RoundsPlan rp) {
   union LdsUnion {
     Shared g;
@@ -493,7 +496,7 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
       ah.k1 = pass == q1 ? j1 : K;
       ah.rowinfo = p.rowinfo;
       ah.models = ra.buf[ra.cur ^ int((rfirst - ra.r0) & 1)];
-      prefetch_pass<E>(ah, p, i * M + m, i);
+      prefetch_pass<EF>(ah, p, i * M + m, i);
       __syncthreads();
     }
     return;
@@ -519,10 +522,10 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
         if (__hip_atomic_load(pu.flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
           // the general pass is one workgroup's: member 0 runs it alone
           ap.rowinfo = pu.rows_real;
-          if (m == 0) csr_pass<E, true>(ap, i, sh.g);
+          if (m == 0) csr_pass<EG, true>(ap, i, sh.g);
           return true;
         }
-        fast_pass<E, MEM>(ap, pu, i, m, sh.f);
+        fast_pass<EF, MEM>(ap, pu, i, m, sh.f);
         if constexpr (!MEM) return true;
         // members: member 0 publishes the worker's half-step only after
         // every member's model stores are complete and released
@@ -572,11 +575,12 @@ hipError_t launch_rounds_pipe(const SgdArgs& a, const RoundsArgs& ra, int n_cu, 
   return pipe ? launch_rounds_e<E, true>(a, ra, n_cu, s) : launch_rounds_e<E, false>(a, ra, n_cu, s);
 }
 
-template <int E, bool MEM>
+template <int EG, int EF, bool MEM>
 hipError_t launch_rounds_planned_em(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
                                     hipStream_t s) {
   int per = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_csr_planned_kernel<E, MEM>, kThreads, 0);
+  hipError_t e =
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, rounds_csr_planned_kernel<EG, EF, MEM>, kThreads, 0);
   if (e != hipSuccess) return e;
   const int64_t grid = int64_t(a.n) * rp.area0.members * (rp.area0.helpers ? 2 : 1);
   if (int64_t(per) * n_cu < grid) return hipErrorCooperativeLaunchTooLarge;
@@ -584,15 +588,22 @@ hipError_t launch_rounds_planned_em(const SgdArgs& a, const RoundsArgs& ra, cons
   RoundsArgs rr = ra;
   RoundsPlan pp = rp;
   void* args[] = {&aa, &rr, &pp};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&rounds_csr_planned_kernel<E, MEM>),
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&rounds_csr_planned_kernel<EG, EF, MEM>),
                                     dim3(uint32_t(grid)), dim3(kThreads), args, 0, s);
 }
 
-template <int E>
+// One member: EF = EG.  Members: the smallest of 3, 5 and EG entries per
+// lane that covers the slices' rows.
+template <int EG>
 hipError_t launch_rounds_planned_e(const SgdArgs& a, const RoundsArgs& ra, const RoundsPlan& rp, int n_cu,
                                    hipStream_t s) {
-  return rp.area0.members > 1 ? launch_rounds_planned_em<E, true>(a, ra, rp, n_cu, s)
-                              : launch_rounds_planned_em<E, false>(a, ra, rp, n_cu, s);
+  if (rp.area0.members == 1) return launch_rounds_planned_em<EG, EG, false>(a, ra, rp, n_cu, s);
+  const int need = rp.area0.max_slice;
+  if constexpr (EG > 3)
+    if (need <= kRowLanes * 3) return launch_rounds_planned_em<EG, 3, true>(a, ra, rp, n_cu, s);
+  if constexpr (EG > 5)
+    if (need <= kRowLanes * 5) return launch_rounds_planned_em<EG, 5, true>(a, ra, rp, n_cu, s);
+  return launch_rounds_planned_em<EG, EG, true>(a, ra, rp, n_cu, s);
 }
 
 // ----------------------------------------------------------------------------
