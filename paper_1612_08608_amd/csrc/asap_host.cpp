@@ -94,7 +94,7 @@ struct asap_ctx {
          off_vmax = 0, off_scan = 0, off_wbar = 0, off_part = 0, off_out = 0, off_rowok = 0,
          off_code = 0, off_lut = 0, off_hot = 0, off_dacc = 0, off_dxcd = 0, off_dcount = 0, off_progress = 0,
          off_vrp = 0, off_vcode = 0, off_mlut = 0, off_mhot = 0, off_xch = 0, off_done = 0, off_xid = 0,
-         total = 0;
+         off_msync = 0, total = 0;
   RoundPlan plan[2];
   int32_t dense_k = 1;  // workgroups per worker the dense workspace is sized for
 
@@ -195,6 +195,7 @@ void layout(asap_ctx* c) {
   c->off_vmax = o;  o = align_up(o + n * 4);
   c->off_scan = o;  o = align_up(o + 8 * 8);
   c->off_rowok = o; o = align_up(o + n * 4);
+  c->off_msync = o; o = align_up(o + n * kMemberSync * 8);
   c->plan[0].sched = o; o = align_up(o + n * size_t(c->S) * 4);
   c->off_wbar = o;  o = align_up(o + size_t(c->dim) * 8);
   c->off_part = o;  o = align_up(o + metric_part_doubles(int64_t(n), c->S) * 8);
@@ -1318,6 +1319,10 @@ extern "C" asap_status asap_run_rounds(asap_ctx* c, const asap_sgd_params* p, in
   ra.err = at<int32_t>(c, c->off_err);
   ra.sched = at<int32_t>(c, c->plan[0].sched);
   ra.rowinfo = at<RowInfo>(c, c->plan[0].rowinfo);
+  ra.msync = at<int64_t>(c, c->off_msync);
+  // the members' words carry round tags, which a launch after asap_set_round
+  // may repeat: every launch starts from -1
+  if ((e = launch_fill_i64(ra.msync, int64_t(n) * kMemberSync, -1, s))) return hip_fail(c, e, "launch init");
   if (c->kind == kCsr) {
     // the passes this launch covers
     const int64_t K = (c->S + p->batch - 1) / p->batch;

@@ -183,7 +183,9 @@ struct RoundsArgs {
   int32_t* err;        // device error words
   int32_t* sched;      // [n][S] dense: this pass's schedule rows
   RowInfo* rowinfo;    // [n][S] CSR: this pass's row descriptors
+  int64_t* msync;      // [n][kMemberSync] members of a worker: reduce go, parts done (-1 at launch)
 };
+constexpr int kMemberSync = 9;  // the go word and one word per member (up to 8)
 // Plans of the passes of a multi-round launch on planned CSR passes: pass
 // first_pass + u has its plan in area u (the pointers of area0 advanced by
 // u * stride bytes); the area is published when ready[u] == token0 + u.

@@ -414,7 +414,7 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_kernel(SgdArgs a, RoundsA
   const int i = int(blockIdx.x);
   __shared__ Shared sh;
   rounds::drive(
-      a, ra, i, 0,
+      a, ra, i, 0, 1,
       [&](int64_t pass) {
         rounds::fill_rowinfo(ra.seed, i, pass, a.S, a.row_ptr, a.y, ra.rowinfo + int64_t(i) * a.S);
       },
@@ -505,7 +505,7 @@ __global__ __launch_bounds__(kThreads) void rounds_csr_planned_kernel(SgdArgs a,
   member_of(int(blockIdx.x), ra.n, M, i, m);
   PlanArgs pu = ring_area(rp, 0);
   rounds::drive(
-      a, ra, i, m,
+      a, ra, i, m, M,
       [&](int64_t pass) {
         const int64_t u = pass - rp.first_pass;
         if (threadIdx.x == 0) {

@@ -517,7 +517,7 @@ __global__ __launch_bounds__(kThreads) void rounds_dense_wide_kernel(SgdArgs a, 
   int i, k;
   wide_member(a.n, ds.K, i, k);
   rounds::drive(
-      a, ra, i, k, [&](int64_t pass) { rounds::fill_schedule(ra.seed, i, pass, a.S, ra.sched + int64_t(i) * a.S); },
+      a, ra, i, k, ds.K, [&](int64_t pass) { rounds::fill_schedule(ra.seed, i, pass, a.S, ra.sched + int64_t(i) * a.S); },
       [&](const SgdArgs& ar) {
         const bool ok = dense_wide_pass<CPQ, SR>(ar, ds, i, k);
         // arrivals of this pass: the opening meeting and one per step

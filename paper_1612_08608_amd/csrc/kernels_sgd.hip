@@ -189,7 +189,7 @@ template <int CPT>
 __global__ __launch_bounds__(1024) void rounds_dense_kernel(SgdArgs a, RoundsArgs ra) {
   const int i = int(blockIdx.x);
   rounds::drive(
-      a, ra, i, 0, [](int64_t) {},  // the pass evaluates its sample order itself
+      a, ra, i, 0, 1, [](int64_t) {},  // the pass evaluates its sample order itself
       [&](const SgdArgs& ar) {
         dense_pass<CPT>(ar, i);
         return true;

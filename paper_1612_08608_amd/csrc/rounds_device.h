@@ -126,14 +126,19 @@ __device__ inline void fill_rowinfo(uint64_t seed, int i, int64_t pass, int64_t 
 // writers released them before the tags this workgroup waited for).
 constexpr int kMixVec = 4;
 
+// Member `part` of `parts` reduces the part-th of the row's float4 columns
+// (the whole row with one part); every output element has the same
+// arithmetic whatever the split.
 template <bool F64>
-__device__ void mix_row(const RoundsArgs& ra, int i, int e, int64_t ld, int64_t dim) {
+__device__ void mix_row(const RoundsArgs& ra, int i, int e, int64_t ld, int64_t dim, int part, int parts) {
   const int p0 = ra.in_ptr[i], deg = ra.in_ptr[i + 1] - p0;
   const float* scale = ra.scaled ? ra.scale2 + int64_t(e) * ra.n : nullptr;
   const float* src = ra.buf[e];
   float* dst = ra.buf[e ^ 1] + int64_t(i) * ld;
-  const int64_t nq = (dim + 3) / 4, T = blockDim.x;
-  for (int64_t q0 = threadIdx.x; q0 < nq; q0 += kMixVec * T) {
+  const int64_t nq_all = (dim + 3) / 4, T = blockDim.x;
+  const int64_t per = (nq_all + parts - 1) / parts;
+  const int64_t qb = min(nq_all, per * part), nq = min(nq_all, qb + per);
+  for (int64_t q0 = qb + threadIdx.x; q0 < nq; q0 += kMixVec * T) {
     double ad[kMixVec][4];
     float4 af[kMixVec];
 #pragma unroll
@@ -187,13 +192,18 @@ __device__ void mix_row(const RoundsArgs& ra, int i, int e, int64_t ld, int64_t 
   }
 }
 
-// The round loop of one workgroup: member `member` of worker i (members > 0
-// exist only for the wide dense pass; member 0 publishes, waits and
-// reduces, the others wait for the reduced row).  `prepare(pass)` writes the
-// pass's schedule inputs (whole workgroup); `pass_fn(a)` runs the half-step
-// and returns false when the members' own rendezvous timed out.
+// The round loop of one workgroup: member `member` of the `members`
+// workgroups of worker i.  Member 0 publishes the half-step (NOTIFY) once
+// pass_fn has returned on every member, waits for the neighbours, and lets
+// the other members go (ra.msync[i][0]); each member reduces its part of
+// the row's columns and reports it (ra.msync[i][1 + member]); member 0 then
+// publishes the reduced row (ACK), which the others wait for before their
+// next pass.  `prepare(pass)` writes the pass's schedule inputs (whole
+// workgroup); `pass_fn(a)` runs the half-step and returns false when the
+// members' own rendezvous timed out.
 template <class Prepare, class Pass>
-__device__ void drive(SgdArgs a, const RoundsArgs& ra, int i, int member, Prepare&& prepare, Pass&& pass_fn) {
+__device__ void drive(SgdArgs a, const RoundsArgs& ra, int i, int member, int members, Prepare&& prepare,
+                      Pass&& pass_fn) {
   __shared__ int stop;
   const int tid = threadIdx.x, n = ra.n;
   const int64_t K = (a.S + a.batch - 1) / a.batch;
@@ -228,10 +238,11 @@ __device__ void drive(SgdArgs a, const RoundsArgs& ra, int i, int member, Prepar
     if (!ok) return;
     int64_t* te = ra.tag + int64_t(e) * n;
     int64_t* tn = ra.tag + int64_t(e ^ 1) * n;
-    if (member == 0) {
-      if (tid == 0) {
+    int64_t* ms = ra.msync + int64_t(i) * kMemberSync;
+    if (tid == 0) {
+      const long long deadline = wall_clock64() + ra.wait_ticks;
+      if (member == 0) {
         tag_release(te + i, tag_half(r));  // NOTIFY
-        const long long deadline = wall_clock64() + ra.wait_ticks;
         const int pi = ra.in_ptr[i], po = ra.out_ptr[i];
         int miss = wait_tags(te, ra.in_idx + pi, ra.in_ptr[i + 1] - pi, tag_half(r), deadline);
         if (miss < 0) miss = wait_tags(te, ra.out_idx + po, ra.out_ptr[i + 1] - po, tag_start(r), deadline);
@@ -240,23 +251,33 @@ __device__ void drive(SgdArgs a, const RoundsArgs& ra, int i, int member, Prepar
         // them after this wait)
         stop = miss >= 0;
         if (stop) report_stale(ra.err, i);
+        else if (members > 1) tag_release(ms, tag_half(r));  // the other members may reduce
+      } else {
+        stop = !wait_tag(ms, tag_half(r), deadline);
       }
-      __syncthreads();
-      if (stop) return;
-      if (ra.fp64_mix)
-        mix_row<true>(ra, i, e, a.ld, a.dim);
-      else
-        mix_row<false>(ra, i, e, a.ld, a.dim);
-      __syncthreads();
-      if (tid == 0) tag_release(tn + i, tag_start(r + 1));  // ACK, and round r + 1 starts from this row
-    } else {
-      if (tid == 0) {
-        stop = !wait_tag(tn + i, tag_start(r + 1), wall_clock64() + ra.wait_ticks);
+    }
+    __syncthreads();
+    if (stop) return;
+    if (ra.fp64_mix)
+      mix_row<true>(ra, i, e, a.ld, a.dim, member, members);
+    else
+      mix_row<false>(ra, i, e, a.ld, a.dim, member, members);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of the row is written
+    __syncthreads();
+    if (tid == 0) {
+      const long long deadline = wall_clock64() + ra.wait_ticks;
+      if (member == 0) {
+        for (int q = 1; q < members && !stop; ++q) stop = !wait_tag(ms + 1 + q, tag_half(r), deadline);
+        if (stop) report_stale(ra.err, i);
+        else tag_release(tn + i, tag_start(r + 1));  // ACK, and round r + 1 starts from this row
+      } else {
+        tag_release(ms + 1 + member, tag_half(r));  // this part is reduced
+        stop = !wait_tag(tn + i, tag_start(r + 1), deadline);
         acquire_fence();
       }
-      __syncthreads();
-      if (stop) return;
     }
+    __syncthreads();
+    if (stop) return;
   }
 }
 
