@@ -256,6 +256,14 @@ def test_csr_members_against_the_oracle(torch, case, members):
         _free_run(torch, wl, "random", 8, 3, loss_curve=True, members=members)
 
 
+def test_csr_members_on_several_xcds(torch):
+    # 12 workers (not a multiple of the 8 XCDs): a worker's members are
+    # consecutive workgroups, which land on different XCDs, so they exchange
+    # their partial margins with device-scope stores
+    wl = synth.SPARSE_LR_64W.with_(n_workers=12, dim=1 << 13, samples=640)
+    _free_run(torch, wl, "random", 4, 3, loss_curve=True, members=2)
+
+
 @pytest.mark.parametrize("members", [1, 4])
 def test_csr_l2_scale_fold(torch, members):
     # strong L2 with a constant step: the pass's scale s = prod (1 - eta l2)

@@ -244,6 +244,9 @@ PLANNED = {
     "c3_shape_128w": (synth.SPARSE_SVM_256W.with_(n_workers=128, dim=1 << 13, samples=256), "random", 8, 3, 0, 0),
     "hinge_l2_2_members": (synth.SPARSE_SVM_256W.with_(n_workers=32, dim=1 << 13, samples=256, l2=1e-3), "random",
                            8, 3, 0, 2),
+    # 12 workers: members of a worker on different XCDs
+    "members_several_xcds": (synth.SPARSE_LR_64W.with_(n_workers=12, dim=1 << 13, samples=256), "random", 4, 3, 0,
+                             2),
     "local_steps": (synth.SPARSE_LR_64W.with_(n_workers=8, dim=1 << 13, samples=512, batch=64), "chain", 0, 7, 2, 0),
     # ~3800 distinct rarely used columns per step: every plan overflows and
     # every pass runs the general code, on both paths
