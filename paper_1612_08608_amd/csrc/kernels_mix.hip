@@ -217,7 +217,7 @@ __device__ __forceinline__ void store_partial(float* d, float4 v, int k) {
 }
 
 // LDS reads in flight per thread
-template <int DEG, int R> constexpr int slab_group() { return DEG <= 5 ? DEG : (R == 2 && DEG > 9 ? 2 : 4); }
+template <int DEG, int R> constexpr int slab_group() { return DEG <= 5 ? DEG : (R == 2 && DEG > 9 ? 1 : 4); }
 
 // Slab kernel.  One THREADS-thread workgroup per CU walks a contiguous
 // range of column chunks; a chunk is all n rows of 4 VEC / n columns (VEC
@@ -297,14 +297,6 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
     }
     ok[rr] = a.row_ok[row] != 0;
   }
-  auto weight = [&](int rr, int p) -> float {
-    if constexpr (UNI) {
-      const float w_in = p == upos[rr] ? uw_self[rr] : uw_off[rr];
-      return p < ulen[rr] ? w_in : 0.f;
-    } else {
-      return nw[rr][p];
-    }
-  };
   const int per = (nchunks + int(gridDim.x) - 1) / int(gridDim.x);
   const int ch0 = int(blockIdx.x) * per, ch1 = min(nchunks, ch0 + per);
 
@@ -346,18 +338,47 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
   // Output float4 q of row rr of this thread from the staged chunk.  Padding
   // entries read the own row with weight 0, which adds an exact zero, so the
   // reads of a group issue back to back with no branches.
-  auto slab_row = [&](int rr, int q) {
+  // the state of the row being computed, copied out of the per-row arrays
+  // by selects (a runtime row index into those arrays would put them in
+  // scratch memory)
+  uint32_t jl[(DEG + 1) / 2];
+  float nl[UNI ? 1 : DEG];
+  float ls_self = 0.f, ls_off = 0.f;
+  int lpos = 0, llen = 0;
+  auto select_row = [&](int rr) {
+    const bool second = R == 2 && rr == 1;
+#pragma unroll
+    for (int k = 0; k < (DEG + 1) / 2; ++k) jl[k] = second ? jq2[R - 1][k] : jq2[0][k];
+    if constexpr (UNI) {
+      ls_self = second ? uw_self[R - 1] : uw_self[0];
+      ls_off = second ? uw_off[R - 1] : uw_off[0];
+      lpos = second ? upos[R - 1] : upos[0];
+      llen = second ? ulen[R - 1] : ulen[0];
+    } else {
+#pragma unroll
+      for (int k = 0; k < DEG; ++k) nl[k] = second ? nw[R - 1][k] : nw[0][k];
+    }
+  };
+  auto lweight = [&](int p) -> float {
+    if constexpr (UNI) {
+      const float w_in = p == lpos ? ls_self : ls_off;
+      return p < llen ? w_in : 0.f;
+    } else {
+      return nl[p];
+    }
+  };
+  auto slab_row = [&](int q) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     // Empty asm statements pin the register plan: the packed slots stay
     // packed and the weights stay in registers (not reloaded from memory),
     // and the reads of one group are not hoisted above the previous group.
 #pragma unroll
-    for (int k = 0; k < (DEG + 1) / 2; ++k) asm volatile("" : "+v"(jq2[rr][k]));
+    for (int k = 0; k < (DEG + 1) / 2; ++k) asm volatile("" : "+v"(jl[k]));
     if constexpr (UNI) {
-      asm volatile("" : "+v"(uw_self[rr]), "+v"(uw_off[rr]), "+v"(upos[rr]), "+v"(ulen[rr]));
+      asm volatile("" : "+v"(ls_self), "+v"(ls_off), "+v"(lpos), "+v"(llen));
     } else {
 #pragma unroll
-      for (int k = 0; k < DEG; ++k) asm volatile("" : "+v"(nw[rr][k]));
+      for (int k = 0; k < DEG; ++k) asm volatile("" : "+v"(nl[k]));
     }
 #pragma unroll
     for (int p0 = 0; p0 < DEG; p0 += G) {
@@ -365,9 +386,9 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
       float4 x[G];
 #pragma unroll
       for (int p = p0; p < p0 + G && p < DEG; ++p)
-        x[p - p0] = slab[((jq2[rr][p / 2] >> (16 * (p & 1))) & 0xffffu) ^ q];
+        x[p - p0] = slab[((jl[p / 2] >> (16 * (p & 1))) & 0xffffu) ^ q];
 #pragma unroll
-      for (int p = p0; p < p0 + G && p < DEG; ++p) fma4(acc, weight(rr, p), x[p - p0]);
+      for (int p = p0; p < p0 + G && p < DEG; ++p) fma4(acc, lweight(p), x[p - p0]);
     }
     // all four components here, or the compiler splits 16-byte LDS reads
     asm volatile("" : "+v"(acc.x), "+v"(acc.y), "+v"(acc.z), "+v"(acc.w));
@@ -379,14 +400,18 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
 #pragma unroll
   for (int rr = 0; rr < R; ++rr) okmask[rr] = __ballot(ok[rr]);
   auto compute = [&](int ch) {
-#pragma unroll
+    // one row at a time (R = 2: the second row's state is selected in, not
+    // kept beside the first's while its outputs are computed)
+#pragma unroll 1
     for (int rr = 0; rr < R; ++rr) {
-      const int row_base = orow[rr] & ~(kOut - 1);
+      select_row(rr);
+      const int row_base = (R == 2 && rr == 1 ? orow[R - 1] : orow[0]) & ~(kOut - 1);
+      const uint64_t okm = R == 2 && rr == 1 ? okmask[R - 1] : okmask[0];
 #pragma unroll 1
       for (int h = 0; h < OPR / kOut; ++h) {
         float4 res[kOut];
 #pragma unroll
-        for (int u = 0; u < kOut; ++u) res[u] = slab_row(rr, oq0 + h * kOut + u);
+        for (int u = 0; u < kOut; ++u) res[u] = slab_row(oq0 + h * kOut + u);
         transpose8(res, lane_in);
         const int64_t c = int64_t(ch) * C + 4 * (oq0 + h * kOut + lane_in);
         if (c < a.dim) {
@@ -394,7 +419,7 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
           const int k_tail = int(min<int64_t>(a.dim - c, 4));
 #pragma unroll
           for (int k = 0; k < kOut; ++k) {
-            if ((okmask[rr] >> (lane - lane_in + k)) & 1) {
+            if ((okm >> (lane - lane_in + k)) & 1) {
               float* d = a.dst + int64_t(row_base + k) * a.ld + c;
               if (full) {
                 *reinterpret_cast<float4*>(d) = res[k];
