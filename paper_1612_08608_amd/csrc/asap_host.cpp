@@ -984,6 +984,7 @@ PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp, c
   pa.members = c->members;
   pa.workers = c->n;
   pa.max_slice = c->max_slice;
+  pa.n_cu = c->n_cu;
   pa.mhot = split ? ::at<int32_t>(c, c->off_mhot) : ::at<int32_t>(c, c->off_hot);
   for (int m = 0; m < kMaxMembers; ++m) pa.n_mhot[m] = m < c->members ? c->n_mhot[m] : 0;
   pa.xch = split ? ::at<unsigned long long>(c, c->off_xch) : nullptr;

@@ -124,6 +124,7 @@ struct PlanArgs {
   int32_t members;
   int32_t workers;          // real workers
   int32_t max_slice;        // longest row of one member's columns
+  int32_t n_cu;             // compute units of the device
   const int32_t* mhot;      // [members][kHotMax] column of each member's hot slot
   int32_t n_mhot[4];        // hot slots of each member
   unsigned long long* xch;  // [workers][2][members][64][2] tagged halves of partial margins (step parity 2nd)

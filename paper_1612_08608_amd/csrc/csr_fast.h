@@ -121,6 +121,16 @@ __device__ __forceinline__ void member_of(int b, int n, int M, int& i, int& m) {
   }
 }
 
+// hold() for 64-bit values
+template <int N>
+__device__ __forceinline__ void hold_u64(unsigned long long (&v)[N]) {
+  static_assert(N == 4 || N == 8, "hold_u64: 4 or 8 values");
+  if constexpr (N == 4) asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
+  if constexpr (N == 8)
+    asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
+                 "+v"(v[7]));
+}
+
 constexpr uint32_t kPrefetchSpin = 1u << 16;  // polls of the pass's progress per step (bounded)
 constexpr int kPrefetchLead = 3;              // steps ahead of the pass
 
@@ -249,8 +259,10 @@ __device__ __forceinline__ double member_exchange(const PlanArgs& p, __amdgpu_bu
 // writes the final L2 scale, and the epoch tag when a.tag is set.  MEM:
 // p.members > 1 (with one member the slice is the whole worker and nothing
 // is exchanged).
-template <int E, bool MEM>
+template <int E, bool MEM, int NT = kThreads>
 __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, FastShared& sh) {
+  constexpr int CP = kCMax / NT, HP = kHList / NT;  // cold and hot list slots per thread
+  static_assert(NT % 64 == 0 && kCMax % NT == 0 && kHList % NT == 0, "fast_pass: thread count");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane & (kRowLanes - 1);
   const int brow = wave * (64 / kRowLanes) + (lane / kRowLanes);
@@ -274,11 +286,11 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
   // members: this worker's exchange words, [2][M][64][2] (unused with one member)
   const auto xr = rsrc(MEM ? p.xch + size_t(i) * size_t(M) * 256u : nullptr, MEM ? uint32_t(M) * 2048u : 0u);
 
-  for (int h = tid; h < H; h += kThreads) {
+  for (int h = tid; h < H; h += NT) {
     sh.vhot[h] = vrow[hot_cols[h]];
     sh.acch[h] = 0ull;
   }
-  for (int q = tid; q < kCMax; q += kThreads) sh.cacc[q] = 0ull;
+  for (int q = tid; q < kCMax; q += NT) sh.cacc[q] = 0ull;
   bool local = false;
   if (tid == 0) {
     sh.xabort = 0;
@@ -324,41 +336,41 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
   RowInfo r1, r2;
   DataReg<E> d0, d1;
   Meta m0, m1, m2, m3;
-  int cl0[kColdPer], lk0[kColdPer], cl1[kColdPer], lk1[kColdPer], cl2[kColdPer];
-  float g0[kColdPer], g1[kColdPer];
-  int hl0[kHotPer], hl1[kHotPer];
+  int cl0[CP], lk0[CP], cl1[CP], lk1[CP], cl2[CP];
+  float g0[CP], g1[CP];
+  int hl0[HP], hl1[HP];
   // list loads: a wave whose first slot is past the count issues nothing
   const int wave0 = __builtin_amdgcn_readfirstlane(wave * 64);
-  auto load_cols = [&](const Meta& m, int (&cl)[kColdPer]) {
+  auto load_cols = [&](const Meta& m, int (&cl)[CP]) {
 #pragma unroll
-    for (int j = 0; j < kColdPer; ++j) {
-      const int u = tid + j * kThreads;
+    for (int j = 0; j < CP; ++j) {
+      const int u = tid + j * NT;
       cl[j] = 0;
-      if (wave0 + j * kThreads < m.uc) cl[j] = ld_i32(clist, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
+      if (wave0 + j * NT < m.uc) cl[j] = ld_i32(clist, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
     }
   };
-  auto load_links = [&](const Meta& m, int (&lk)[kColdPer]) {
+  auto load_links = [&](const Meta& m, int (&lk)[CP]) {
 #pragma unroll
-    for (int j = 0; j < kColdPer; ++j) {
-      const int u = tid + j * kThreads;
+    for (int j = 0; j < CP; ++j) {
+      const int u = tid + j * NT;
       lk[j] = -1;
-      if (wave0 + j * kThreads < m.uc) lk[j] = ld_i32(clink, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
+      if (wave0 + j * NT < m.uc) lk[j] = ld_i32(clink, uint32_t(m.soff + (u < m.uc ? u : 0)) * 4u);
     }
   };
-  auto load_hot = [&](const Meta& m, int (&hl)[kHotPer]) {
+  auto load_hot = [&](const Meta& m, int (&hl)[HP]) {
 #pragma unroll
-    for (int j = 0; j < kHotPer; ++j) {
-      const int u = tid + j * kThreads;
+    for (int j = 0; j < HP; ++j) {
+      const int u = tid + j * NT;
       hl[j] = 0;
-      if (wave0 + j * kThreads < m.uh) hl[j] = ld_i32(hlist, uint32_t(m.soff + (u < m.uh ? u : 0)) * 4u);
+      if (wave0 + j * NT < m.uh) hl[j] = ld_i32(hlist, uint32_t(m.soff + (u < m.uh ? u : 0)) * 4u);
     }
   };
-  auto gather = [&](const Meta& m, const int (&cl)[kColdPer], float (&g)[kColdPer]) {
+  auto gather = [&](const Meta& m, const int (&cl)[CP], float (&g)[CP]) {
 #pragma unroll
-    for (int j = 0; j < kColdPer; ++j) {
-      const int u = tid + j * kThreads;
+    for (int j = 0; j < CP; ++j) {
+      const int u = tid + j * NT;
       g[j] = 0.f;
-      if (wave0 + j * kThreads < m.uc) g[j] = ld_f32(w.model, uint32_t(u < m.uc ? cl[j] : 0) * 4u);
+      if (wave0 + j * NT < m.uc) g[j] = ld_f32(w.model, uint32_t(u < m.uc ? cl[j] : 0) * 4u);
     }
   };
   {
@@ -392,14 +404,14 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
       m1 = m2;
       m2 = uniform(m3);  // loaded by the previous step, landed at its fence
 #pragma unroll
-      for (int j = 0; j < kColdPer; ++j) {
+      for (int j = 0; j < CP; ++j) {
         cl0[j] = cl1[j];
         lk0[j] = lk1[j];
         g0[j] = g1[j];
         cl1[j] = cl2[j];
       }
 #pragma unroll
-      for (int j = 0; j < kHotPer; ++j) hl0[j] = hl1[j];
+      for (int j = 0; j < HP; ++j) hl0[j] = hl1[j];
     }
     const int64_t b0 = k * a.batch;
     const int Bp = int(min(int64_t(a.batch), a.S - b0));
@@ -413,8 +425,8 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
     // launch -> its slot, else the value gathered a step ago (the first step
     // of a launch gathers them all: the launch before wrote them back)
 #pragma unroll
-    for (int j = 0; j < kColdPer; ++j) {
-      const int u = tid + j * kThreads;
+    for (int j = 0; j < CP; ++j) {
+      const int u = tid + j * NT;
       if (u < m0.uc) cv[u] = (k > k0 && lk0[j] >= 0) ? cvp[lk0[j]] : g0[j];
     }
     lds_barrier();
@@ -464,33 +476,32 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
     // update: all accumulator and value reads of a thread first, then the
     // writes (a wave whose first slot is past the count skips a slot)
     {
-      unsigned long long acc[kHotPer + kColdPer];
-      float old[kHotPer + kColdPer];
+      unsigned long long acc[HP + CP];
+      float old[HP + CP];
 #pragma unroll
-      for (int j = 0; j < kHotPer; ++j) {
+      for (int j = 0; j < HP; ++j) {
         acc[j] = 0ull;
         old[j] = 0.f;
-        if (wave0 + j * kThreads < m0.uh) {
+        if (wave0 + j * NT < m0.uh) {
           acc[j] = sh.acch[hl0[j]];
           old[j] = sh.vhot[hl0[j]];
         }
       }
 #pragma unroll
-      for (int j = 0; j < kColdPer; ++j) {
-        const int u = tid + j * kThreads;
-        acc[kHotPer + j] = 0ull;
-        old[kHotPer + j] = 0.f;
-        if (wave0 + j * kThreads < m0.uc) {
-          acc[kHotPer + j] = sh.cacc[u];
-          old[kHotPer + j] = cv[u];
+      for (int j = 0; j < CP; ++j) {
+        const int u = tid + j * NT;
+        acc[HP + j] = 0ull;
+        old[HP + j] = 0.f;
+        if (wave0 + j * NT < m0.uc) {
+          acc[HP + j] = sh.cacc[u];
+          old[HP + j] = cv[u];
         }
       }
-      static_assert(kHotPer + kColdPer == 4, "update batch holds four slots");
-      asm volatile("" : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(old[0]), "+v"(old[1]),
-                   "+v"(old[2]), "+v"(old[3]));
+      hold_u64(acc);
+      hold(old);
 #pragma unroll
-      for (int j = 0; j < kHotPer; ++j) {
-        const int u = tid + j * kThreads;
+      for (int j = 0; j < HP; ++j) {
+        const int u = tid + j * NT;
         if (u < m0.uh && acc[j] != 0ull) {
           const int h = hl0[j];
           sh.vhot[h] = float(double(old[j]) - coefA * double(static_cast<long long>(acc[j])) * from_fx);
@@ -498,11 +509,11 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
         }
       }
 #pragma unroll
-      for (int j = 0; j < kColdPer; ++j) {
-        const int u = tid + j * kThreads;
-        if (u < m0.uc && acc[kHotPer + j] != 0ull) {
+      for (int j = 0; j < CP; ++j) {
+        const int u = tid + j * NT;
+        if (u < m0.uc && acc[HP + j] != 0ull) {
           const float nv =
-              float(double(old[kHotPer + j]) - coefA * double(static_cast<long long>(acc[kHotPer + j])) * from_fx);
+              float(double(old[HP + j]) - coefA * double(static_cast<long long>(acc[HP + j])) * from_fx);
           cv[u] = nv;
           sh.cacc[u] = 0ull;
           st_f32(w.model, uint32_t(cl0[j]) * 4u, nv);
@@ -514,11 +525,11 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
     if (s < 1e-6) {  // fold the scale back into v before it underflows
       const float sf = float(s);
       __syncthreads();
-      for (int h = tid; h < H; h += kThreads) sh.vhot[h] *= sf;
-      for (int64_t c = m + int64_t(tid) * M; c < a.dim; c += int64_t(kThreads) * M) vrow[c] *= sf;  // own columns
+      for (int h = tid; h < H; h += NT) sh.vhot[h] *= sf;
+      for (int64_t c = m + int64_t(tid) * M; c < a.dim; c += int64_t(NT) * M) vrow[c] *= sf;  // own columns
 #pragma unroll
-      for (int j = 0; j < kColdPer; ++j) {
-        const int u = tid + j * kThreads;
+      for (int j = 0; j < CP; ++j) {
+        const int u = tid + j * NT;
         if (u < m0.uc) cv[u] *= sf;  // the next step links to these
         g1[j] *= sf;                 // gathered before the fold
       }
@@ -529,7 +540,7 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
       if (sh.xabort) break;  // reported through p.xerr; the partners time out too
   }
 
-  for (int h = tid; h < H; h += kThreads) vrow[hot_cols[h]] = sh.vhot[h];
+  for (int h = tid; h < H; h += NT) vrow[hot_cols[h]] = sh.vhot[h];
   if (tid == 0) {
     if (m == 0) {
       a.scale[i] = float(s);

@@ -297,8 +297,11 @@ __global__ __launch_bounds__(NT) void csr_link_kernel(PlanArgs p) {
 // ----------------------------------------------------------------------------
 // the pass on the plan (csr_fast.h); block n + i prefetches for worker i
 // ----------------------------------------------------------------------------
-template <int E, bool MEM>
-__global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanArgs p) {
+// NT threads: 1024 (64 rows of 16 lanes), or 512 for minibatches of at most
+// 32 rows when the pass fills the device, so that planning blocks fit beside
+// it on every compute unit (the results do not depend on NT).
+template <int E, bool MEM, int NT = kThreads>
+__global__ __launch_bounds__(NT) void sgd_csr_fast_kernel(SgdArgs a, PlanArgs p) {
   if (*p.flag) return;  // the general kernel takes this round
   const int M = MEM ? p.members : 1;
   int i, m;
@@ -311,7 +314,7 @@ __global__ __launch_bounds__(kThreads) void sgd_csr_fast_kernel(SgdArgs a, PlanA
   }
   __shared__ FastShared sh;
   member_of(int(blockIdx.x), a.n, M, i, m);
-  fast_pass<E, MEM>(a, p, i, m, sh);
+  fast_pass<E, MEM, NT>(a, p, i, m, sh);
 }
 
 __global__ void pack_values_kernel(const int32_t* __restrict__ code, const float* __restrict__ val, int64_t nnz,
@@ -331,6 +334,11 @@ hipError_t launch_fast_e(const SgdArgs& a, const PlanArgs& p, hipStream_t s) {
     void* args[] = {&aa, &pp};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&sgd_csr_fast_kernel<E, true>), dim3(grid),
                                       dim3(kThreads), args, 0, s);
+  }
+  if (p.helpers == 0 && a.batch <= kFastRows / 2 && int64_t(a.n) * 2 > p.n_cu) {
+    hipLaunchKernelGGL((sgd_csr_fast_kernel<E, false, kThreads / 2>), dim3(uint32_t(a.n)), dim3(kThreads / 2), 0, s,
+                       a, p);
+    return hipGetLastError();
   }
   // with helpers, block n + i prefetches for block i: the same XCD when n is
   // a multiple of the 8 XCDs (blocks are dealt to them round-robin)

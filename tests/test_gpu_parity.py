@@ -256,6 +256,14 @@ def test_csr_members_against_the_oracle(torch, case, members):
         _free_run(torch, wl, "random", 8, 3, loss_curve=True, members=members)
 
 
+def test_csr_small_batch_pass_on_a_full_device(torch):
+    # 160 workers with minibatches of 32 rows fill the device: the planned
+    # pass runs 512-thread workgroups (32 rows of 16 lanes), so that the next
+    # round's planning fits beside them
+    wl = synth.SPARSE_SVM_256W.with_(n_workers=160, dim=1 << 12, samples=200, l2=1e-3)
+    _free_run(torch, wl, "random", 8, 3, loss_curve=True)
+
+
 def test_csr_members_on_several_xcds(torch):
     # 12 workers (not a multiple of the 8 XCDs): a worker's members are
     # consecutive workgroups, which land on different XCDs, so they exchange
