@@ -43,8 +43,7 @@ using namespace csr;
 
 constexpr int kHotWords = (kHotMax + 31) / 32;
 
-constexpr int kPlanThreads = 512;
-constexpr int kPlanWaves = kPlanThreads / 64;
+constexpr int kPlanThreads = 256;
 constexpr int kLinkBits = 12;
 constexpr int kLinkTab = 1 << kLinkBits;     // link hash positions (>= 2 kCMax)
 
@@ -145,21 +144,24 @@ __global__ __launch_bounds__(kScanThreads) void step_scan_kernel(PlanArgs p) {
 // ----------------------------------------------------------------------------
 // plan of one (worker, step): distinct columns, slots, per-nonzero codes
 // ----------------------------------------------------------------------------
-// TB: LDS for 2^TB table positions; a step uses the smallest power of two
-// >= 2 * (its nonzeros), at most 2^TB.  NT threads; H nonzeros per lane and
-// row (rows of at most 64 H).
-template <int TB, int NT, int H>
+// The step's T nonzeros are numbered in row order and dealt to the threads
+// flat (thread t takes e = t, t + NT, ...: every lane busy whatever the row
+// lengths); an LDS byte per nonzero names its row.  TB: LDS for 2^TB table
+// positions (a step uses the smallest power of two >= 2 T, at most 2^TB).
+// G: nonzeros per thread, G NT >= the step's most (rows x longest row).
+template <int TB, int NT, int G>
 __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
   constexpr int NW = NT / 64;
-  static_assert(NT >= kHotWords, "one hot-bitmap word per thread");
-  __shared__ int keys[1 << TB];
-  __shared__ uint16_t ids[1 << TB];  // slots < 2^TB <= 2^13
+  constexpr int PMAX = (1 << TB) / NT;  // table positions per thread, at most
+  static_assert(NT >= kHotWords && NT >= kFastRows, "one hot-bitmap word and one row per thread");
+  __shared__ int keys[1 << TB];      // a column, then its slot
   __shared__ uint32_t hot[kHotWords];
   __shared__ int sc[NW];
-  __shared__ long long rstart[kFastRows];
+  __shared__ int roff[kFastRows];    // a row's first nonzero in the step's numbering
   __shared__ int rlen[kFastRows];
+  __shared__ int rdelta[kFastRows];  // row start - worker start - roff
+  __shared__ uint8_t rowof[G * NT];
   __shared__ int overflow;
-  constexpr int kRowsPerWave = kFastRows / NW;
   const int K = p.K, B = p.batch;
   const int i = int(blockIdx.x) / K, k = int(blockIdx.x) % K;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -169,60 +171,93 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
   const int Bp = int(min<int64_t>(B, S - b0));  // <= kFastRows
   const int32_t* so = p.step_off + int64_t(i) * (S + 1);
   const int64_t lbase = seg + so[k];
-  // a table of at least twice the step's nonzeros (at most 2^TB)
   const int T = so[k + 1] - so[k];
+  if (T > G * NT) {  // never with the host's choice of G; the general kernel would run
+    if (t == 0) {
+      p.cnt[(int64_t(i) * K + k) * 2 + 0] = 0;
+      p.cnt[(int64_t(i) * K + k) * 2 + 1] = 0;
+      atomicOr(p.flag, 1);
+    }
+    return;
+  }
+  // a table of at least twice the step's nonzeros (at most 2^TB)
   int bits = 8;
   while (bits < TB && (1 << bits) < 2 * T) ++bits;
   const int tab = 1 << bits;
-  if (t < Bp) {
-    const RowInfo r = p.rowinfo[int64_t(i) * S + b0 + t];
-    rstart[t] = r.start;
-    rlen[t] = r.len;
+  if (wave == 0) {
+    // rows' offsets in the step's numbering: an inclusive scan over lanes
+    int len = 0;
+    long long st = 0;
+    if (lane < Bp) {
+      const RowInfo r = p.rowinfo[int64_t(i) * S + b0 + lane];
+      st = r.start;
+      len = r.len;
+    }
+    int x = len;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    roff[lane] = x - len;
+    rlen[lane] = len;
+    rdelta[lane] = int(st - seg) - (x - len);
   }
   for (int q = t; q < tab; q += NT) keys[q] = -1;
   for (int q = t; q < kHotWords; q += NT) hot[q] = 0u;
   if (t == 0) overflow = 0;
   __syncthreads();
-  // every code of the step in registers (rows of at most 64 H nonzeros: H
-  // per lane), all loads issued before any is used; -1 marks no entry
-  int cc[kRowsPerWave][H];
+  for (int b = wave; b < Bp; b += NW)
+    for (int x = lane; x < rlen[b]; x += 64) rowof[roff[b] + x] = uint8_t(b);
+  __syncthreads();
+  // the thread's codes in registers, all loads issued before any is used
+  int cc[G], pos[G];
 #pragma unroll
-  for (int j = 0; j < kRowsPerWave; ++j) {
-    const int b = wave + j * NW;
-    const int len = b < Bp ? rlen[b] : 0;
-    const long long st = b < Bp ? rstart[b] : 0;
-#pragma unroll
-    for (int h = 0; h < H; ++h) {
-      const int e = lane + 64 * h;
-      cc[j][h] = e < len ? p.code[st + e] : -1;
-    }
+  for (int g = 0; g < G; ++g) {
+    cc[g] = -1;  // no entry
+    pos[g] = -1;
   }
 #pragma unroll
-  for (int j = 0; j < kRowsPerWave; ++j)
+  for (int g = 0; g < G; ++g) {
+    if (g * NT >= T) break;
+    const int e = t + g * NT;
+    if (e < T) cc[g] = p.code[seg + rdelta[rowof[e]] + e];
+  }
+  // hot slots into the bitmap, cold columns into the table (their positions
+  // kept for the codes; a hot entry keeps -2, no entry -1)
 #pragma unroll
-    for (int h = 0; h < H; ++h) {
-      const int c = cc[j][h];
-      if (c == -1) continue;
-      if (is_hot(c)) {
-        const int hs = hot_slot(c);
-        atomicOr(&hot[hs >> 5], 1u << (hs & 31));
-      } else if (table_insert(keys, bits, c) < 0) {
-        overflow = 1;
-      }
+  for (int g = 0; g < G; ++g) {
+    if (g * NT >= T) break;
+    const int c = cc[g];
+    if (c == -1) continue;
+    pos[g] = -2;
+    if (is_hot(c)) {
+      const int hs = hot_slot(c);
+      const uint32_t bit = 1u << (hs & 31);
+      if (!(hot[hs >> 5] & bit)) atomicOr(&hot[hs >> 5], bit);
+    } else {
+      pos[g] = table_insert(keys, bits, c);
+      if (pos[g] == -1) overflow = 1;
     }
+  }
   __syncthreads();
-  // cold slots in table order: thread t numbers a contiguous run of positions
-  const int per = tab / NT > 0 ? tab / NT : 1;
-  const int q0 = t * per, q1 = min(q0 + per, tab);
+  // cold slots: thread t numbers the positions t + j NT (a wave reads 64
+  // consecutive words, no bank conflicts), read once and overwritten by the
+  // slot (by the same thread, so no other reads them in between)
+  int kv[PMAX];
   int cnt = 0;
-  for (int q = q0; q < q1; ++q) cnt += keys[q] >= 0;
+#pragma unroll
+  for (int j = 0; j < PMAX; ++j) {
+    kv[j] = t + j * NT < tab ? keys[t + j * NT] : -1;
+    cnt += kv[j] >= 0;
+  }
   int Uc = 0;
   int id = block_scan<NW>(cnt, sc, &Uc);
-  for (int q = q0; q < q1; ++q) {
-    const int key = keys[q];
-    if (key >= 0) {
-      ids[q] = uint16_t(id);
-      p.clist[lbase + id] = key;
+#pragma unroll
+  for (int j = 0; j < PMAX; ++j) {
+    if (kv[j] >= 0) {
+      keys[t + j * NT] = id;
+      p.clist[lbase + id] = kv[j];
       ++id;
     }
   }
@@ -231,24 +266,16 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
   int Uh = 0;
   int hid = block_scan<NW>(__popc(word), sc, &Uh);
   for (uint32_t w = word; w; w &= w - 1) p.hlist[lbase + hid++] = t * 32 + __ffs(w) - 1;
-  __syncthreads();  // ids complete
+  __syncthreads();  // slots complete
+  // the code half of each cold entry's (code, value) pair: a hot entry's code
+  // and every value do not change from round to round and are written once,
+  // at bind
 #pragma unroll
-  for (int j = 0; j < kRowsPerWave; ++j) {
-    const int b = wave + j * NW;
-#pragma unroll
-    for (int h = 0; h < H; ++h) {
-      const int c = cc[j][h];
-      if (c == -1) continue;
-      int out = c;
-      if (!is_hot(c)) {
-        const int pos = table_find(keys, bits, c);
-        out = pos >= 0 ? int(ids[pos]) : 0;
-      }
-      // the code half of a cold entry's (code, value) pair: a hot entry's
-      // code and every value do not change from round to round and are
-      // written once, at bind
-      if (!is_hot(c)) reinterpret_cast<int*>(p.pack + rstart[b] + lane + 64 * h)[0] = out;
-    }
+  for (int g = 0; g < G; ++g) {
+    if (g * NT >= T) break;
+    const int e = t + g * NT;
+    if (e >= T || pos[g] == -2) continue;  // no entry, or a hot one
+    reinterpret_cast<int*>(p.pack + seg + rdelta[rowof[e]] + e)[0] = pos[g] >= 0 ? keys[pos[g]] : 0;
   }
   if (t == 0) {
     p.cnt[(int64_t(i) * K + k) * 2 + 0] = Uc;
@@ -362,28 +389,24 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   // fuller table overflows into the general kernel, as does a step over
   // kCMax).  Smaller tables keep more blocks resident.
   static_assert((1 << 12) >= 2 * kCMax, "a 2^12-position table holds twice the cold slots");
-  const int64_t most = std::min<int64_t>(2 * int64_t(std::min(p.batch, kFastRows)) * max_row, 2 * kCMax);
-  // rows of at most 64 nonzeros: one per lane and 256 threads (a small
-  // step leaves most of a larger block idle); else two and 512
-  if (max_row <= 64) {
-    if (most <= (1 << 10))
-      hipLaunchKernelGGL((csr_plan_kernel<10, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
-    else if (most <= (1 << 11))
-      hipLaunchKernelGGL((csr_plan_kernel<11, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
-    else
-      hipLaunchKernelGGL((csr_plan_kernel<12, 256, 1>), dim3(blocks), dim3(256), 0, s, p);
-  } else {
-    if (most <= (1 << 10))
-      hipLaunchKernelGGL((csr_plan_kernel<10, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
-    else if (most <= (1 << 11))
-      hipLaunchKernelGGL((csr_plan_kernel<11, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
-    else
-      hipLaunchKernelGGL((csr_plan_kernel<12, kPlanThreads, 2>), dim3(blocks), dim3(kPlanThreads), 0, s, p);
-  }
+  const int64_t most = int64_t(std::min(p.batch, kFastRows)) * max_row;  // nonzeros of a step, at most
+  const int64_t tab = std::min<int64_t>(2 * most, 2 * kCMax);
+  constexpr int NT = kPlanThreads;
+  if (tab <= (1 << 10))
+    hipLaunchKernelGGL((csr_plan_kernel<10, NT, 2>), dim3(blocks), dim3(NT), 0, s, p);
+  else if (tab <= (1 << 11))
+    hipLaunchKernelGGL((csr_plan_kernel<11, NT, 4>), dim3(blocks), dim3(NT), 0, s, p);
+  else if (most <= 8 * NT)
+    hipLaunchKernelGGL((csr_plan_kernel<12, NT, 8>), dim3(blocks), dim3(NT), 0, s, p);
+  else if (most <= 16 * NT)
+    hipLaunchKernelGGL((csr_plan_kernel<12, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
+  else  // twice the threads rather than twice the registers
+    hipLaunchKernelGGL((csr_plan_kernel<12, 2 * NT, 16>), dim3(blocks), dim3(2 * NT), 0, s, p);
+  static_assert(kFastRows * kRowLanes * 8 <= 32 * kPlanThreads, "16 nonzeros per thread of 2 NT cover the longest plannable step");
   if (max_row <= 64)
     hipLaunchKernelGGL(csr_link_kernel<256>, dim3(blocks), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(csr_link_kernel<kPlanThreads>, dim3(blocks), dim3(kPlanThreads), 0, s, p);
+    hipLaunchKernelGGL(csr_link_kernel<512>, dim3(blocks), dim3(512), 0, s, p);
   return hipGetLastError();
 }
 
