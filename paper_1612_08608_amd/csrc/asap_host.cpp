@@ -87,6 +87,7 @@ struct asap_ctx {
   int32_t members_req = 0;   // asap_set_csr_members (0: chosen from the worker and compute-unit counts)
   int32_t max_slice = 0;     // longest row of one member's columns
   int32_t n_mhot[kMaxMembers] = {0, 0, 0, 0};
+  double cold_share = 1.0;   // of the nonzeros, those without a hot slot (sampled at bind)
   uint64_t xseq = 1;         // exchange tag of the next planned step (never reused by a context)
 
   // workspace layout (byte offsets)
@@ -385,6 +386,12 @@ asap_status choose_hot_columns(asap_ctx* c, hipStream_t s) {
       (e = hipStreamSynchronize(s)))
     return hip_fail(c, e, "hot column tables");
   c->n_mhot[0] = int32_t(H);
+  // the share of the sampled nonzeros without a hot slot (of their member's
+  // set when there are several): planning sizes its link kernel by it
+  double all = 0.0, cold = 0.0;
+  for (int32_t j : cols) all += h[j];
+  if (c->members == 1)
+    for (size_t k = H; k < cols.size(); ++k) cold += h[cols[k]];
   if (c->members > 1) {
     // each member keeps the most frequent of its own columns, by the same
     // order
@@ -403,6 +410,7 @@ asap_status choose_hot_columns(asap_ctx* c, hipStream_t s) {
         mhot[size_t(m) * kHotMax + k] = own[k];
         mlut[own[k]] = int16_t(k);
       }
+      for (size_t k = Hm; k < own.size(); ++k) cold += h[own[k]];
       c->n_mhot[m] = int32_t(Hm);
     }
     if ((e = hipMemcpyAsync(at<int32_t>(c, c->off_mhot), mhot.data(), mhot.size() * 4, hipMemcpyHostToDevice, s)) ||
@@ -410,6 +418,7 @@ asap_status choose_hot_columns(asap_ctx* c, hipStream_t s) {
         (e = hipStreamSynchronize(s)))
       return hip_fail(c, e, "member hot column tables");
   }
+  c->cold_share = all > 0.0 ? cold / all : 0.0;
   return ASAP_OK;
 }
 
@@ -985,6 +994,11 @@ PlanArgs plan_args(asap_ctx* c, const asap_sgd_params* p, const RoundPlan& rp, c
   pa.workers = c->n;
   pa.max_slice = c->max_slice;
   pa.n_cu = c->n_cu;
+  // cold nonzeros of a slice's step, on average
+  const double rows = double(c->n) * double(c->S);
+  pa.cold_step = rows > 0.0 ? int32_t(std::min(double(p->batch) * double(c->nnz) / rows * c->cold_share / c->members,
+                                               double(1 << 30)))
+                            : 0;
   pa.mhot = split ? ::at<int32_t>(c, c->off_mhot) : ::at<int32_t>(c, c->off_hot);
   for (int m = 0; m < kMaxMembers; ++m) pa.n_mhot[m] = m < c->members ? c->n_mhot[m] : 0;
   pa.xch = split ? ::at<unsigned long long>(c, c->off_xch) : nullptr;

@@ -125,6 +125,7 @@ struct PlanArgs {
   int32_t workers;          // real workers
   int32_t max_slice;        // longest row of one member's columns
   int32_t n_cu;             // compute units of the device
+  int32_t cold_step;        // cold nonzeros of a slice's step, on average (a sampled estimate)
   const int32_t* mhot;      // [members][kHotMax] column of each member's hot slot
   int32_t n_mhot[4];        // hot slots of each member
   unsigned long long* xch;  // [workers][2][members][64][2] tagged halves of partial margins (step parity 2nd)

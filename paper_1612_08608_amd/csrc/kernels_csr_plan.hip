@@ -44,8 +44,6 @@ using namespace csr;
 constexpr int kHotWords = (kHotMax + 31) / 32;
 
 constexpr int kPlanThreads = 256;
-constexpr int kLinkBits = 12;
-constexpr int kLinkTab = 1 << kLinkBits;     // link hash positions (>= 2 kCMax)
 
 __device__ __forceinline__ uint32_t mult_hash(int c, int bits) {
   return (uint32_t(c) * 2654435761u) >> (32 - bits);
@@ -147,7 +145,8 @@ __global__ __launch_bounds__(kScanThreads) void step_scan_kernel(PlanArgs p) {
 // The step's T nonzeros are numbered in row order and dealt to the threads
 // flat (thread t takes e = t, t + NT, ...: every lane busy whatever the row
 // lengths); an LDS byte per nonzero names its row.  TB: LDS for 2^TB table
-// positions (a step uses the smallest power of two >= 2 T, at most 2^TB).
+// positions (a step uses the smallest power of two >= twice its cold
+// nonzeros, from 2^6 up to 2^TB).
 // G: nonzeros per thread, G NT >= the step's most (rows x longest row).
 template <int TB, int NT, int G>
 __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
@@ -162,6 +161,7 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
   __shared__ int rdelta[kFastRows];  // row start - worker start - roff
   __shared__ uint8_t rowof[G * NT];
   __shared__ int overflow;
+  __shared__ int ncold;  // the step's cold nonzeros
   const int K = p.K, B = p.batch;
   const int i = int(blockIdx.x) / K, k = int(blockIdx.x) % K;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -180,10 +180,6 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
     }
     return;
   }
-  // a table of at least twice the step's nonzeros (at most 2^TB)
-  int bits = 8;
-  while (bits < TB && (1 << bits) < 2 * T) ++bits;
-  const int tab = 1 << bits;
   if (wave == 0) {
     // rows' offsets in the step's numbering: an inclusive scan over lanes
     int len = 0;
@@ -203,9 +199,11 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
     rlen[lane] = len;
     rdelta[lane] = int(st - seg) - (x - len);
   }
-  for (int q = t; q < tab; q += NT) keys[q] = -1;
   for (int q = t; q < kHotWords; q += NT) hot[q] = 0u;
-  if (t == 0) overflow = 0;
+  if (t == 0) {
+    overflow = 0;
+    ncold = 0;
+  }
   __syncthreads();
   for (int b = wave; b < Bp; b += NW)
     for (int x = lane; x < rlen[b]; x += 64) rowof[roff[b] + x] = uint8_t(b);
@@ -223,6 +221,21 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
     const int e = t + g * NT;
     if (e < T) cc[g] = p.code[seg + rdelta[rowof[e]] + e];
   }
+  // a table of at least twice the step's cold nonzeros (at most 2^TB
+  // positions; a step's distinct cold columns are usually far fewer than its
+  // nonzeros, most of which have hot slots)
+  int mine = 0;
+#pragma unroll
+  for (int g = 0; g < G; ++g) mine += cc[g] != -1 && !is_hot(cc[g]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o, 64);
+  if (lane == 0) atomicAdd(&ncold, mine);
+  __syncthreads();
+  int bits = 6;
+  while (bits < TB && (1 << bits) < 2 * ncold) ++bits;
+  const int tab = 1 << bits;
+  for (int q = t; q < tab; q += NT) keys[q] = -1;
+  __syncthreads();
   // hot slots into the bitmap, cold columns into the table (their positions
   // kept for the codes; a hot entry keeps -2, no entry -1)
 #pragma unroll
@@ -285,39 +298,74 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
 }
 
 // ----------------------------------------------------------------------------
-// links: slot of each cold column of step k in step k-1, or -1
+// links: slot of each cold column of step k in step k-1, or -1; a block
+// takes R consecutive steps of one worker and loads the first PER NT entries
+// of the R + 1 lists it needs at once (any further ones where they are used).
+// TB: tables of up to 2^TB positions (2^11 hold every slot; 2^12 keep the
+// probes of the fullest lists short)
 // ----------------------------------------------------------------------------
-template <int NT>
+template <int NT, int R, int PER, int TB>
 __global__ __launch_bounds__(NT) void csr_link_kernel(PlanArgs p) {
-  __shared__ int keys[kLinkTab];
-  __shared__ int vals[kLinkTab];
-  const int K = p.K;
-  const int i = int(blockIdx.x) / K, k = int(blockIdx.x) % K;
+  static_assert((1 << TB) >= kCMax, "a link table holds every cold slot of a step");
+  __shared__ int keys[1 << TB];
+  __shared__ uint16_t vals[1 << TB];  // slots < kCMax
+  const int K = p.K, KB = (K + R - 1) / R;
+  const int i = int(blockIdx.x) / KB, k0 = (int(blockIdx.x) % KB) * R;
   const int t = threadIdx.x;
   const int64_t S = p.S;
   const int64_t seg = p.row_ptr[int64_t(i) * S];
   const int32_t* so = p.step_off + int64_t(i) * (S + 1);
-  const int Uc = min(p.cnt[(int64_t(i) * K + k) * 2], kCMax);
-  const int64_t lbase = seg + so[k];
-  const int Up = k > 0 ? min(p.cnt[(int64_t(i) * K + k - 1) * 2], kCMax) : 0;
-  if (Uc == 0) return;
-  // a table of at least four times the previous step's columns (at most
-  // 2^kLinkBits, twice kCMax)
-  int bits = 6;
-  while (bits < kLinkBits && (1 << bits) < 4 * Up) ++bits;
-  for (int q = t; q < (1 << bits); q += NT) keys[q] = -1;
-  __syncthreads();
-  if (k > 0) {
-    const int64_t pbase = seg + so[k - 1];
-    for (int u = t; u < Up; u += NT) {
-      const int pos = table_insert(keys, bits, p.clist[pbase + u]);
-      if (pos >= 0) vals[pos] = u;  // columns are distinct within a step
-    }
+  // entry r is step k0 + r - 1
+  int U[R + 1];
+  int64_t base[R + 1];
+  int col[R + 1][PER];
+#pragma unroll
+  for (int r = 0; r <= R; ++r) {
+    const int k = k0 + r - 1;
+    U[r] = k >= 0 && k < K ? min(p.cnt[(int64_t(i) * K + k) * 2], kCMax) : 0;
+    base[r] = seg + (U[r] ? so[k] : 0);
   }
-  __syncthreads();
-  for (int u = t; u < Uc; u += NT) {
-    const int pos = k > 0 ? table_find(keys, bits, p.clist[lbase + u]) : -1;
-    p.clink[lbase + u] = pos >= 0 ? vals[pos] : -1;
+#pragma unroll
+  for (int r = 0; r <= R; ++r)
+#pragma unroll
+    for (int j = 0; j < PER; ++j) col[r][j] = t + j * NT < U[r] ? p.clist[base[r] + t + j * NT] : -1;
+#pragma unroll
+  for (int r = 1; r <= R; ++r) {
+    const int Uc = U[r], Up = U[r - 1];
+    if (Uc == 0) continue;  // uniform: every thread skips the step
+    if (Up == 0) {  // no previous step, or one without cold columns
+      for (int u = t; u < Uc; u += NT) p.clink[base[r] + u] = -1;
+      continue;
+    }
+    // a table of at least twice the previous step's columns, at most 2^TB
+    // positions (linear probing holds up to that many)
+    int bits = 6;
+    while (bits < TB && (1 << bits) < 2 * Up) ++bits;
+    __syncthreads();  // the previous step's lookups are done
+    for (int q = t; q < (1 << bits); q += NT) keys[q] = -1;
+    __syncthreads();
+    // columns are distinct within a step
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      if (col[r - 1][j] < 0) continue;
+      const int pos = table_insert(keys, bits, col[r - 1][j]);
+      if (pos >= 0) vals[pos] = uint16_t(t + j * NT);
+    }
+    for (int u = t + PER * NT; u < Up; u += NT) {
+      const int pos = table_insert(keys, bits, p.clist[base[r - 1] + u]);
+      if (pos >= 0) vals[pos] = uint16_t(u);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      if (col[r][j] < 0) continue;
+      const int pos = table_find(keys, bits, col[r][j]);
+      p.clink[base[r] + t + j * NT] = pos >= 0 ? int(vals[pos]) : -1;
+    }
+    for (int u = t + PER * NT; u < Uc; u += NT) {
+      const int pos = table_find(keys, bits, p.clist[base[r] + u]);
+      p.clink[base[r] + u] = pos >= 0 ? int(vals[pos]) : -1;
+    }
   }
 }
 
@@ -383,30 +431,44 @@ bool csr_plan_fits(const SgdArgs& a) {
 hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   const uint32_t blocks = uint32_t(int64_t(p.n) * p.K);
   hipLaunchKernelGGL(step_scan_kernel, dim3(uint32_t(p.n)), dim3(kScanThreads), 0, s, p);
-  // the largest step holds at most batch * max_row nonzeros; the table
+  // the largest step holds at most batch * max_row nonzeros.  Its table
   // holds its distinct cold columns, of which a plan that the pass can take
-  // has at most kCMax, so 2 kCMax positions (TB = 12) always suffice (a
-  // fuller table overflows into the general kernel, as does a step over
-  // kCMax).  Smaller tables keep more blocks resident.
-  static_assert((1 << 12) >= 2 * kCMax, "a 2^12-position table holds twice the cold slots");
+  // has at most kCMax: 2^11 positions hold them all (linear probing fills a
+  // table completely; a fuller step overflows into the general kernel, as
+  // does a step over kCMax), and a step uses twice its cold nonzeros, so
+  // that the probes stay short in all but the fullest steps.  Small tables
+  // keep more blocks resident, also beside a pass that fills the device.
+  static_assert((1 << 11) >= kCMax, "a 2^11-position table holds every cold slot");
   const int64_t most = int64_t(std::min(p.batch, kFastRows)) * max_row;  // nonzeros of a step, at most
-  const int64_t tab = std::min<int64_t>(2 * most, 2 * kCMax);
   constexpr int NT = kPlanThreads;
-  if (tab <= (1 << 10))
+  if (most <= 2 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<10, NT, 2>), dim3(blocks), dim3(NT), 0, s, p);
-  else if (tab <= (1 << 11))
+  else if (most <= 4 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 4>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 8 * NT)
-    hipLaunchKernelGGL((csr_plan_kernel<12, NT, 8>), dim3(blocks), dim3(NT), 0, s, p);
+    hipLaunchKernelGGL((csr_plan_kernel<11, NT, 8>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 16 * NT)
-    hipLaunchKernelGGL((csr_plan_kernel<12, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
-  else  // twice the threads rather than twice the registers
+    hipLaunchKernelGGL((csr_plan_kernel<11, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
+  else if (p.cold_step <= 768)  // twice the threads rather than twice the registers
+    hipLaunchKernelGGL((csr_plan_kernel<11, 2 * NT, 16>), dim3(blocks), dim3(2 * NT), 0, s, p);
+  else  // and a table of 2^12 positions for steps with many cold columns
     hipLaunchKernelGGL((csr_plan_kernel<12, 2 * NT, 16>), dim3(blocks), dim3(2 * NT), 0, s, p);
   static_assert(kFastRows * kRowLanes * 8 <= 32 * kPlanThreads, "16 nonzeros per thread of 2 NT cover the longest plannable step");
-  if (max_row <= 64)
-    hipLaunchKernelGGL(csr_link_kernel<256>, dim3(blocks), dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL(csr_link_kernel<512>, dim3(blocks), dim3(512), 0, s, p);
+  // steps whose lists (at most their cold nonzeros, estimated) fit one
+  // entry per thread with some margin: 8 steps per block, the lists' heads
+  // loaded at once; else 4 steps, whole lists, in tables of 2^12 positions
+  // for lists of more than 768 entries
+  static_assert(kCMax % 256 == 0, "whole lists in registers");
+  if (p.cold_step <= 192) {
+    const uint32_t lb = uint32_t(int64_t(p.n) * ((p.K + 7) / 8));
+    hipLaunchKernelGGL((csr_link_kernel<256, 8, 1, 11>), dim3(lb), dim3(256), 0, s, p);
+  } else {
+    const uint32_t lb = uint32_t(int64_t(p.n) * ((p.K + 3) / 4));
+    if (p.cold_step <= 768)
+      hipLaunchKernelGGL((csr_link_kernel<256, 4, kCMax / 256, 11>), dim3(lb), dim3(256), 0, s, p);
+    else
+      hipLaunchKernelGGL((csr_link_kernel<256, 4, kCMax / 256, 12>), dim3(lb), dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 
