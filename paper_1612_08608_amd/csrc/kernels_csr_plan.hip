@@ -226,7 +226,10 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
   // nonzeros, most of which have hot slots)
   int mine = 0;
 #pragma unroll
-  for (int g = 0; g < G; ++g) mine += cc[g] != -1 && !is_hot(cc[g]);
+  for (int g = 0; g < G; ++g) {
+    if (g * NT >= T) break;
+    mine += cc[g] != -1 && !is_hot(cc[g]);
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o, 64);
   if (lane == 0) atomicAdd(&ncold, mine);
@@ -302,11 +305,11 @@ __global__ __launch_bounds__(NT) void csr_plan_kernel(PlanArgs p) {
 // takes R consecutive steps of one worker and loads the first PER NT entries
 // of the R + 1 lists it needs at once (any further ones where they are used).
 // TB: tables of up to 2^TB positions (2^11 hold every slot; 2^12 keep the
-// probes of the fullest lists short)
+// probes of the fullest lists short; with 2^10, a list that does not fit
+// raises the flag, and the general kernel runs the round)
 // ----------------------------------------------------------------------------
 template <int NT, int R, int PER, int TB>
 __global__ __launch_bounds__(NT) void csr_link_kernel(PlanArgs p) {
-  static_assert((1 << TB) >= kCMax, "a link table holds every cold slot of a step");
   __shared__ int keys[1 << TB];
   __shared__ uint16_t vals[1 << TB];  // slots < kCMax
   const int K = p.K, KB = (K + R - 1) / R;
@@ -335,6 +338,10 @@ __global__ __launch_bounds__(NT) void csr_link_kernel(PlanArgs p) {
     if (Uc == 0) continue;  // uniform: every thread skips the step
     if (Up == 0) {  // no previous step, or one without cold columns
       for (int u = t; u < Uc; u += NT) p.clink[base[r] + u] = -1;
+      continue;
+    }
+    if (Up > (1 << TB)) {  // uniform; never when 2^TB >= kCMax
+      if (t == 0) atomicOr(p.flag, 1);
       continue;
     }
     // a table of at least twice the previous step's columns, at most 2^TB
@@ -437,7 +444,10 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   // table completely; a fuller step overflows into the general kernel, as
   // does a step over kCMax), and a step uses twice its cold nonzeros, so
   // that the probes stay short in all but the fullest steps.  Small tables
-  // keep more blocks resident, also beside a pass that fills the device.
+  // keep more blocks resident, also beside a pass that fills the device:
+  // where steps have few cold nonzeros (estimated at bind), 2^10 positions,
+  // five times the estimate (a step with more distinct cold columns than
+  // that overflows into the general kernel).
   static_assert((1 << 11) >= kCMax, "a 2^11-position table holds every cold slot");
   const int64_t most = int64_t(std::min(p.batch, kFastRows)) * max_row;  // nonzeros of a step, at most
   constexpr int NT = kPlanThreads;
@@ -447,6 +457,8 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 4>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 8 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 8>), dim3(blocks), dim3(NT), 0, s, p);
+  else if (most <= 16 * NT && p.cold_step <= 192)  // small tables: three blocks fit beside a 512-thread pass
+    hipLaunchKernelGGL((csr_plan_kernel<10, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 16 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
   else if (p.cold_step <= 768)  // twice the threads rather than twice the registers
@@ -456,12 +468,12 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   static_assert(kFastRows * kRowLanes * 8 <= 32 * kPlanThreads, "16 nonzeros per thread of 2 NT cover the longest plannable step");
   // steps whose lists (at most their cold nonzeros, estimated) fit one
   // entry per thread with some margin: 8 steps per block, the lists' heads
-  // loaded at once; else 4 steps, whole lists, in tables of 2^12 positions
-  // for lists of more than 768 entries
+  // loaded at once, tables of 2^10 positions; else 4 steps, whole lists, in
+  // tables of 2^12 positions for lists of more than 768 entries
   static_assert(kCMax % 256 == 0, "whole lists in registers");
   if (p.cold_step <= 192) {
     const uint32_t lb = uint32_t(int64_t(p.n) * ((p.K + 7) / 8));
-    hipLaunchKernelGGL((csr_link_kernel<256, 8, 1, 11>), dim3(lb), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((csr_link_kernel<256, 8, 1, 10>), dim3(lb), dim3(256), 0, s, p);
   } else {
     const uint32_t lb = uint32_t(int64_t(p.n) * ((p.K + 3) / 4));
     if (p.cold_step <= 768)
