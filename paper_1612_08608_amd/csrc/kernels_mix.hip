@@ -50,6 +50,19 @@ __device__ __forceinline__ uint32_t xcd_tile(uint32_t bid, uint32_t total) {
   return (bid % 8u) * (total / 8u) + bid / 8u;
 }
 
+// Non-temporal 16-byte accesses, for data a reduce reads or writes exactly
+// once (the slab kernel's staging loads and result stores): 4-5% faster
+// than plain accesses for 1024 x 2^20 models.
+typedef float nt4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 ld_nt(const float4* p) {
+  const nt4 x = __builtin_nontemporal_load(reinterpret_cast<const nt4*>(p));
+  return make_float4(x.x, x.y, x.z, x.w);
+}
+__device__ __forceinline__ void st_nt(float4* p, const float4& v) {
+  const nt4 x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<nt4*>(p));
+}
+
 __device__ __forceinline__ void fma4(float4& acc, float w, const float4& x) {
   acc.x = fmaf(w, x.x, acc.x);
   acc.y = fmaf(w, x.y, acc.y);
@@ -325,7 +338,7 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
     for (int m = 0; m < kSlabPF; ++m) {
       const bool in = live && off + 4 * (q0 + sq(m)) < a.dim;
       const char* base = reinterpret_cast<const char*>(a.src + off + int64_t(srow(m)) * a.ld + 4 * sq(m));
-      buf[m] = in ? *reinterpret_cast<const float4*>(base + vo) : make_float4(0.f, 0.f, 0.f, 0.f);
+      buf[m] = in ? ld_nt(reinterpret_cast<const float4*>(base + vo)) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   auto stage = [&](const float4 (&buf)[kSlabPF]) {
@@ -422,7 +435,7 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
             if ((okm >> (lane - lane_in + k)) & 1) {
               float* d = a.dst + int64_t(row_base + k) * a.ld + c;
               if (full) {
-                *reinterpret_cast<float4*>(d) = res[k];
+                st_nt(reinterpret_cast<float4*>(d), res[k]);
               } else {
                 store_partial(d, res[k], k_tail);
               }
