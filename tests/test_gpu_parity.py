@@ -256,6 +256,15 @@ def test_csr_members_against_the_oracle(torch, case, members):
         _free_run(torch, wl, "random", 8, 3, loss_curve=True, members=members)
 
 
+def test_csr_long_steps_with_many_cold_columns(torch):
+    # one workgroup per worker over 64-row steps of Poisson(80) rows on 2^20
+    # columns: up to 64 x 114 nonzeros and about 1400 distinct cold columns
+    # per step, so planning takes 512-thread blocks and tables of 2^12
+    # positions, and links hold whole lists
+    wl = synth.SPARSE_LR_64W.with_(n_workers=8, samples=2048)
+    _free_run(torch, wl, "random", 4, 3, loss_curve=True, members=1)
+
+
 def test_csr_small_batch_pass_on_a_full_device(torch):
     # 160 workers with minibatches of 32 rows fill the device: the planned
     # pass runs 512-thread workgroups (32 rows of 16 lanes), so that the next
