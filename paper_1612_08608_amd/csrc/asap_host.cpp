@@ -10,6 +10,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -86,6 +87,9 @@ struct asap_ctx {
   int32_t members = 1;
   int32_t members_req = 0;   // asap_set_csr_members (0: chosen from the worker and compute-unit counts)
   int32_t max_slice = 0;     // longest row of one member's columns
+  // step_most[b]: the most nonzeros b rows of one slice hold (the b longest
+  // rows of the fullest slice), b <= kPlanStepRows: what one planned step holds
+  std::vector<int32_t> step_most;
   int32_t n_mhot[kMaxMembers] = {0, 0, 0, 0};
   double cold_share = 1.0;   // of the nonzeros, those without a hot slot (sampled at bind)
   uint64_t xseq = 1;         // exchange tag of the next planned step (never reused by a context)
@@ -426,10 +430,45 @@ asap_status choose_hot_columns(asap_ctx* c, hipStream_t s) {
 // each member's columns, slice v = worker * members + member, laid out one
 // after another) and every nonzero's code in slice order.  One member: the
 // slices are the workers.
+// step_most from the row lengths of every slice ([slices][S], in slice order).
+void set_step_most(asap_ctx* c, const std::vector<int32_t>& len, int64_t slices) {
+  c->step_most.assign(kPlanStepRows + 1, 0);
+  std::vector<int32_t> top;
+  for (int64_t v = 0; v < slices; ++v) {
+    top.assign(len.begin() + v * c->S, len.begin() + (v + 1) * c->S);
+    const int64_t b = std::min<int64_t>(kPlanStepRows, c->S);
+    std::partial_sort(top.begin(), top.begin() + b, top.end(), std::greater<int32_t>());
+    int32_t acc = 0;
+    for (int64_t q = 0; q < b; ++q) {
+      acc += top[size_t(q)];
+      c->step_most[size_t(q + 1)] = std::max(c->step_most[size_t(q + 1)], acc);
+    }
+  }
+  for (int q = 1; q <= kPlanStepRows; ++q) c->step_most[q] = std::max(c->step_most[q], c->step_most[q - 1]);
+}
+
+// The most nonzeros one planned step of `batch` rows can hold.
+int64_t step_bound(const asap_ctx* c, int32_t batch) {
+  const int32_t b = std::min<int32_t>(batch, kPlanStepRows);
+  if (size_t(b) < c->step_most.size()) return c->step_most[size_t(b)];
+  return int64_t(b) * c->max_slice;  // not measured: rows times the longest row
+}
+
 asap_status split_members(asap_ctx* c, hipStream_t s) {
   c->max_slice = c->max_row;
-  if (c->members == 1) return ASAP_OK;
   hipError_t e;
+  if (c->members == 1) {
+    // the rows' lengths, for the bound on a step's nonzeros
+    const size_t rows = size_t(c->n) * size_t(c->S);
+    std::vector<int64_t> rp(rows + 1);
+    if ((e = hipMemcpyAsync(rp.data(), c->row_ptr, (rows + 1) * 8, hipMemcpyDeviceToHost, s)) ||
+        (e = hipStreamSynchronize(s)))
+      return hip_fail(c, e, "row offsets readback");
+    std::vector<int32_t> len(rows);
+    for (size_t q = 0; q < rows; ++q) len[q] = int32_t(rp[q + 1] - rp[q]);
+    set_step_most(c, len, c->n);
+    return ASAP_OK;
+  }
   const int32_t M = c->members;
   const size_t rows = size_t(c->n) * size_t(M) * size_t(c->S);
   // the counts (int32) go to the slice-offset array first, which the
@@ -451,6 +490,7 @@ asap_status split_members(asap_ctx* c, hipStream_t s) {
   vrp[rows] = acc;
   if (acc != c->nnz) return fail(c, ASAP_E_INVALID_ARG, "member split counted %lld of %lld nonzeros",
                                  (long long)acc, (long long)c->nnz);
+  set_step_most(c, h, int64_t(c->n) * M);
   int64_t* d_vrp = at<int64_t>(c, c->off_vrp);
   if ((e = hipMemcpyAsync(d_vrp, vrp.data(), (rows + 1) * 8, hipMemcpyHostToDevice, s)) ||
       (e = launch_member_scatter(c->row_ptr, c->col, c->val, at<int16_t>(c, c->off_mlut), c->n, c->S, M, d_vrp,
@@ -1044,7 +1084,7 @@ hipError_t prepare_csr_round(asap_ctx* c, const asap_sgd_params* p, int64_t roun
       e = launch_rowinfo(sched, pa.row_ptr, c->y, c->n, c->S, reinterpret_cast<RowInfo*>(base + rp.vrowinfo), s,
                          c->members);
     if (e == hipSuccess) e = launch_fill_i32(pa.flag, 1, 0, s);
-    if (e == hipSuccess) e = launch_csr_plan(pa, c->max_slice, s);
+    if (e == hipSuccess) e = launch_csr_plan(pa, step_bound(c, p->batch), s);
   }
   return e;
 }

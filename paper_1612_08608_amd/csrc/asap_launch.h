@@ -136,7 +136,10 @@ struct PlanArgs {
 };
 constexpr int kMaxMembers = 4;
 bool csr_plan_fits(const SgdArgs& a);
-hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s);
+// Rows of a planned CSR step, at most (the planned pass's minibatch limit).
+constexpr int kPlanStepRows = 64;
+// most: the most nonzeros one step of a slice can hold
+hipError_t launch_csr_plan(const PlanArgs& p, int64_t most, hipStream_t s);
 // pack[q] = (code[q], bits of val[q]) for every nonzero: the round-invariant
 // part of the plan (the planning kernel rewrites the cold entries' codes)
 hipError_t launch_pack_values(const int32_t* code, const float* val, int64_t nnz, int2* pack, hipStream_t s);

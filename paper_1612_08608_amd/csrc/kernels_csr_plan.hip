@@ -44,6 +44,7 @@ using namespace csr;
 constexpr int kHotWords = (kHotMax + 31) / 32;
 
 constexpr int kPlanThreads = 256;
+static_assert(kPlanStepRows == kFastRows, "the host bounds steps of the planned pass's rows");
 
 __device__ __forceinline__ uint32_t mult_hash(int c, int bits) {
   return (uint32_t(c) * 2654435761u) >> (32 - bits);
@@ -435,10 +436,11 @@ bool csr_plan_fits(const SgdArgs& a) {
   return a.batch <= kFastRows && a.max_row <= kRowLanes * 8 && a.n_hot <= kHotMax;
 }
 
-hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
+hipError_t launch_csr_plan(const PlanArgs& p, int64_t most, hipStream_t s) {
   const uint32_t blocks = uint32_t(int64_t(p.n) * p.K);
   hipLaunchKernelGGL(step_scan_kernel, dim3(uint32_t(p.n)), dim3(kScanThreads), 0, s, p);
-  // the largest step holds at most batch * max_row nonzeros.  Its table
+  // `most` bounds a step's nonzeros (the longest rows of the fullest slice,
+  // found at bind; never more than batch * longest row).  A step's table
   // holds its distinct cold columns, of which a plan that the pass can take
   // has at most kCMax: 2^11 positions hold them all (linear probing fills a
   // table completely; a fuller step overflows into the general kernel, as
@@ -449,15 +451,16 @@ hipError_t launch_csr_plan(const PlanArgs& p, int max_row, hipStream_t s) {
   // five times the estimate (a step with more distinct cold columns than
   // that overflows into the general kernel).
   static_assert((1 << 11) >= kCMax, "a 2^11-position table holds every cold slot");
-  const int64_t most = int64_t(std::min(p.batch, kFastRows)) * max_row;  // nonzeros of a step, at most
   constexpr int NT = kPlanThreads;
   if (most <= 2 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<10, NT, 2>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 4 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 4>), dim3(blocks), dim3(NT), 0, s, p);
+  else if (most <= 8 * NT && p.cold_step <= 192)  // small tables: more blocks fit beside a 512-thread pass
+    hipLaunchKernelGGL((csr_plan_kernel<10, NT, 8>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 8 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 8>), dim3(blocks), dim3(NT), 0, s, p);
-  else if (most <= 16 * NT && p.cold_step <= 192)  // small tables: three blocks fit beside a 512-thread pass
+  else if (most <= 16 * NT && p.cold_step <= 192)
     hipLaunchKernelGGL((csr_plan_kernel<10, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 16 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
