@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "asap.h"
+
 namespace asap {
 
 // Epoch tags: 2r = "models of round r at the start of the round",

@@ -48,7 +48,7 @@ __device__ __forceinline__ void lds_barrier() {
 // in fp64; the logistic factor 1 / (1 + e^{y m}) needs only fp32 accuracy.
 __device__ __forceinline__ double loss_coef(double m, double y, int loss) {
   const double ym = y * m;
-  if (loss == 1) return ym < 1.0 ? -y : 0.0;
+  if (loss == ASAP_LOSS_HINGE) return ym < 1.0 ? -y : 0.0;
   return -y / double(1.0f + expf(float(ym)));
 }
 

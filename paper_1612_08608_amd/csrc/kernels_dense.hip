@@ -56,8 +56,8 @@ constexpr int kMaxBatch = 512;  // minibatch limit of asap_sgd_params
 // in fp64; the logistic factor 1 / (1 + e^{y m}) needs only fp32 accuracy.
 __device__ __forceinline__ float loss_coef(double m, float y, int loss) {
   const double ym = double(y) * m;
-  if (loss == 1) return ym < 1.0 ? -y : 0.f;  // hinge
-  return -y / (1.f + expf(float(ym)));         // logistic
+  if (loss == ASAP_LOSS_HINGE) return ym < 1.0 ? -y : 0.f;
+  return -y / (1.f + expf(float(ym)));  // logistic
 }
 
 __device__ __forceinline__ double step_size(int lr_kind, float lr0, int64_t t) {

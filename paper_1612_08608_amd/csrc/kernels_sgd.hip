@@ -20,16 +20,13 @@
 namespace asap {
 namespace {
 
-constexpr int kLogistic = 0;
-constexpr int kHinge = 1;
-
 // d loss(y m) / d m: logistic -y / (1 + e^{y m}); hinge -y if y m < 1 else 0.
 // Margins are accumulated in fp64 (a 4096-term fp32 dot product with a
 // wide dynamic range loses more than the 1e-5 the models are held to), and
 // the coefficient -- including the hinge decision -- is taken in fp64.
 __device__ __forceinline__ double loss_coef(double m, double y, int loss) {
   const double ym = y * m;
-  if (loss == kHinge) return ym < 1.0 ? -y : 0.0;
+  if (loss == ASAP_LOSS_HINGE) return ym < 1.0 ? -y : 0.0;
   return -y / (1.0 + exp(ym));
 }
 
