@@ -452,6 +452,9 @@ hipError_t launch_csr_plan(const PlanArgs& p, int64_t most, hipStream_t s) {
   // that overflows into the general kernel).
   static_assert((1 << 11) >= kCMax, "a 2^11-position table holds every cold slot");
   constexpr int NT = kPlanThreads;
+  // the pass of several members per worker takes at most half the compute
+  // units: planning then runs beside it on the others
+  const bool beside = p.members > 1 && int64_t(p.workers) * p.members * 2 <= p.n_cu;
   if (most <= 2 * NT)
     hipLaunchKernelGGL((csr_plan_kernel<10, NT, 2>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 4 * NT)
@@ -462,9 +465,13 @@ hipError_t launch_csr_plan(const PlanArgs& p, int64_t most, hipStream_t s) {
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 8>), dim3(blocks), dim3(NT), 0, s, p);
   else if (most <= 16 * NT && p.cold_step <= 192)
     hipLaunchKernelGGL((csr_plan_kernel<10, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
-  else if (most <= 16 * NT)
+  else if (most <= 16 * NT && !beside)
     hipLaunchKernelGGL((csr_plan_kernel<11, NT, 16>), dim3(blocks), dim3(NT), 0, s, p);
-  else if (p.cold_step <= 768)  // twice the threads rather than twice the registers
+  // beyond 16 nonzeros per thread, or beside a pass on compute units of its
+  // own, twice the threads (planning beside 64 workers x 2 members in
+  // 512-thread blocks: the pass 2.34 -> 2.30 ms; alone, 256-thread blocks
+  // plan faster)
+  else if (p.cold_step <= 768)
     hipLaunchKernelGGL((csr_plan_kernel<11, 2 * NT, 16>), dim3(blocks), dim3(2 * NT), 0, s, p);
   else  // and a table of 2^12 positions for steps with many cold columns
     hipLaunchKernelGGL((csr_plan_kernel<12, 2 * NT, 16>), dim3(blocks), dim3(2 * NT), 0, s, p);
