@@ -431,25 +431,25 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
     }
     lds_barrier();
     // prefetch: nonzeros, links, hot slots and values of k+1, row and
-    // columns of k+2.  The loads whose results the next step's prefetch
-    // needs (metadata, rows, columns) go first and the random model gathers
-    // last, so that waiting for the former (loads complete in order) does
-    // not wait for the gathers.  With one member it is issued here, after
-    // the barrier, so that the address work of some waves overlaps the LDS
-    // work of others (256 workers: pass 0.96 -> 0.94 ms with this order);
-    // members issue it after their exchange, whose polls (vector loads) would
-    // otherwise wait for it (64 workers x 2 members: pass 2.30 -> 2.22 ms).
-    auto prefetch = [&]() {
-      m3 = load_meta(so_v, cn_v, k + 3, lane);
-      r2 = load_row(a, ri, k + 2, kend, brow);
-      load_cols(m2, cl2);
-      load_packed<E>(pk, w.seg, r1, row_valid(a, k + 1, kend, brow), sub, d1);
-      load_links(m1, lk1);
-      load_hot(m1, hl1);
+    // columns of k+2, issued here, after the barrier, so that the address
+    // work of some waves overlaps the LDS work of others.  The loads whose
+    // results the next step's prefetch needs (metadata, rows, columns) go
+    // first and the random model gathers last, so that waiting for the
+    // former (loads complete in order) does not wait for the gathers (256
+    // workers: pass 0.96 -> 0.94 ms with this order).  Members issue the
+    // gathers after their exchange, whose polls (vector loads) would
+    // otherwise wait for them (64 workers x 2 members: pass 2.30 -> 2.12 ms).
+    m3 = load_meta(so_v, cn_v, k + 3, lane);
+    r2 = load_row(a, ri, k + 2, kend, brow);
+    load_cols(m2, cl2);
+    load_packed<E>(pk, w.seg, r1, row_valid(a, k + 1, kend, brow), sub, d1);
+    load_links(m1, lk1);
+    load_hot(m1, hl1);
+    auto gather_next = [&]() {
       gather(m1, cl1, g1);
-      asm volatile("" ::: "memory");  // keep the prefetch issued here, ahead of the LDS work
+      asm volatile("" ::: "memory");  // keep the gathers issued here, ahead of the LDS work
     };
-    if constexpr (!MEM) prefetch();
+    if constexpr (!MEM) gather_next();
 
     // one LDS read per entry, its address chosen by the code (a read per
     // branch would serialise on the shared destination register); all reads
@@ -469,7 +469,7 @@ __device__ void fast_pass(const SgdArgs& a, const PlanArgs& p, int i, int m, Fas
     if constexpr (MEM)
       dot = member_exchange(p, xr, m, brow, lane, a.xtag + uint32_t(a.round * K + k - a.xg0), dot,
                             row_valid(a, k, kend, brow), local, sh);
-    if constexpr (MEM) prefetch();
+    if constexpr (MEM) gather_next();
     const double cf = (d0.ok & kRowExists) ? loss_coef(s * dot, double(d0.y), a.loss) : 0.0;
     if (cf != 0.0) {
 #pragma unroll
