@@ -6,12 +6,12 @@
 // It is bound by HBM bandwidth (arithmetic intensity < 1 flop/byte), so MFMA
 // has no role here.  What matters is that every model byte crosses HBM once.
 //
-// slab kernel (n a power of two in [8, 1024], rows of at most 17 entries): one
-// 512-thread workgroup per CU owns a contiguous range of column chunks; a
-// chunk holds all n rows of a column range (128 KiB above 512 rows, so that
-// it holds a whole 128-byte line of every row; else 64 KiB) and is staged in
-// LDS, so each neighbour re-read is an LDS read.  The loads of the next
-// chunk (two with 64 KiB chunks) are in flight while one is computed.  A
+// slab kernel (n a power of two in [8, 1024], rows of at most 17 entries):
+// each workgroup owns a contiguous range of column chunks; a chunk holds all
+// n rows of a column range, sized so that it holds a whole 128-byte line of
+// every row (128 KiB above 512 rows, 64 KiB above 256, else 32 KiB), and is
+// staged in LDS, so each neighbour re-read is an LDS read.  The loads of the
+// next chunk (two below 1024 rows) are in flight while one is computed.  A
 // thread keeps the neighbour lists of its output rows in registers (two
 // weights per row when all of a row's entries but its own share one weight).
 // LDS slots of a row are XOR-swizzled by the row's low bits so that lanes
@@ -237,7 +237,7 @@ __device__ __forceinline__ void store_partial(float* d, float4 v, int k) {
 // LDS reads in flight per thread
 template <int DEG, int R> constexpr int slab_group() { return DEG <= 5 ? DEG : (R == 2 && DEG > 9 ? 1 : 4); }
 
-// Slab kernel.  One THREADS-thread workgroup per CU walks a contiguous
+// Slab kernel.  A THREADS-thread workgroup walks a contiguous
 // range of column chunks; a chunk is all n rows of 4 VEC / n columns (VEC
 // float4), staged in LDS.  Thread t stages float4 slots t + THREADS m of the
 // chunk (m < VEC / THREADS); NBUF register buffers keep the loads of the
@@ -261,6 +261,7 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
   const int X = min(Q, 8) - 1;               // swizzle mask
   const int tid = threadIdx.x;
   constexpr int OPR = kSlabPF / R;           // outputs per row per thread per chunk
+  static_assert(OPR >= kOut && OPR % kOut == 0, "mix_slab_kernel: whole groups of transposed outputs");
   constexpr int G = slab_group<DEG, R>();
   // this thread's output rows and first float4
   int orow[R];
@@ -318,7 +319,7 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
   const int per = (nchunks + int(gridDim.x) - 1) / int(gridDim.x);
   const int ch0 = int(blockIdx.x) * per, ch1 = min(nchunks, ch0 + per);
 
-  // Staging: slot s = tid + 512 m of a chunk is float4 s mod Q of row s div
+  // Staging: slot s = tid + THREADS m of a chunk is float4 s mod Q of row s div
   // Q.  The per-thread part of the address is a 32-bit byte offset below
   // 2^31 (the launcher checks it); the rest is wave-uniform.
   const int lq = __builtin_ctz(Q);
@@ -514,18 +515,23 @@ namespace {
 // and rows of at most 17 entries
 bool slab_graph(int n, int max_deg) { return n >= 8 && n <= 1024 && !(n & (n - 1)) && max_deg <= 17; }
 
-// per-thread staging offset (rows below 512/Q, float4 slots below Q) and
-// chunk count within 31 bits
-constexpr int kSlabThreads = 512;
-// chunk size (float4): 128 KiB above 512 rows, so that a chunk holds a whole
-// 128-byte line of every row, else 64 KiB (shorter chunks pipeline better
-// when each CU has only a few of them)
-int slab_vec(int n) { return n > 512 ? 8192 : 4096; }
+// Shapes: above 256 rows one 512-thread workgroup per CU with a 128 KiB
+// (above 512 rows) or 64 KiB chunk; up to 256 rows 256-thread workgroups
+// with 32 KiB chunks, up to four per CU.  Every chunk holds a whole 128-byte
+// line of every row (Q >= 8 float4).  Small workgroups leave room on a CU for
+// the kernels that plan the next round beside the reduce: 256 workers x
+// 2^18, random 8-regular: reduce 0.32 -> 0.29 ms, round 1.36 -> 1.32 ms.
+int slab_threads(int n) { return n > 256 ? 512 : 256; }
+int slab_vec(int n) { return n > 512 ? 8192 : n > 256 ? 4096 : 2048; }
+int slab_per_cu(int n) { return n > 256 ? 1 : 4; }
 
+// per-thread staging offset (rows below THREADS/Q, float4 slots below Q) and
+// chunk count within 31 bits
 bool slab_fits(const MixArgs& a) {
+  const int T = slab_threads(a.n);
   const int Q = slab_vec(a.n) / a.n, C = 4 * Q;
-  const int rows = Q > kSlabThreads ? 1 : kSlabThreads / Q;
-  if ((int64_t(rows - 1) * a.ld + 4 * int64_t(std::min(Q, kSlabThreads))) * 4 >= (int64_t(1) << 31)) return false;
+  const int rows = Q > T ? 1 : T / Q;
+  if ((int64_t(rows - 1) * a.ld + 4 * int64_t(std::min(Q, T))) * 4 >= (int64_t(1) << 31)) return false;
   return (a.dim + C - 1) / C < (int64_t(1) << 31);
 }
 }  // namespace
@@ -539,18 +545,23 @@ hipError_t launch_slab(const MixArgs& a, int n_cu, hipStream_t s) {
   if (!slab_fits(a)) return hipErrorNotSupported;
   const int C = 4 * (slab_vec(a.n) / a.n);
   const int nchunks = int((a.dim + C - 1) / C);
-  const int grid = std::max(1, std::min(nchunks, n_cu));
-  const dim3 g(grid), b(kSlabThreads);
+  const int grid = std::max(1, std::min(nchunks, slab_per_cu(a.n) * n_cu));
+  const dim3 g(grid), b(slab_threads(a.n));
   if (a.n > 512) {
     if (a.uniform_rows)
-      hipLaunchKernelGGL((mix_slab_kernel<DEG, 2, kSlabThreads, 1, 8192, true>), g, b, 0, s, a, nchunks);
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 2, 512, 1, 8192, true>), g, b, 0, s, a, nchunks);
     else
-      hipLaunchKernelGGL((mix_slab_kernel<DEG, 2, kSlabThreads, 1, 8192, false>), g, b, 0, s, a, nchunks);
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 2, 512, 1, 8192, false>), g, b, 0, s, a, nchunks);
+  } else if (a.n > 256) {
+    if (a.uniform_rows)
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, 512, 2, 4096, true>), g, b, 0, s, a, nchunks);
+    else
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, 512, 2, 4096, false>), g, b, 0, s, a, nchunks);
   } else {
     if (a.uniform_rows)
-      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, kSlabThreads, 2, 4096, true>), g, b, 0, s, a, nchunks);
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, 256, 2, 2048, true>), g, b, 0, s, a, nchunks);
     else
-      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, kSlabThreads, 2, 4096, false>), g, b, 0, s, a, nchunks);
+      hipLaunchKernelGGL((mix_slab_kernel<DEG, 1, 256, 2, 2048, false>), g, b, 0, s, a, nchunks);
   }
   return hipGetLastError();
 }
