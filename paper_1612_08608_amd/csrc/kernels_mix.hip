@@ -151,7 +151,10 @@ __global__ __launch_bounds__(64) void mean_kernel(MixArgs a, uint32_t nseg) {
   if (c < a.dim) {
     const double w0 = a.nbr_w[0];
     Acc4 acc;
-#pragma unroll 8
+    // 32 rows' loads in flight per wave (one wave per segment leaves few
+    // waves on a CU): 256 workers x 2^18 beside the next round's planning,
+    // 0.32 -> 0.24 ms; the order of the sum is unchanged
+#pragma unroll 32
     for (int j = 0; j < a.n; ++j) {
       double wt = w0;
       if (a.scale) wt *= double(a.scale[j]);
