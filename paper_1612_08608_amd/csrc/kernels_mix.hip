@@ -421,6 +421,33 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
   uint64_t okmask[R];
 #pragma unroll
   for (int rr = 0; rr < R; ++rr) okmask[rr] = __ballot(ok[rr]);
+  // one transposed group of 8 outputs: rows row_base + k, columns from c
+  auto store_group = [&](const float4 (&res)[kOut], int64_t c, int row_base, uint64_t okm) {
+    if (c < a.dim) {
+      const bool full = c + 4 <= a.dim;
+      const int k_tail = int(min<int64_t>(a.dim - c, 4));
+#pragma unroll
+      for (int k = 0; k < kOut; ++k) {
+        if ((okm >> (lane - lane_in + k)) & 1) {
+          float* d = a.dst + int64_t(row_base + k) * a.ld + c;
+          if (full) {
+            st_nt(reinterpret_cast<float4*>(d), res[k]);
+          } else {
+            store_partial(d, res[k], k_tail);
+          }
+        }
+      }
+    }
+  };
+  // With two output rows per thread and up to 5 entries per row, the second
+  // row's group is held back and stored after the next chunk's loads are
+  // issued, so that the wait for those loads at the next staging does not
+  // also wait for these stores to drain (1024 x 2^20: d = 2 1.745 -> 1.714
+  // ms, d = 4 1.772 -> 1.755 ms; with 9 entries the extra registers made
+  // d = 8 slower).
+  constexpr bool kDefer = R == 2 && DEG <= 5 && OPR == kOut;
+  float4 pend[kDefer ? kOut : 1];
+  int64_t pend_c = -1;
   auto compute = [&](int ch) {
     // one row at a time (R = 2: the second row's state is selected in, not
     // kept beside the first's while its outputs are computed)
@@ -436,22 +463,20 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
         for (int u = 0; u < kOut; ++u) res[u] = slab_row(oq0 + h * kOut + u);
         transpose8(res, lane_in);
         const int64_t c = int64_t(ch) * C + 4 * (oq0 + h * kOut + lane_in);
-        if (c < a.dim) {
-          const bool full = c + 4 <= a.dim;
-          const int k_tail = int(min<int64_t>(a.dim - c, 4));
+        if (kDefer && rr == R - 1) {
 #pragma unroll
-          for (int k = 0; k < kOut; ++k) {
-            if ((okm >> (lane - lane_in + k)) & 1) {
-              float* d = a.dst + int64_t(row_base + k) * a.ld + c;
-              if (full) {
-                st_nt(reinterpret_cast<float4*>(d), res[k]);
-              } else {
-                store_partial(d, res[k], k_tail);
-              }
-            }
-          }
+          for (int u = 0; u < (kDefer ? kOut : 1); ++u) pend[u] = res[u];
+          pend_c = c;
+        } else {
+          store_group(res, c, row_base, okm);
         }
       }
+    }
+  };
+  auto flush = [&]() {
+    if constexpr (kDefer) {
+      if (pend_c >= 0) store_group(pend, pend_c, orow[R - 1] & ~(kOut - 1), okmask[R - 1]);
+      pend_c = -1;
     }
   };
   if constexpr (NBUF == 2) {
@@ -480,8 +505,10 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
       stage(bufA);
       lds_barrier();
       load(bufA, ch + 1);
+      flush();
       compute(ch);
     }
+    flush();
   }
   if (blockIdx.x == 0) {
     const bool head = R == 2 || tid < n;
