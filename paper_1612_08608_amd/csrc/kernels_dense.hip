@@ -387,16 +387,31 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
       for (int q = 0; q < CPQ; ++q)
 #pragma unroll
         for (int e = 0; e < 4; ++e) g[q][e] = 0.0;
-      for (int m = 0; m < K; ++m) {
+      // the partials of 8 members at a time are loaded before any is added,
+      // in member order (32 workers x 4096, 8 members: 7.14 -> 7.01 ms per
+      // pass against a load-add chain per member)
+      typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+      for (int m0 = 0; m0 < K; m0 += 8) {
+        u4v pu[8][CPQ];
 #pragma unroll
-        for (int q = 0; q < CPQ; ++q) {
-          const uint32_t off = uint32_t((m * ds.ldp + (q * kThreads + tid) * 4) * 4);
-          const auto u = __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, 16);  // sc1: device scope
-          const unsigned u0 = u[0], u1 = u[1], u2 = u[2], u3 = u[3];
-          g[q][0] += double(__uint_as_float(u0));
-          g[q][1] += double(__uint_as_float(u1));
-          g[q][2] += double(__uint_as_float(u2));
-          g[q][3] += double(__uint_as_float(u3));
+        for (int mm = 0; mm < 8; ++mm)
+#pragma unroll
+          for (int q = 0; q < CPQ; ++q) {
+            const int m = m0 + mm < K ? m0 + mm : m0;
+            const uint32_t off = uint32_t((m * ds.ldp + (q * kThreads + tid) * 4) * 4);
+            pu[mm][q] = __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, 16);  // sc1: device scope
+          }
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm) {
+          if (m0 + mm >= K) break;
+#pragma unroll
+          for (int q = 0; q < CPQ; ++q) {
+            const unsigned u0 = pu[mm][q][0], u1 = pu[mm][q][1], u2 = pu[mm][q][2], u3 = pu[mm][q][3];
+            g[q][0] += double(__uint_as_float(u0));
+            g[q][1] += double(__uint_as_float(u1));
+            g[q][2] += double(__uint_as_float(u2));
+            g[q][3] += double(__uint_as_float(u3));
+          }
         }
       }
     }
