@@ -387,9 +387,11 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
       for (int q = 0; q < CPQ; ++q)
 #pragma unroll
         for (int e = 0; e < 4; ++e) g[q][e] = 0.0;
-      // the partials of 8 members at a time are loaded before any is added,
-      // in member order (32 workers x 4096, 8 members: 7.14 -> 7.01 ms per
-      // pass against a load-add chain per member)
+      // the members' partials in blocks of 8, unrolled, added in member
+      // order (32 workers x 4096, 8 members: 7.14 -> 7.01 ms per pass against
+      // a rolled loop over the members; the compiler still issues the loads
+      // two at a time beside the adds, and holding four members' loads in
+      // flight at once gained nothing)
       typedef unsigned int u4v __attribute__((ext_vector_type(4)));
       for (int m0 = 0; m0 < K; m0 += 8) {
         u4v pu[8][CPQ];
