@@ -443,8 +443,9 @@ __global__ __launch_bounds__(THREADS) void mix_slab_kernel(MixArgs a, int nchunk
   // row's group is held back and stored after the next chunk's loads are
   // issued, so that the wait for those loads at the next staging does not
   // also wait for these stores to drain (1024 x 2^20: d = 2 1.745 -> 1.714
-  // ms, d = 4 1.772 -> 1.755 ms; with 9 entries the extra registers made
-  // d = 8 slower).
+  // ms, d = 4 1.772 -> 1.755 ms; with 9 entries, holding the whole group or
+  // half of it made d = 8 slower: its longer neighbour sums let the stores
+  // drain anyway).
   constexpr bool kDefer = R == 2 && DEG <= 5 && OPR == kOut;
   float4 pend[kDefer ? kOut : 1];
   int64_t pend_c = -1;
