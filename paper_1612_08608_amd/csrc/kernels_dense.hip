@@ -287,11 +287,23 @@ __device__ __forceinline__ bool dense_wide_pass(const SgdArgs& a, const DenseSyn
     lds_barrier();
     float cf = 0.f;
     if (lane < SR && lane < p.hi - p.sb) {
+      // the partials of two waves are read before they are added (in wave and
+      // row order, as one chain would): one LDS round trip per 8 partials
+      // instead of per 2 (32 workers x 4096: 7.01 -> 6.88 ms per pass; four
+      // waves at a time gained nothing more)
       double m = 0.0;
 #pragma unroll
-      for (int v = 0; v < kWaves; ++v)
+      for (int v0 = 0; v0 < kWaves; v0 += 2) {
+        double tv[2][4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) m += red[par][v][r][lane];
+        for (int v = 0; v < 2; ++v)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tv[v][r] = red[par][v0 + v][r][lane];
+#pragma unroll
+        for (int v = 0; v < 2; ++v)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) m += tv[v][r];
+      }
       cf = loss_coef(m, yl, a.loss);
     }
     par ^= 1;
